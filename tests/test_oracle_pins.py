@@ -1,0 +1,281 @@
+"""Pins of the oracle against the mathematics of the paper's formulation
+(Section 4.2) and solver (Section 4.3), on seeded random tiny instances.
+
+Each check uses something other than the oracle's own code: numpy library
+routines (bincount, reshape-sum, stable argsort), the constraints C1-C5, the
+objective of Eqs. 5-8 evaluated on dense arrays, brute-force optima and an
+independent enumerator of refinement candidates.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from planmodel import (Topo, best_candidate, brute_force_opt_no_compute, check_constraints,
+                       cross_domain_assignments, domain_demand, enumerate_candidates, loads,
+                       objective, stage1_best_benefit)
+
+
+def random_instance(seed, R=None, G=None, P=None, N=None, k=None, big=False):
+    """A tiny instance whose every rank's top-k array is simulated."""
+    rng = np.random.default_rng(seed)
+    if G is None:
+        G = int(rng.choice([1, 2, 3, 4]))
+    if R is None:
+        R = G * int(rng.choice([1, 2, 3]))
+    if P is None:
+        P = int(rng.choice([1, 2, 3]))
+    E = R * P
+    if N is None:
+        N = int(rng.integers(0, 4))
+    if k is None:
+        k = int(rng.integers(1, min(E, 3) + 1))
+    cI = int(rng.integers(0, 3))
+    cX = int(rng.integers(cI, 7))
+    S = int(rng.integers(1, 5))
+    # skewed popularity, some experts hot
+    pop = rng.dirichlet(np.full(E, 0.3))
+    topks = []
+    for s in range(R):
+        T = int(rng.integers(0, 40 if big else 14))
+        ids = rng.choice(E, size=(T, k), p=pop).astype(np.int32)
+        topks.append(ids)
+    omega = np.stack([np.bincount(t.ravel(), minlength=E) for t in topks]).astype(np.int32)
+    Dmax = max(1, int(domain_demand(Topo(R, G, E, cI, cX, S, 0, N), omega).max()))
+    W = int(rng.integers(0, 2 * S * Dmax + 2))
+    t = Topo(R, G, E, cI, cX, S, W, N)
+    return t, omega, topks
+
+
+def run(t, omega, topk, self_rank, **kw):
+    topo = oracle.topology(t.R, t.G, t.E, self_rank, t.cI, t.cX, t.S, t.W)
+    return oracle.plan_ref(topo, omega, topk, t.N, **kw)
+
+
+SEEDS = list(range(60))
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_histogram_and_demand(seed):
+    t, omega, topks = random_instance(seed)
+    s = seed % t.R
+    out = run(t, omega, topks[s], s, debug=True, move_cap=1000)
+    assert out["status"] == 0
+    assert (out["hist"] == np.bincount(topks[s].ravel(), minlength=t.E)).all()
+    D = domain_demand(t, omega)
+    assert (out["demand"] == D).all()
+    assert (D.sum(axis=0) == omega.sum(axis=0)).all()
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_stage1_placement(seed):
+    """Inter-node placement (Eq. 9): greedy sum of b is the subset optimum, the
+    ranks follow 'least occupied rank with a free slot', C3-C5 hold."""
+    t, omega, topks = random_instance(seed, N=int(np.random.default_rng(seed).integers(0, 3)))
+    out = run(t, omega, topks[0], 0, debug=True, move_cap=1000)
+    x1 = out["x_stage1"].astype(bool)
+    D = domain_demand(t, omega)
+    mains = np.zeros_like(x1)
+    mains[np.arange(t.E), np.arange(t.E) // t.P] = True
+    reps = x1 & ~mains
+    for d in range(t.M):
+        ranks = range(d * t.G, (d + 1) * t.G)
+        chosen = [e for e in range(t.E) if reps[e, list(ranks)].any()]
+        # at most one replica per (domain, expert), only remote mains with b > 0
+        for e in chosen:
+            assert reps[e, list(ranks)].sum() == 1
+            assert t.dom(t.main(e)) != d
+            assert 2 * int(D[d, e]) * t.S - t.W > 0
+        total_b = sum(2 * int(D[d, e]) * t.S - t.W for e in chosen)
+        assert total_b == stage1_best_benefit(t, D, d)
+        # closed form of 'fewest used slots, ties to the lowest rank': the i-th
+        # chosen candidate in (b desc, e asc) order lands on rank dG + i mod G,
+        # slot i div G
+        order = sorted(chosen, key=lambda e: (-(2 * int(D[d, e]) * t.S - t.W), e))
+        for i, e in enumerate(order):
+            r = d * t.G + i % t.G
+            assert reps[e, r]
+            assert out["replica_slots"][r, i // t.G] == e
+    check_constraints(t, omega, x1, out["q_routed"])
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_routing_construction(seed):
+    """Routing after stage 1: C1/C2, same-domain preference, even split with
+    the remainder on the lowest ranks."""
+    t, omega, topks = random_instance(seed)
+    out = run(t, omega, topks[0], 0, debug=True, move_cap=1000)
+    x1 = out["x_stage1"].astype(bool)
+    q = out["q_routed"].astype(np.int64)
+    check_constraints(t, omega, x1, q)
+    for s in range(t.R):
+        for e in range(t.E):
+            w = int(omega[s, e])
+            hosts = np.nonzero(x1[e])[0]
+            local = [r for r in hosts if t.dom(r) == t.dom(s)]
+            sel = local if local else list(hosts)
+            got = q[s, e]
+            assert got[[r for r in range(t.R) if r not in sel]].sum() == 0
+            share = got[sel]
+            n = len(sel)
+            assert share.tolist() == [w // n + (1 if i < w % n else 0) for i in range(n)]
+    assert (loads(q) == out["load_routed"]).all()
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_refinement_steps(seed):
+    """Replay every committed move of the intra-node refinement (Eq. 10)
+    against an independent enumerator: the chosen candidate is the key
+    minimum, its split is a minimum-cost split, its cost change equals the
+    change of Eqs. 6-7, and the invariants of Section 4.3 hold."""
+    rng = np.random.default_rng(1000 + seed)
+    t, omega, topks = random_instance(1000 + seed, N=int(rng.integers(1, 4)), big=True)
+    out = run(t, omega, topks[0], 0, debug=True, move_cap=10000)
+    assert out["n_moves"] <= 10000
+    x = out["x_stage1"].astype(bool).copy()
+    q = out["q_routed"].astype(np.int64).copy()
+    mains = np.zeros_like(x)
+    mains[np.arange(t.E), np.arange(t.E) // t.P] = True
+    used = (x & ~mains).sum(axis=0)
+    cross0 = cross_domain_assignments(t, q)
+    D = domain_demand(t, omega)
+    i = 0
+    for d in range(t.M):
+        for _ in range(int(out["iters"][d])):
+            dd, rb, rt, e, delta, created = out["moves"][i].tolist()
+            assert dd == d
+            avail = [int(q[s, e, rb]) for s in range(t.R)]
+            small = np.prod([a + 1 for a in avail], dtype=float) <= 5000
+            rb_e, cands = enumerate_candidates(t, x, q, used, d, brute_split=small)
+            assert rb_e == rb
+            best = best_candidate(cands)
+            assert best is not None
+            assert (best["e"], best["rt"], best["delta"], best["hosts"]) == (e, rt, delta, not created)
+            m = out["move_m"][i].astype(np.int64)
+            assert m.tolist() == best["m"]
+            assert m.sum() == delta and (m >= 0).all()
+            L_pre = loads(q)
+            pre = objective(t, x, q)
+            if created:
+                assert not x[e, rt] and used[rt] < t.N
+                x[e, rt] = True
+                used[rt] += 1
+            q[:, e, rb] -= m
+            q[:, e, rt] += m
+            post = objective(t, x, q)
+            assert post - pre == int(out["move_dcost"][i]) == best["dcost"]
+            L = loads(q)
+            assert L[rb] >= L[rt]                                  # order not reversed
+            assert (L.astype(np.int64) ** 2).sum() < (L_pre.astype(np.int64) ** 2).sum()
+            assert cross_domain_assignments(t, q) == cross0        # no new cross-domain routes
+            check_constraints(t, omega, x, q, D)
+            i += 1
+        # stop rule: the busiest rank of the domain has no candidate left
+        _, cands = enumerate_candidates(t, x, q, used, d, brute_split=False)
+        assert best_candidate(cands) is None
+    assert i == out["n_moves"]
+    assert (q == out["q_final"]).all()
+    assert (x == out["x_final"].astype(bool)).all()
+    assert (loads(q) == out["load_final"]).all()
+
+
+def _stable_dest(t, topk, q_self):
+    """Destinations by the stable-argsort construction: occurrences of each
+    expert in row-major order, sliced by the per-instance counts in ascending
+    rank order."""
+    ids = topk.ravel()
+    dest = np.full(ids.size, -1, np.int64)
+    order = np.argsort(ids, kind="stable")
+    start = 0
+    for e in range(t.E):
+        cnt = int((ids == e).sum())
+        seq = np.repeat(np.arange(t.R), q_self[e].astype(np.int64))
+        assert seq.size == cnt
+        dest[order[start:start + cnt]] = seq
+        start += cnt
+    return dest.reshape(topk.shape)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_rerouting_and_cross_rank(seed):
+    """Every rank derives the same replica slots; each rank's destinations
+    follow the stable construction; send counts add up to the rank loads."""
+    t, omega, topks = random_instance(2000 + seed, big=True)
+    slots0 = None
+    total = np.zeros(t.R, np.int64)
+    for s in range(t.R):
+        out = run(t, omega, topks[s], s, debug=True, move_cap=10000)
+        assert out["status"] == 0
+        if slots0 is None:
+            slots0 = out["replica_slots"].copy()
+            L = out["load_final"]
+        assert (out["replica_slots"] == slots0).all()
+        q_self = out["q_final"][s]
+        dest = out["token_dest"]
+        assert (dest == _stable_dest(t, topks[s], q_self)).all()
+        assert (np.bincount(dest.ravel(), minlength=t.R) == out["send_counts"]).all()
+        assert out["send_counts"].sum() == topks[s].size
+        # every destination hosts its expert
+        xf = out["x_final"].astype(bool)
+        assert xf[topks[s].ravel(), dest.ravel()].all() if dest.size else True
+        total += out["send_counts"]
+    assert (total == L).all()
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_static_ep_without_slots(seed):
+    """N = 0: no replicas, every assignment goes to its expert's main."""
+    t, omega, topks = random_instance(3000 + seed, N=0)
+    out = run(t, omega, topks[0], 0)
+    assert (out["replica_slots"].size == 0)
+    assert (out["token_dest"] == topks[0] // t.P).all()
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_single_domain_has_no_stage1(seed):
+    """M = 1: every main is inside the only domain, stage 1 places nothing."""
+    rng = np.random.default_rng(seed)
+    G = int(rng.choice([2, 3, 4]))
+    t, omega, topks = random_instance(4000 + seed, R=G, G=G, N=int(rng.integers(1, 3)))
+    out = run(t, omega, topks[0], 0, debug=True, move_cap=1000)
+    x1 = out["x_stage1"].astype(bool)
+    assert x1.sum() == t.E
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_one_gpu_per_node_reaches_the_optimum(seed):
+    """G = 1 and t_FFN = 0: refinement has nothing to do and the plan's
+    objective (Eqs. 6-8) equals the brute-force optimum over all placements."""
+    rng = np.random.default_rng(5000 + seed)
+    R = int(rng.choice([2, 3]))
+    P = 1 if R == 3 else int(rng.choice([1, 2]))
+    t, omega, topks = random_instance(5000 + seed, R=R, G=1, P=P, N=int(rng.integers(0, 2)))
+    out = run(t, omega, topks[0], 0, debug=True, move_cap=1000)
+    assert out["n_moves"] == 0
+    got = objective(t, out["x_final"], out["q_final"])
+    assert got == brute_force_opt_no_compute(t, omega)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_balanced_static_plan_is_kept(seed):
+    """Equal rank loads and no profitable replica: the plan is static EP,
+    which is optimal (L_max equals the mean, no transfer)."""
+    rng = np.random.default_rng(6000 + seed)
+    G = int(rng.choice([1, 2, 4]))
+    R = G * int(rng.choice([1, 2]))
+    P = int(rng.choice([1, 2]))
+    E = R * P
+    per = int(rng.integers(1, 6))
+    omega = np.zeros((R, E), np.int32)
+    # every source sends 'per' assignments to each expert of its own rank only
+    for s in range(R):
+        omega[s, s * P:(s + 1) * P] = per
+    S = 2
+    W = 2 * per * G * S  # b <= 0 for every remote (d, e): D <= per * G
+    t = Topo(R, G, E, 1, 3, S, W, int(rng.integers(0, 3)))
+    topk = np.repeat(np.arange(P, dtype=np.int32), per).reshape(-1, 1)
+    out = run(t, omega, topk, 0, debug=True, move_cap=100)
+    assert (out["replica_slots"] == -1).all()
+    assert out["n_moves"] == 0
+    assert objective(t, out["x_final"], out["q_final"]) == 0
