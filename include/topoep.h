@@ -1,0 +1,164 @@
+/*
+ * topoep.h -- C ABI of the TopoEP per-layer planner on one MI355X (gfx950).
+ *
+ * The planner turns one EP rank's routing result into a topology-aware plan
+ * (TopoEP, Sections 3.1 and 4):
+ *   1. the per-expert histogram of the rank's top-k ids, which is this
+ *      rank's row of the routing matrix Omega (Eq. 3);
+ *   2. the domain demand D (Eq. 4) and inter-node replica placement driven by
+ *      the benefit b = 2 D S_tok - ||W_e|| (Section 4.3, Eq. 9);
+ *   3. routing construction q, U, L (Section 4.3) and intra-node refinement
+ *      with the transfer amount of Eq. 10;
+ *   4. rerouting of every (token, k) assignment to an expert instance, and
+ *      per-destination send counts (the q[self][e][r] of Section 4.2 expanded
+ *      to assignments).
+ *
+ * Conventions shared by every entry point:
+ *   - All counts are int32; all arrays are row-major and densely packed.
+ *   - "device" pointers are HIP device memory of the current device; the
+ *     caller owns every buffer (inputs, outputs, workspace).  The library
+ *     keeps no state between calls and never allocates or frees device
+ *     memory during a call.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is only enqueued: a call returns before the GPU finishes, with no
+ *     host-device synchronisation and no device-to-host copy, so an enqueue
+ *     may be captured in a HIP graph.  Outputs are valid once the stream
+ *     reaches them.
+ *   - One workspace serves one plan at a time: plans that share a workspace
+ *     must be ordered on one stream.
+ *   - main(e) = e / (E/R) (main instances spread contiguously and evenly,
+ *     Section 3.2); dom(r) = r / G.  Cost c(s,r) = 0 if s == r, cost_intra
+ *     inside a domain, cost_inter across domains (a two-level instance of
+ *     the symmetric cost matrix C of Section 4.1).
+ */
+#ifndef TOPOEP_H
+#define TOPOEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* System model of Section 4.1, passed by host pointer and copied into the
+ * kernel arguments. */
+typedef struct topoep_topology {
+  int32_t num_ranks;      /* R > 0                                              */
+  int32_t ranks_per_node; /* G > 0, G divides R (G <= 64)                       */
+  int32_t num_experts;    /* E > 0, R divides E                                 */
+  int32_t self_rank;      /* rank whose local_topk is passed, 0 <= self < R     */
+  int32_t cost_intra;     /* c(s,r) for s != r in one domain, >= 0              */
+  int32_t cost_inter;     /* c(s,r) across domains, >= 0                        */
+  int64_t tok_bytes;      /* S_tok, bytes of one routed activation, > 0         */
+  int64_t expert_bytes;   /* ||W_e||, bytes of one expert (all equal), >= 0     */
+} topoep_topology;
+
+/* Optional launch shape.  Every valid shape gives bitwise-identical results;
+ * it only changes speed.  NULL selects the default. */
+typedef struct topoep_launch {
+  int32_t items_per_thread; /* 1, 2, 4 or 8 ids per thread per tile              */
+  int32_t block_threads;    /* 64..1024, multiple of 64, for histogram/reroute    */
+  int32_t tiles_per_block;  /* >= 1; 0 = choose from the problem size             */
+  int32_t solve_threads;    /* 64..1024, multiple of 64, for the solver           */
+} topoep_launch;
+
+/* Host return codes. */
+#define TOPOEP_OK 0
+#define TOPOEP_EINVAL (-1)     /* bad argument (see topoep_plan)                   */
+#define TOPOEP_EWORKSPACE (-2) /* workspace smaller than required, or misaligned  */
+#define TOPOEP_EHIP (-3)       /* a HIP launch failed (hipGetLastError)            */
+#define TOPOEP_ELIMIT (-4)     /* per-domain solver state exceeds on-chip memory  */
+
+/* Device status bits, written by the plan into *status. */
+#define TOPOEP_ST_BAD_ID 1u      /* an id of local_topk is outside [0, E)            */
+#define TOPOEP_ST_NEG_LOAD 2u    /* global_load holds a negative entry               */
+#define TOPOEP_ST_SELF_DIFF 4u   /* global_load[self] differs from the histogram of  */
+                                 /* local_topk (informational: the plan always uses  */
+                                 /* the histogram as row self of Omega)              */
+#define TOPOEP_ST_RANGE 8u       /* sum of loads > INT32_MAX, or                     */
+                                 /* 4 S total max(c,1) + max(c,1) W >= 2^62, so the  */
+                                 /* integer cost terms would not be exact            */
+#define TOPOEP_ST_SYNC 16u       /* a bounded in-kernel wait gave up (outputs wrong) */
+#define TOPOEP_ST_ITER 32u       /* refinement hit its iteration bound               */
+/* With BAD_ID, NEG_LOAD or RANGE no plan is made: replica_slots = -1,
+ * send_counts = 0, token_dest = -1. */
+
+/*
+ * Bytes of device workspace topoep_plan needs for these sizes (default
+ * launch shape).  Returns TOPOEP_OK, TOPOEP_EINVAL for invalid sizes, or
+ * TOPOEP_ELIMIT when one domain's solver state cannot fit in LDS.
+ */
+int topoep_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k,
+                           int32_t replica_budget, size_t *bytes_out);
+
+/* Same for an explicit launch shape (NULL = default). */
+int topoep_workspace_bytes_ex(const topoep_topology *topo, int32_t T, int32_t k,
+                              int32_t replica_budget, const topoep_launch *launch,
+                              size_t *bytes_out);
+
+/*
+ * Enqueue one plan (Sections 3.1 and 4.3).
+ *
+ *   global_load    device int32 [R, E]: Omega as the EP all-gather delivers
+ *                  it (row s = assignments of rank s per expert).  Row
+ *                  self_rank is replaced by the histogram of local_topk.
+ *   local_topk     device int32 [T, k]: this rank's top-k expert ids.  May be
+ *                  NULL when T == 0.  Duplicate ids in one token count
+ *                  independently.
+ *   replica_budget N_slot >= 0 replica slots per rank (Section 4.1).  Budgets
+ *                  above E - E/R are legal; the extra slots stay empty.
+ *   replica_slots  device int32 out [R, N_slot]: slot j of rank r holds the
+ *                  expert of the j-th replica created on r (inter-node
+ *                  placement first, then refinement in commit order), -1 if
+ *                  empty.
+ *   token_dest     device int32 out [T, k]: the rank that executes each
+ *                  assignment.  The rho-th occurrence (row-major) of expert e
+ *                  goes to instance r_i, instances of e with a nonzero share
+ *                  of this rank's assignments in ascending rank, where
+ *                  sum_{j<i} q[self][e][r_j] <= rho < sum_{j<=i} q[self][e][r_j].
+ *                  May be NULL when T == 0.
+ *   send_counts    device int32 out [R]: sum_e q[self][e][r].
+ *   status         device int32 out [1]: TOPOEP_ST_* bits.
+ *   workspace      device memory of at least topoep_workspace_bytes bytes,
+ *                  256-byte aligned; its contents need no initialisation and
+ *                  are overwritten.
+ *
+ * Host checks (TOPOEP_EINVAL): null pointers; R <= 0; G <= 0 or G does not
+ * divide R; R does not divide E; k < 1 or k > E; T < 0 or T * k > INT32_MAX;
+ * N_slot < 0; self_rank outside [0, R); negative costs; S_tok <= 0;
+ * ||W|| < 0.  TOPOEP_ELIMIT: G > 64 or a domain's state exceeds LDS.
+ * TOPOEP_EWORKSPACE: workspace too small or not 256-byte aligned.
+ * TOPOEP_EHIP: a kernel launch failed.
+ */
+int topoep_plan(const topoep_topology *topo, const int32_t *global_load,
+                const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
+                int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts,
+                int32_t *status, void *workspace, size_t workspace_bytes, void *stream);
+
+/* topoep_plan with an explicit launch shape (NULL = default). */
+int topoep_plan_ex(const topoep_topology *topo, const int32_t *global_load,
+                   const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
+                   int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts,
+                   int32_t *status, void *workspace, size_t workspace_bytes, void *stream,
+                   const topoep_launch *launch);
+
+/*
+ * Enqueue a single kernel of the plan, for measurement: stage 0 = histogram
+ * (Eq. 3 row), 1 = solver (Eqs. 4, 9, 10 and routing), 2 = reroute.  The
+ * arguments are those of topoep_plan_ex.  A stage reads the workspace state
+ * the earlier stages left for the same inputs, so a stage may be repeated
+ * after one full plan and gives the same outputs.  TOPOEP_EINVAL for a stage
+ * outside [0, 2].
+ */
+int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t *global_load,
+                      const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
+                      int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts,
+                      int32_t *status, void *workspace, size_t workspace_bytes, void *stream,
+                      const topoep_launch *launch);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TOPOEP_H */

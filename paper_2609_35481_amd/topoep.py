@@ -1,0 +1,187 @@
+"""Thin Python binding of the planner's C ABI (include/topoep.h).
+
+Argument marshalling only: torch provides device memory and the current
+stream; every step of the plan runs in the HIP kernels of libtopoep.so.
+Importing this module fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtopoep.so")
+
+OK = 0
+EINVAL = -1
+EWORKSPACE = -2
+EHIP = -3
+ELIMIT = -4
+
+ST_BAD_ID = 1
+ST_NEG_LOAD = 2
+ST_SELF_DIFF = 4
+ST_RANGE = 8
+ST_SYNC = 16
+ST_ITER = 32
+
+STAGE_HIST = 0
+STAGE_SOLVE = 1
+STAGE_REROUTE = 2
+
+
+class Topology(ctypes.Structure):
+    """topoep_topology: R ranks, G per node, E experts, this rank, costs, S_tok, ||W||."""
+    _fields_ = [("num_ranks", ctypes.c_int32), ("ranks_per_node", ctypes.c_int32),
+                ("num_experts", ctypes.c_int32), ("self_rank", ctypes.c_int32),
+                ("cost_intra", ctypes.c_int32), ("cost_inter", ctypes.c_int32),
+                ("tok_bytes", ctypes.c_int64), ("expert_bytes", ctypes.c_int64)]
+
+
+class Launch(ctypes.Structure):
+    """topoep_launch: launch shape (results do not depend on it)."""
+    _fields_ = [("items_per_thread", ctypes.c_int32), ("block_threads", ctypes.c_int32),
+                ("tiles_per_block", ctypes.c_int32), ("solve_threads", ctypes.c_int32)]
+
+
+class TopoepError(RuntimeError):
+    def __init__(self, fn, rc):
+        super().__init__("%s returned %d" % (fn, rc))
+        self.rc = rc
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libtopoep.so is not built (run __graft_entry__.build() or "
+                      "python -m paper_2609_35481_amd.build): " + LIB_PATH)
+
+_lib = ctypes.CDLL(LIB_PATH)
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_lib.topoep_workspace_bytes_ex.restype = ctypes.c_int
+_lib.topoep_workspace_bytes_ex.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32,
+                                           ctypes.POINTER(Launch), ctypes.POINTER(ctypes.c_size_t)]
+_lib.topoep_workspace_bytes.restype = ctypes.c_int
+_lib.topoep_workspace_bytes.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32,
+                                        ctypes.POINTER(ctypes.c_size_t)]
+_PLAN_ARGS = [ctypes.POINTER(Topology), _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
+              ctypes.c_size_t, _vp]
+_lib.topoep_plan.restype = ctypes.c_int
+_lib.topoep_plan.argtypes = _PLAN_ARGS
+_lib.topoep_plan_ex.restype = ctypes.c_int
+_lib.topoep_plan_ex.argtypes = _PLAN_ARGS + [ctypes.POINTER(Launch)]
+_lib.topoep_plan_stage.restype = ctypes.c_int
+_lib.topoep_plan_stage.argtypes = [_i32] + _PLAN_ARGS + [ctypes.POINTER(Launch)]
+
+EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
+           "topoep_plan_ex", "topoep_plan_stage")
+
+
+def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
+    return Topology(R, G, E, self_rank, c_intra, c_inter, S, W)
+
+
+def _launch_ptr(launch):
+    if launch is None:
+        return None
+    if isinstance(launch, Launch):
+        return ctypes.byref(launch)
+    return ctypes.byref(Launch(*launch))
+
+
+def workspace_bytes(topo: Topology, T: int, k: int, replica_budget: int, launch=None) -> int:
+    out = ctypes.c_size_t(0)
+    rc = _lib.topoep_workspace_bytes_ex(ctypes.byref(topo), T, k, replica_budget,
+                                        _launch_ptr(launch), ctypes.byref(out))
+    if rc != OK:
+        raise TopoepError("topoep_workspace_bytes", rc)
+    return out.value
+
+
+def _dev_i32(t, name, shape=None):
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.int32 or not t.is_cuda:
+        raise TypeError("%s must be a CUDA int32 tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    return t
+
+
+class Planner:
+    """Holds the output tensors and workspace of one (topology, T, k, N)
+    problem so repeated plans allocate nothing (and can be graph-captured)."""
+
+    def __init__(self, topo: Topology, T: int, k: int, replica_budget: int, device=None, launch=None):
+        self.topo = topo
+        self.T, self.k, self.N = int(T), int(k), int(replica_budget)
+        self.launch = launch
+        dev = torch.device(device if device is not None else "cuda")
+        R = topo.num_ranks
+        self.ws_bytes = workspace_bytes(topo, self.T, self.k, self.N, launch)
+        # 256-byte aligned workspace carved from a byte tensor
+        self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+        base = self._ws.data_ptr()
+        self.ws_ptr = (base + 255) & ~255
+        self.replica_slots = torch.empty((R, self.N), dtype=torch.int32, device=dev)
+        self.token_dest = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
+        self.send_counts = torch.empty((R,), dtype=torch.int32, device=dev)
+        self.status = torch.empty((1,), dtype=torch.int32, device=dev)
+
+    def _args(self, global_load, local_topk, stream):
+        R, E = self.topo.num_ranks, self.topo.num_experts
+        _dev_i32(global_load, "global_load", (R, E))
+        if self.T > 0:
+            _dev_i32(local_topk, "local_topk", (self.T, self.k))
+        if stream is None:
+            stream = torch.cuda.current_stream(global_load.device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        return (ctypes.byref(self.topo), global_load.data_ptr(),
+                local_topk.data_ptr() if self.T > 0 else None, self.T, self.k, self.N,
+                self.replica_slots.data_ptr() if self.replica_slots.numel() else None,
+                self.token_dest.data_ptr() if self.T > 0 else None,
+                self.send_counts.data_ptr(), self.status.data_ptr(), self.ws_ptr,
+                self.ws_bytes, sp)
+
+    def plan(self, global_load, local_topk, stream=None):
+        """Enqueue topoep_plan_ex; returns (replica_slots, token_dest, send_counts, status)."""
+        rc = _lib.topoep_plan_ex(*self._args(global_load, local_topk, stream), _launch_ptr(self.launch))
+        if rc != OK:
+            raise TopoepError("topoep_plan", rc)
+        return self.replica_slots, self.token_dest, self.send_counts, self.status
+
+    def stage(self, stage: int, global_load, local_topk, stream=None):
+        """Enqueue one kernel of the plan (0 hist, 1 solve, 2 reroute)."""
+        rc = _lib.topoep_plan_stage(stage, *self._args(global_load, local_topk, stream),
+                                    _launch_ptr(self.launch))
+        if rc != OK:
+            raise TopoepError("topoep_plan_stage", rc)
+
+    def workspace_view(self) -> torch.Tensor:
+        off = self.ws_ptr - self._ws.data_ptr()
+        return self._ws[off:off + self.ws_bytes]
+
+
+def plan(topo: Topology, global_load, local_topk, replica_budget: int, stream=None, launch=None):
+    """One-shot plan: allocates outputs and workspace, enqueues topoep_plan.
+
+    Returns (replica_slots [R, N], token_dest [T, k], send_counts [R], status [1])
+    as CUDA int32 tensors, valid once the stream reaches them.
+    """
+    T, k = (int(local_topk.shape[0]), int(local_topk.shape[1])) if local_topk is not None else (0, 1)
+    p = Planner(topo, T, k, replica_budget, device=global_load.device, launch=launch)
+    # The workspace returns to torch's caching allocator with the Planner;
+    # reuse of that memory is ordered after these kernels on the same stream.
+    return p.plan(global_load, local_topk, stream)
+
+
+def raw_plan(*args):
+    """Direct call of topoep_plan with raw pointers (for ABI tests)."""
+    return _lib.topoep_plan(*args)
+
+
+def raw_workspace_bytes(topo, T, k, N):
+    out = ctypes.c_size_t(0)
+    rc = _lib.topoep_workspace_bytes(ctypes.byref(topo), T, k, N, ctypes.byref(out))
+    return rc, out.value

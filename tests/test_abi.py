@@ -1,0 +1,94 @@
+"""The C ABI library loads, exports every function include/topoep.h declares,
+and validates host arguments (no GPU work: only host-side paths are called)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "topoep.h")
+
+
+@pytest.fixture(scope="module")
+def tp():
+    from paper_2609_35481_amd import topoep
+    return topoep
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*int\s+(topoep_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert "topoep_plan" in names and "topoep_workspace_bytes" in names
+    assert len(names) == 5
+
+
+def test_library_exports_every_declared_symbol(tp):
+    lib = ctypes.CDLL(tp.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(declared_functions()) == set(tp.EXPORTS)
+
+
+def test_struct_layout_matches_header(tp):
+    assert ctypes.sizeof(tp.Topology) == 6 * 4 + 2 * 8
+    assert tp.Topology.tok_bytes.offset == 24
+    assert ctypes.sizeof(tp.Launch) == 16
+
+
+def base(tp, **kw):
+    args = dict(R=8, G=4, E=16, self_rank=0, c_intra=1, c_inter=4, S=4096, W=1 << 20)
+    args.update(kw)
+    return tp.topology(args["R"], args["G"], args["E"], args["self_rank"], args["c_intra"],
+                       args["c_inter"], args["S"], args["W"])
+
+
+def test_workspace_bytes_ok(tp):
+    n = tp.workspace_bytes(base(tp), 512, 2, 1)
+    assert n > 0 and n % 256 == 0
+    assert tp.workspace_bytes(base(tp), 0, 1, 0) > 0
+
+
+@pytest.mark.parametrize("kw,T,k,N,rc", [
+    (dict(R=0), 8, 1, 1, -1), (dict(G=3), 8, 1, 1, -1), (dict(E=12), 8, 1, 1, -1),
+    (dict(self_rank=8), 8, 1, 1, -1), (dict(self_rank=-1), 8, 1, 1, -1),
+    (dict(c_intra=-1), 8, 1, 1, -1), (dict(c_inter=-1), 8, 1, 1, -1), (dict(S=0), 8, 1, 1, -1),
+    (dict(W=-1), 8, 1, 1, -1), ({}, -1, 1, 1, -1), ({}, 8, 0, 1, -1), ({}, 8, 17, 1, -1),
+    ({}, 8, 1, -1, -1), ({}, 1 << 30, 4, 1, -1),
+    (dict(R=128, G=128, E=128), 8, 1, 1, -4),
+])
+def test_workspace_bytes_rejects(tp, kw, T, k, N, rc):
+    R = kw.get("R", 8)
+    t = base(tp, **kw)
+    got, _ = tp.raw_workspace_bytes(t, T, k, N)
+    assert got == rc
+
+
+def test_lds_limit_is_reported(tp):
+    # one domain of 64 ranks x 64 instances x 256 sources cannot sit in LDS
+    t = base(tp, R=256, G=64, E=256 * 60)
+    got, _ = tp.raw_workspace_bytes(t, 16, 1, 4)
+    assert got == tp.ELIMIT
+
+
+def test_plan_rejects_null_and_small_workspace_without_launching(tp):
+    t = base(tp)
+    ws = tp.workspace_bytes(t, 16, 2, 1)
+    # null global_load
+    assert tp.raw_plan(ctypes.byref(t), None, 256, 16, 2, 1, 512, 1024, 2048, 4096, 8192, ws, None) == tp.EINVAL
+    # misaligned workspace
+    assert tp.raw_plan(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 4096, 8192 + 4, ws,
+                       None) == tp.EWORKSPACE
+    # too small
+    assert tp.raw_plan(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 4096, 8192, ws - 256,
+                       None) == tp.EWORKSPACE
+    # bad launch shape
+    with pytest.raises(tp.TopoepError):
+        tp.workspace_bytes(t, 16, 2, 1, launch=(3, 256, 0, 256))
+    with pytest.raises(tp.TopoepError):
+        tp.workspace_bytes(t, 16, 2, 1, launch=(4, 96, 0, 256))

@@ -1,0 +1,336 @@
+"""GPU parity: every output of the HIP planner (replica_slots, token_dest,
+send_counts, status) equals the oracle's bit for bit, through the C ABI.
+
+Integer work throughout, so the bar is exact equality.  Cases: the paper's
+worked example, seeded random tiny instances (ragged sizes, every topology
+shape), the five workload configurations at full size, larger replica
+budgets that keep the refinement busy at scale, edge cases, launch-shape
+and repeat determinism, HIP-graph replay, and the single-stage entry point.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workload
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2609_35481_amd import topoep  # noqa: E402
+from test_oracle_pins import random_instance  # noqa: E402
+
+DEV = torch.device("cuda:0")
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def gpu_plan(R, G, E, self_rank, cI, cX, S, W, N, gl, tk, launch=None):
+    topo = topoep.topology(R, G, E, self_rank, cI, cX, S, W)
+    T, k = tk.shape
+    p = topoep.Planner(topo, T, k, N, device=DEV, launch=launch)
+    gl_d = torch.from_numpy(np.ascontiguousarray(gl, dtype=np.int32)).to(DEV)
+    tk_d = torch.from_numpy(np.ascontiguousarray(tk, dtype=np.int32)).to(DEV)
+    slots, dest, sc, st = p.plan(gl_d, tk_d)
+    torch.cuda.synchronize()
+    return dict(replica_slots=slots.cpu().numpy(), token_dest=dest.cpu().numpy(),
+                send_counts=sc.cpu().numpy(), status=int(st.item()))
+
+
+def ref_plan(R, G, E, self_rank, cI, cX, S, W, N, gl, tk):
+    topo = oracle.topology(R, G, E, self_rank, cI, cX, S, W)
+    return oracle.plan_ref(topo, gl, tk, N)
+
+
+def assert_same(got, ref, what=""):
+    assert got["status"] == ref["status"], (what, got["status"], ref["status"])
+    for key in ("replica_slots", "send_counts", "token_dest"):
+        a, b = got[key], ref[key]
+        assert a.shape == b.shape, (what, key, a.shape, b.shape)
+        if not np.array_equal(a, b):
+            bad = np.argwhere(a != b)
+            raise AssertionError("%s: %s differs at %d places, first %s: gpu %s oracle %s" % (
+                what, key, len(bad), bad[0].tolist(), a[tuple(bad[0])], b[tuple(bad[0])]))
+
+
+def both(*args, launch=None, what=""):
+    say("case", what)
+    got = gpu_plan(*args, launch=launch)
+    ref = ref_plan(*args)
+    assert_same(got, ref, what)
+    return got, ref
+
+
+def cfg_args(cfg, self_rank, gl, tk, N=None):
+    return (cfg.R, cfg.G, cfg.E, self_rank, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W,
+            cfg.N if N is None else N, gl, tk)
+
+
+# ---------------------------------------------------------------- paper example
+
+@pytest.mark.parametrize("self_rank", [0, 1, 2, 3])
+def test_worked_example(self_rank):
+    g = json.load(open(os.path.join(GOLD, "worked_example.json")))
+    tp = g["topology"]
+    om = np.array(g["omega"], np.int32)
+    tk = np.repeat(np.arange(tp["E"], dtype=np.int32), om[self_rank]).reshape(-1, 1)
+    got, _ = both(tp["R"], tp["G"], tp["E"], self_rank, tp["c_intra"], tp["c_inter"], tp["S"], tp["W"],
+                  tp["N"], om, tk, what="worked example self=%d" % self_rank)
+    assert got["replica_slots"].tolist() == g["expected"]["replica_slots"]
+
+
+# ---------------------------------------------------------------- random tiny
+
+@pytest.mark.parametrize("seed", range(150))
+def test_random_tiny(seed):
+    rng = np.random.default_rng(7000 + seed)
+    t, omega, topks = random_instance(7000 + seed, big=bool(seed % 2))
+    s = int(rng.integers(t.R))
+    tk = topks[s]
+    if tk.shape[0] == 0:
+        tk = np.zeros((0, topks[0].shape[1] if topks[0].ndim == 2 else 1), np.int32)
+    both(t.R, t.G, t.E, s, t.cI, t.cX, t.S, t.W, t.N, omega, tk, what="tiny seed %d" % seed)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_refinement_heavy(seed):
+    """Several slots per rank, one hot expert per domain: long refinement."""
+    rng = np.random.default_rng(9000 + seed)
+    G = int(rng.choice([2, 4, 8]))
+    M = int(rng.choice([1, 2, 4]))
+    R = G * M
+    P = int(rng.choice([1, 2, 4]))
+    E = R * P
+    k = int(rng.integers(1, min(E, 4) + 1))
+    N = int(rng.integers(1, 5))
+    pop = rng.dirichlet(np.full(E, 0.2))
+    topks = [rng.choice(E, size=(int(rng.integers(50, 400)), k), p=pop).astype(np.int32) for _ in range(R)]
+    omega = np.stack([np.bincount(x.ravel(), minlength=E) for x in topks]).astype(np.int32)
+    cI = int(rng.integers(0, 3))
+    cX = int(rng.integers(cI, 9))
+    S = int(rng.integers(1, 64))
+    W = int(rng.integers(1, 2 * S * 400))
+    s = int(rng.integers(R))
+    both(R, G, E, s, cI, cX, S, W, N, omega, topks[s], what="refine seed %d" % seed)
+
+
+# ---------------------------------------------------------------- configurations
+
+CONFIG_CASES = [("tiny", 0, 0), ("mixtral", 0, 0), ("mixtral", 7, 0), ("qwen3", 0, 0), ("qwen3", 5, 3),
+                ("dsv3", 0, 0), ("dsv3", 57, 0), ("stress", 0, 0)]
+
+
+@pytest.mark.parametrize("name,layer,mb", CONFIG_CASES)
+def test_config_full_size(name, layer, mb):
+    cfg = workload.get(name)
+    gl, tk = workload.make_layer(cfg, layer, mb, 0)
+    both(*cfg_args(cfg, 0, gl, tk), what="%s layer %d mb %d" % (name, layer, mb))
+
+
+@pytest.mark.parametrize("name,N", [("dsv3", 4), ("dsv3", 8), ("qwen3", 6), ("mixtral", 3), ("stress", 8)])
+def test_config_larger_budget(name, N):
+    """More slots than stage 1 can fill: the refinement commits many moves."""
+    cfg = workload.get(name)
+    gl, tk = workload.make_layer(cfg, 1, 0, 0)
+    both(*cfg_args(cfg, 0, gl, tk, N=N), what="%s N=%d" % (name, N))
+
+
+@pytest.mark.parametrize("name", ["tiny", "qwen3"])
+def test_every_self_rank_agrees(name):
+    """Every rank derives the same replica slots; send counts add up to the
+    rank loads of the plan (Section 3.1: no coordinator, no broadcast)."""
+    cfg = workload.get(name)
+    allr = workload.all_rank_topk(cfg, 0, 0)
+    gl, _ = workload.make_layer(cfg, 0, 0, 0)
+    slots = None
+    total = np.zeros(cfg.R, np.int64)
+    ranks = range(cfg.R) if cfg.R <= 8 else [0, 1, 7, 8, 15, 16, 31]
+    for s in ranks:
+        got, _ = both(*cfg_args(cfg, s, gl, np.ascontiguousarray(allr[s])), what="%s self=%d" % (name, s))
+        if slots is None:
+            slots = got["replica_slots"]
+        assert np.array_equal(got["replica_slots"], slots)
+        total += got["send_counts"]
+    if cfg.R <= 8:
+        ref = oracle.plan_ref(oracle.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W),
+                              gl, allr[0], cfg.N, debug=True, move_cap=10000)
+        assert np.array_equal(total, ref["load_final"])
+
+
+# ---------------------------------------------------------------- edge cases
+
+def _tiny():
+    cfg = workload.get("tiny")
+    gl, tk = workload.make_layer(cfg, 0, 0, 0)
+    return cfg, gl, tk
+
+
+def test_empty_local_batch():
+    cfg, gl, _ = _tiny()
+    gl = gl.copy()
+    gl[0] = 0
+    both(*cfg_args(cfg, 0, gl, np.zeros((0, cfg.k), np.int32)), what="T=0")
+
+
+def test_static_ep_budget_zero():
+    cfg, gl, tk = _tiny()
+    got, _ = both(*cfg_args(cfg, 0, gl, tk, N=0), what="N=0")
+    assert np.array_equal(got["token_dest"], tk // cfg.P)
+
+
+def test_budget_beyond_experts():
+    cfg, gl, tk = _tiny()
+    both(*cfg_args(cfg, 0, gl, tk, N=40), what="N=40")
+
+
+def test_k1_and_ragged():
+    rng = np.random.default_rng(3)
+    E, R, G = 24, 6, 3
+    tk = rng.integers(0, E, size=(1237, 1)).astype(np.int32)
+    gl = rng.integers(0, 300, size=(R, E)).astype(np.int32)
+    gl[2] = np.bincount(tk.ravel(), minlength=E)
+    both(R, G, E, 2, 1, 5, 33, 5000, 2, gl, tk, what="k=1 ragged")
+
+
+def test_one_gpu_per_node_and_single_domain():
+    cfg, gl, tk = _tiny()
+    both(cfg.R, 1, cfg.E, 0, 1, 4, cfg.S, cfg.W, 2, gl, tk, what="G=1")
+    both(cfg.R, cfg.R, cfg.E, 0, 1, 4, cfg.S, cfg.W, 2, gl, tk, what="M=1")
+
+
+def test_zero_intra_cost():
+    cfg, gl, tk = _tiny()
+    both(cfg.R, cfg.G, cfg.E, 0, 0, 4, cfg.S, cfg.W, 3, gl, tk, what="c_intra=0")
+
+
+def test_bad_id():
+    cfg, gl, tk = _tiny()
+    tk = tk.copy()
+    tk[100, 1] = cfg.E + 3
+    got, _ = both(*cfg_args(cfg, 0, gl, tk), what="bad id")
+    assert got["status"] & topoep.ST_BAD_ID
+    tk[100, 1] = -5
+    both(*cfg_args(cfg, 0, gl, tk), what="negative id")
+
+
+def test_negative_load_and_mismatch():
+    cfg, gl, tk = _tiny()
+    g2 = gl.copy()
+    g2[3, 5] = -2
+    got, _ = both(*cfg_args(cfg, 0, g2, tk), what="negative load")
+    assert got["status"] == topoep.ST_NEG_LOAD
+    g3 = gl.copy()
+    g3[0, 1] += 5
+    got, _ = both(*cfg_args(cfg, 0, g3, tk), what="self row mismatch")
+    assert got["status"] == topoep.ST_SELF_DIFF
+
+
+def test_range_bit():
+    cfg, gl, tk = _tiny()
+    got, _ = both(cfg.R, cfg.G, cfg.E, 0, 1, 1 << 10, 1 << 50, cfg.W, 1, gl, tk, what="range S")
+    assert got["status"] & topoep.ST_RANGE
+    got, _ = both(cfg.R, cfg.G, cfg.E, 0, 1, 4, cfg.S, 1 << 61, 1, gl, tk, what="range W")
+    assert got["status"] & topoep.ST_RANGE
+
+
+def test_many_domains_more_than_solver_groups():
+    """M = 256 domains (G = 1): solver workgroups loop over several domains."""
+    rng = np.random.default_rng(11)
+    R, G, E = 256, 1, 256
+    tk = rng.integers(0, E, size=(300, 2)).astype(np.int32)
+    gl = rng.integers(0, 20, size=(R, E)).astype(np.int32)
+    gl[5] = np.bincount(tk.ravel(), minlength=E)
+    both(R, G, E, 5, 1, 4, 64, 1500, 2, gl, tk, what="M=256")
+
+
+# ---------------------------------------------------------------- determinism
+
+LAUNCHES = [(1, 64, 0, 64), (2, 128, 1, 128), (4, 256, 0, 256), (8, 256, 2, 512), (8, 1024, 0, 1024),
+            (1, 1024, 3, 64), (4, 512, 1, 256)]
+
+
+@pytest.mark.parametrize("launch", LAUNCHES)
+@pytest.mark.parametrize("name", ["mixtral", "dsv3"])
+def test_launch_shapes_are_bitwise_identical(name, launch):
+    cfg = workload.get(name)
+    gl, tk = workload.make_layer(cfg, 2, 0, 0)
+    N = cfg.N + 2
+    both(*cfg_args(cfg, 0, gl, tk, N=N), launch=launch, what="%s launch %s" % (name, launch))
+
+
+def test_repeated_runs_identical():
+    cfg = workload.get("dsv3")
+    gl, tk = workload.make_layer(cfg, 3, 0, 0)
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    p = topoep.Planner(topo, cfg.T, cfg.k, 4, device=DEV)
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    first = None
+    for i in range(50):
+        out = [x.clone() for x in p.plan(gl_d, tk_d)]
+        if first is None:
+            first = out
+        else:
+            for a, b in zip(out, first):
+                assert torch.equal(a, b), i
+    ref = ref_plan(*cfg_args(cfg, 0, gl, tk, N=4))
+    torch.cuda.synchronize()
+    assert np.array_equal(first[1].cpu().numpy(), ref["token_dest"])
+
+
+def test_graph_replay_matches_eager():
+    """The enqueue is captured in a HIP graph and replayed with eager work in
+    between; every replay equals the oracle."""
+    cfg = workload.get("qwen3")
+    gl, tk = workload.make_layer(cfg, 4, 1, 0)
+    ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV)
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        p.plan(gl_d, tk_d)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        p.plan(gl_d, tk_d)
+    for i in range(5):
+        p.token_dest.fill_(-9)
+        p.send_counts.fill_(-9)
+        junk = torch.randn(1 << 16, device=DEV).sum()
+        g.replay()
+        torch.cuda.synchronize()
+        got = dict(replica_slots=p.replica_slots.cpu().numpy(), token_dest=p.token_dest.cpu().numpy(),
+                   send_counts=p.send_counts.cpu().numpy(), status=int(p.status.item()))
+        assert_same(got, ref, "graph replay %d" % i)
+        del junk
+
+
+def test_single_stages_repeat():
+    """After one plan, re-running each stage alone reproduces the outputs."""
+    cfg = workload.get("tiny")
+    gl, tk = workload.make_layer(cfg, 0, 0, 0)
+    ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV)
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    p.plan(gl_d, tk_d)
+    for stage in (2, 1, 2, 0, 1, 2):
+        p.token_dest.fill_(-9)
+        p.stage(stage, gl_d, tk_d)
+        if stage != 2:
+            p.stage(2, gl_d, tk_d)
+        torch.cuda.synchronize()
+        assert np.array_equal(p.token_dest.cpu().numpy(), ref["token_dest"]), stage
