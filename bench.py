@@ -1,0 +1,277 @@
+"""Benchmark of the TopoEP planner on one MI355X.
+
+A step plans every MoE layer of one microbatch: for each layer, the
+histogram, solver and reroute kernels run back to back on one stream, all
+layers captured in one HIP graph (the layers are planned one after another,
+as they would be in a forward pass).  Inputs (the synthetic routing matrix
+and this rank's top-k ids of every layer) are resident in HBM before the
+timed region.
+
+Printed JSON line: value = rerouted assignments per second over the whole
+step; plan_latency_us_per_layer = step time / layers.  ``roofline`` covers
+the kernel with the longest average duration, timed with HIP events on the
+stream it runs on; ``cpu_baseline`` times the CPU oracle on a bounded sample
+of the same workload on this host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config dsv3]
+       python bench.py --sweep    (histogram/reroute bandwidth sweep)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workload  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "plan latency (us) per MoE layer at EP32/256e/top-8; rerouted assignments/s"
+DESCR = {
+    "tiny": "Tiny: 2 nodes x 4 GPUs (R=8), E=16, top-2, T=512, 1 slot, 1 layer",
+    "mixtral": "Mixtral-like: 1 node x 8 GPUs (R=8), E=8, top-2, T=4096, 1 slot, 32 layers",
+    "qwen3": "Qwen3-MoE-like: 4 nodes x 8 GPUs (R=32), E=128, top-8, T=4096, 2 slots, 48 layers",
+    "dsv3": "DeepSeek-V3-like: 4 nodes x 8 GPUs (R=32), E=256, top-8, T=8192, 2 slots, 58 layers",
+    "stress": "Stress: 32 nodes x 8 GPUs (R=256), E=512, top-8, T=16384, 4 slots, 16 layers",
+}
+
+
+def _gen(args):
+    name, layer, mb = args
+    cfg = workload.get(name)
+    return workload.make_layer(cfg, layer, mb, 0)
+
+
+def make_inputs(cfg, layers, mb=0, workers=None):
+    jobs = [(cfg.name, l, mb) for l in range(layers)]
+    workers = workers or min(16, os.cpu_count() or 1, layers)
+    if workers > 1 and layers > 1:
+        import multiprocessing as mp
+        with mp.get_context("fork").Pool(workers) as pool:
+            return pool.map(_gen, jobs)
+    return [_gen(j) for j in jobs]
+
+
+def algorithmic_bytes(cfg, N):
+    """Bytes the method must move per layer, by kernel."""
+    a = cfg.T * cfg.k
+    return {
+        "hist": 4 * a,                                   # read the ids
+        "solve": 4 * cfg.R * cfg.E + 4 * cfg.R * (N + 1),  # read Omega, write slots and counts
+        "reroute": 8 * a,                                # read the ids, write destinations
+    }
+
+
+def cpu_baseline(cfg, inputs, budget_s=15.0):
+    import oracle
+    n = 0
+    t0 = time.perf_counter()
+    for gl, tk in inputs:
+        oracle.plan_cfg(cfg, gl, tk, 0)
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n * cfg.T * cfg.k / dt, "unit": "assignments/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d layers of the %s workload (planned back to back, one thread): "
+                      "%.0f us per layer" % (n, len(inputs), cfg.name, dt / n * 1e6)}
+
+
+def time_stage(torch, planners, dev_inputs, stage, reps):
+    """Average duration of one kernel of the plan, from HIP events recorded
+    around each launch on the stream the kernel runs on."""
+    stream = torch.cuda.current_stream()
+    durs = []
+    for r in range(reps):
+        for p, (g, t) in zip(planners, dev_inputs):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            p.stage(stage, g, t, stream=stream)
+            b.record(stream)
+            durs.append((a, b))
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in durs])
+    return float(np.mean(ms)) * 1e3, float(np.median(ms)) * 1e3   # microseconds
+
+
+def run_bench(args):
+    import torch
+    from paper_2609_35481_amd import topoep
+
+    cfg = workload.get(args.config)
+    N = cfg.N
+    layers = cfg.layers if args.layers <= 0 else args.layers
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    inputs = make_inputs(cfg, layers)
+    t_gen = time.perf_counter() - t_gen
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev))
+                  for gl, tk in inputs]
+    planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev) for _ in range(layers)]
+
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        for p, (g, t) in zip(planners, dev_inputs):
+            p.plan(g, t)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for p, (g, t) in zip(planners, dev_inputs):
+            p.plan(g, t)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        graph.replay()
+        b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    ms_per_step = wall / args.steps * 1e3
+    assign = layers * cfg.T * cfg.k
+    value = assign / (ms_per_step / 1e3)
+
+    # every plan of the last replay must be a valid plan (status 0)
+    st = torch.stack([p.status for p in planners]).cpu().numpy().ravel()
+    if (st & ~topoep.ST_SELF_DIFF).any():
+        raise SystemExit("plan status bits set: %s" % np.unique(st))
+
+    # per-kernel durations (HIP events around each launch, eager, same stream)
+    stages = {}
+    for name, sid in (("hist", 0), ("solve", 1), ("reroute", 2)):
+        stages[name] = time_stage(torch, planners, dev_inputs, sid, max(1, args.stage_reps))
+    # restore complete plans in every workspace
+    for p, (g, t) in zip(planners, dev_inputs):
+        p.plan(g, t)
+    torch.cuda.synchronize()
+
+    nbytes = algorithmic_bytes(cfg, N)
+    dom = max(stages, key=lambda k: stages[k][0])
+    avg_us = stages[dom][0]
+    achieved = nbytes[dom] / (avg_us * 1e-6) / 1e9
+    roof = {"bound": "hbm", "kernel": dom + "_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+            "algorithmic_bytes_per_launch": nbytes[dom], "avg_kernel_us": avg_us}
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "assignments/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": DESCR[cfg.name], "layers_per_step": layers, "tokens_per_rank": cfg.T,
+                   "top_k": cfg.k, "ranks": cfg.R, "experts": cfg.E, "replica_slots": N,
+                   "assignments_per_layer": cfg.T * cfg.k},
+        "plan_latency_us_per_layer": ms_per_step * 1e3 / layers,
+        "plan_latency_us_per_layer_p10_p50_p90": [float(np.percentile(step_ms, q)) * 1e3 / layers
+                                                  for q in (10, 50, 90)],
+        "kernel_avg_us": {k: round(v[0], 3) for k, v in stages.items()},
+        "kernel_median_us": {k: round(v[1], 3) for k, v in stages.items()},
+        "roofline": roof,
+        "input_generation_s": round(t_gen, 2),
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds)
+    return out
+
+
+def run_sweep(args):
+    """Histogram and reroute alone over synthetic id arrays of growing size,
+    past the 256 MB Infinity Cache, with a fixed plan."""
+    import torch
+    from paper_2609_35481_amd import topoep
+
+    dev = torch.device("cuda:0")
+    rows = []
+    for E in (128, 512):
+        R, G = 32, 8
+        for lg in range(16, args.sweep_max_log2 + 1, 2):
+            n = 1 << lg
+            k = 8
+            T = n // k
+            rng = np.random.default_rng(lg)
+            p = workload.generate.zipf_weights(E, 1.0)
+            tk = torch.from_numpy(rng.choice(E, size=(T, k), p=p).astype(np.int32)) if n <= (1 << 22) else None
+            if tk is None:
+                small = torch.from_numpy(rng.choice(E, size=(1 << 22,), p=p).astype(np.int32)).to(dev)
+                tk_d = small.repeat(n // (1 << 22)).view(T, k)
+            else:
+                tk_d = tk.to(dev)
+            hist = torch.bincount(tk_d.view(-1).long(), minlength=E).to(torch.int32)
+            # other ranks' rows stay small so that the total load fits int32
+            gl = torch.randint(0, 1000, (R, E), dtype=torch.int32, device=dev)
+            gl[0] = hist
+            topo = topoep.topology(R, G, E, 0, 1, 8, 4096, 9 << 20)
+            pl = topoep.Planner(topo, T, k, 2, device=dev)
+            pl.plan(gl, tk_d)
+            torch.cuda.synchronize()
+            st = int(pl.status.item())
+            res = {}
+            for name, sid, bpa in (("hist", 0, 4), ("reroute", 2, 8)):
+                reps = 5 if n >= (1 << 26) else 20
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                pl.stage(sid, gl, tk_d)
+                a.record()
+                for _ in range(reps):
+                    pl.stage(sid, gl, tk_d)
+                b.record()
+                torch.cuda.synchronize()
+                us = a.elapsed_time(b) * 1e3 / reps
+                res[name] = {"us": round(us, 2), "GB/s": round(bpa * n / us / 1e3, 1)}
+            rows.append({"E": E, "ids": n, "status": st, **res})
+            print(json.dumps(rows[-1]), flush=True)
+            del pl, tk_d, gl
+            torch.cuda.empty_cache()
+    return rows
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="dsv3", choices=sorted(DESCR))
+    ap.add_argument("--layers", type=int, default=0, help="0 = the configuration's layer count")
+    ap.add_argument("--stage-reps", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-max-log2", type=int, default=28)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the planner is replicated per rank and has no "
+              "cross-GPU step in this build (--gpus %d requested)" % args.gpus, file=sys.stderr)
+        raise SystemExit(2)
+    if args.sweep:
+        run_sweep(args)
+        return
+    print(json.dumps(run_bench(args)), flush=True)
+
+
+if __name__ == "__main__":
+    main()

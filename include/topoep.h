@@ -61,6 +61,9 @@ typedef struct topoep_launch {
   int32_t block_threads;    /* 64..1024, multiple of 64, for histogram/reroute    */
   int32_t tiles_per_block;  /* >= 1; 0 = choose from the problem size             */
   int32_t solve_threads;    /* 64..1024, multiple of 64, for the solver           */
+  int32_t solver;           /* 0 = choose, 1 = one workgroup for all domains       */
+                            /* (needs the whole state in LDS), 2 = one workgroup */
+                            /* per domain with a grid barrier                    */
 } topoep_launch;
 
 /* Host return codes. */

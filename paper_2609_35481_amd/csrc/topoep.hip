@@ -7,30 +7,37 @@
 //            LDS-privatised histogram; within a wave the lanes holding the
 //            same expert are found with ballots over the id bits, and only
 //            the lowest such lane adds the group's popcount.  Writes the
-//            block's partial histogram (routing-matrix row of this rank,
-//            Eq. 3, Section 3.1).
-//   solve    one workgroup per domain (NVLink/xGMI node).  Sums the block
-//            partials (row self of Omega and the per-block offsets for the
-//            reroute), computes the domain demand D (Eq. 4) and the
-//            inter-node placement by the benefit b = 2 D S - W (Eq. 9); a
-//            bounded grid barrier publishes every domain's replicas; each
-//            workgroup then builds its instances' routing q (Section 4.3,
-//            routing construction) in LDS and runs the intra-node refinement
-//            (Eq. 10) on one wavefront with wave64 reductions and no
-//            barriers per iteration.  The last workgroup to finish turns this
-//            rank's q row into a per-expert instance list.
+//            block's partial histogram (this rank's row of the routing
+//            matrix Omega, Eq. 3, Section 3.1).
+//   solve    the placement solver, in one of two shapes:
+//            - one workgroup for every domain when the whole state fits in
+//              the 160 KB of LDS: Omega, every domain's instances and their
+//              q columns live on one CU, and each domain's refinement runs
+//              on its own wavefront;
+//            - one workgroup per domain (NVLink/xGMI node) otherwise, with a
+//              bounded grid barrier that publishes the inter-node placement
+//              of every domain and a last-workgroup step that assembles
+//              this rank's instance list.
+//            Either way: domain demand D (Eq. 4), inter-node placement by
+//            the benefit b = 2 D S - W (Eq. 9), routing construction q, U, L
+//            (Section 4.3) and intra-node refinement (Eq. 10) with wave64
+//            reductions and no barrier per iteration.  Extra workgroups of
+//            the same launch compute each histogram block's exclusive
+//            per-expert offsets for the reroute, off the solver's path.
 //   reroute  same chunking as hist.  Stable rank of every assignment among
 //            the earlier assignments of its expert (ballot peer masks inside
-//            a wave, per-wave counts scanned across waves, block offsets from
-//            the solver), then the instance whose prefix range holds it.
+//            a wave, per-wave counts scanned across waves, block offsets),
+//            then the instance whose prefix range holds it.
 //
 // All arithmetic is integer; no atomic decides an order or a placement
 // (LDS/global integer atomics only accumulate commutative counts, masks and
-// a grid-barrier ticket), so results are bitwise reproducible across runs
-// and launch shapes.
+// barrier tickets, or pick list slots whose order is re-established by a
+// key), so results are bitwise reproducible across runs and launch shapes.
+// Divisions by launch-time constants use a multiply and a shift (fastdiv.h).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fastdiv.h"
 #include "topoep.h"
 
 namespace {
@@ -47,39 +54,43 @@ constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kMaxSolveGroups = 128;    // co-resident by a wide margin (256 CUs)
-constexpr int kTargetBlocks = 256;      // histogram/reroute blocks to aim for
+constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
+constexpr int kOffsetExperts = 64;      // experts per offset workgroup
 constexpr uint32_t kSpinLimit = 1u << 24;
 constexpr uint32_t kIterLimit = 1u << 22;
+constexpr int kSmallDiv = 64;
 
 // ---------------------------------------------------------------- plan
 
 struct Plan {
-  int R, G, M, E, P, N, Neff, PN, I, self, MW, RW, nbits, cap1, nent_cap;
+  int R, G, M, E, P, N, Neff, PN, I, self, MW, RW, nbits, cap1, nent_cap, QS;
   int cI, cX;
   int64_t S, W;
   int64_t n, chunk;
-  int nb;
+  int nb, n_solvers, n_helpers;
   uint32_t spin_limit, iter_limit;
+  FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
+  FastDiv fsmall[kSmallDiv + 1];   // divisors 1..kSmallDiv (hosting-domain counts)
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   uint32_t *ctrl;
-  int32_t *partials, *offsets, *blk_err, *hist, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
-};
-
-// LDS layout of the solver, in int32 words (shared by host sizing and device).
-struct SolveLds {
-  int cb, hs, ce, mask, slots, used, L, e_of, U, misc, qcol, words;
+  int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
 };
 
 __host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
 __host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
 
-__host__ __device__ inline SolveLds solve_lds(const Plan &p) {
-  SolveLds l;
+// LDS layout of the one-workgroup-per-domain solver, in int32 words.
+struct DomainLds {
+  int ck, hs, rows, mask, slots, used, L, e_of, U, misc, qcol, words;
+};
+
+__host__ __device__ inline DomainLds domain_lds(const Plan &p) {
+  DomainLds l;
   int o = 0;
-  l.cb = o;    o += 2 * p.E;                 // int64 benefits of stage-1 candidates
+  l.ck = o;    o += 2 * p.E;                 // uint64 stage-1 candidate keys
   l.hs = o;    o += p.E;                     // row self of Omega (histogram)
-  l.ce = o;    o += p.E;                     // stage-1 candidate experts
+  l.rows = o;  o += p.G * p.E;               // Omega rows of the domain's sources
   l.mask = o;  o += p.E * p.MW;              // per expert: domains hosting it
   l.slots = o; o += p.G * imax(p.Neff, 1);   // replica slots of the domain's ranks
   l.used = o;  o += p.G;
@@ -89,7 +100,37 @@ __host__ __device__ inline SolveLds solve_lds(const Plan &p) {
   o = (o + 3) & ~3;
   l.misc = o;  o += 64;
   l.qcol = o;                                // q[s][e][r] of the domain's instances
-  o += imax(p.I * p.R, 2 * p.E + 2 + p.E * p.RW + 64);
+  o += imax(p.I * p.QS, imax(2 * p.E + 2 + p.E * p.RW + 64, 1024));
+  l.words = o;
+  return l;
+}
+
+// LDS layout of the single-workgroup solver: every domain's state at once.
+struct SingleLds {
+  int ck, hs, cnt, mask, repl, nsel, slots, used, L, e_of, U, misc, om, qcol, words;
+};
+
+__host__ __device__ inline SingleLds single_lds(const Plan &p) {
+  SingleLds l;
+  int o = 0;
+  l.ck = o;    o += 2 * p.M * p.E;            // uint64 stage-1 candidate keys per domain
+  l.hs = o;    o += p.E;                      // histogram of local_topk
+  l.cnt = o;   o += p.M;                      // candidates per domain
+  l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
+  l.repl = o;  o += p.M * imax(p.cap1, 1);    // stage-1 replicas per domain
+  l.nsel = o;  o += p.M;
+  l.slots = o; o += p.R * imax(p.Neff, 1);    // replica slots of every rank
+  l.used = o;  o += p.R;
+  l.L = o;     o += p.R;                      // rank loads
+  l.e_of = o;  o += p.M * p.I;                // expert of each instance
+  l.U = o;     o += p.M * p.I;                // instance loads
+  o = (o + 3) & ~3;
+  l.misc = o;  o += 64;
+  l.om = o;                                   // Omega' [R][E], then list scratch
+  o += imax(p.R * p.E, p.E + 2 + p.E * p.RW + 2 * p.nent_cap + 64);
+  o = (o + 3) & ~3;
+  l.qcol = o;                                 // partial-sum scratch, then q columns
+  o += imax(p.M * p.I * p.QS, 1024);
   l.words = o;
   return l;
 }
@@ -118,6 +159,67 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Workgroup barrier that orders LDS only: it does not wait for outstanding
+// global stores (the solver's outputs), unlike __syncthreads.
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Cross-lane moves within rows of 16 lanes (DPP); every lane of the wave
+// must be active.  0x121..0x12F = row_ror:1..15, 0x111..0x11F = row_shr,
+// 0x142/0x143 = row_bcast:15/31.
+template <int C>
+__device__ inline uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, C, 0xF, 0xF, true);
+}
+template <int C>
+__device__ inline uint64_t dpp_mov64(uint64_t v) {
+  return ((uint64_t)dpp_mov<C>((uint32_t)(v >> 32)) << 32) | dpp_mov<C>((uint32_t)v);
+}
+__device__ inline uint64_t readlane64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+
+// Wave-wide minimum / maximum / sum, the same value in every lane: rotations
+// by 8, 4, 2, 1 inside each row of 16 lanes, then the four row results.
+__device__ inline uint64_t wave_min_u64(uint64_t v) {
+  uint64_t o;
+  o = dpp_mov64<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x121>(v); v = o < v ? o : v;
+  uint64_t a = readlane64(v, 0), b = readlane64(v, 16), c = readlane64(v, 32), d = readlane64(v, 48);
+  a = b < a ? b : a;
+  c = d < c ? d : c;
+  return c < a ? c : a;
+}
+
+__device__ inline uint64_t wave_max_u64(uint64_t v) { return ~wave_min_u64(~v); }
+
+__device__ inline uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp_mov64<0x128>(v);
+  v += dpp_mov64<0x124>(v);
+  v += dpp_mov64<0x122>(v);
+  v += dpp_mov64<0x121>(v);
+  return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
+}
+
+// Inclusive prefix sum over the 64 lanes (row shifts, then row broadcasts).
+__device__ inline int wave_incl_scan(int x) {
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
+  return x;
+}
+
+__device__ inline int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+
 __device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t b1, uint64_t b2,
                                 uint64_t b3) {
   if (a1 != b1) return a1 < b1;
@@ -125,32 +227,24 @@ __device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t 
   return a3 < b3;
 }
 
+// Lexicographic minimum of (k1, k2, k3) over the wave, in every lane: one
+// wave minimum per key, the later ones only when the earlier key ties.
 __device__ inline void wave_argmin3(uint64_t &k1, uint64_t &k2, uint64_t &k3) {
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t o1 = __shfl_xor(k1, off), o2 = __shfl_xor(k2, off), o3 = __shfl_xor(k3, off);
-    if (lex_less(o1, o2, o3, k1, k2, k3)) {
-      k1 = o1;
-      k2 = o2;
-      k3 = o3;
-    }
+  const uint64_t m1 = wave_min_u64(k1);
+  uint64_t tie = __ballot(k1 == m1);
+  if (__popcll(tie) == 1) {
+    const int l = __ffsll((long long)tie) - 1;
+    k1 = m1;
+    k2 = readlane64(k2, l);
+    k3 = readlane64(k3, l);
+    return;
   }
-}
-
-__device__ inline uint64_t wave_max_u64(uint64_t v) {
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t o = __shfl_xor(v, off);
-    v = o > v ? o : v;
-  }
-  return v;
-}
-
-__device__ inline int wave_incl_scan(int x) {
-  const int lane = lane_id();
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  return x;
+  const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
+  tie = __ballot(k1 == m1 && k2 == m2);
+  const uint64_t m3 = wave_min_u64((k1 == m1 && k2 == m2) ? k3 : ~0ull);
+  k1 = m1;
+  k2 = m2;
+  k3 = m3;
 }
 
 // Exclusive scan of a[0..n) in place by the whole workgroup; returns the total.
@@ -163,7 +257,7 @@ __device__ int block_excl_scan(int *a, int n, int *tmp) {
   for (int i = lo; i < hi; ++i) s += a[i];
   const int incl = wave_incl_scan(s);
   if (lane == 63) tmp[wave] = incl;
-  __syncthreads();
+  lds_barrier();
   if (tid == 0) {
     int run = 0;
     for (int w = 0; w < nw; ++w) {
@@ -173,7 +267,7 @@ __device__ int block_excl_scan(int *a, int n, int *tmp) {
     }
     tmp[nw] = run;
   }
-  __syncthreads();
+  lds_barrier();
   int run = tmp[wave] + incl - s;
   for (int i = lo; i < hi; ++i) {
     const int t = a[i];
@@ -181,12 +275,160 @@ __device__ int block_excl_scan(int *a, int n, int *tmp) {
     run += t;
   }
   const int total = tmp[nw];
-  __syncthreads();
+  lds_barrier();
   return total;
 }
 
-// Grid barrier of the solver's workgroups: every workgroup is resident (at
-// most kMaxSolveGroups), and the wait is bounded so the kernel always exits.
+// Global -> LDS copy by the whole workgroup, four 16-byte loads in flight
+// per thread when source, destination and length allow.
+__device__ void copy_to_lds(int *dst, const int *src, int n) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0 && (n & 3) == 0) {
+    const int n4 = n >> 2;
+    const int4 *s4 = reinterpret_cast<const int4 *>(src);
+    int4 *d4 = reinterpret_cast<int4 *>(dst);
+    int base = tid;
+    for (; base + 3 * nt < n4; base += 4 * nt) {
+      const int4 a = s4[base], b = s4[base + nt], c = s4[base + 2 * nt], d = s4[base + 3 * nt];
+      d4[base] = a;
+      d4[base + nt] = b;
+      d4[base + 2 * nt] = c;
+      d4[base + 3 * nt] = d;
+    }
+    for (; base < n4; base += nt) d4[base] = s4[base];
+  } else {
+    int base = tid;
+    for (; base + 3 * nt < n; base += 4 * nt) {
+      const int a = src[base], b = src[base + nt], c = src[base + 2 * nt], d = src[base + 3 * nt];
+      dst[base] = a;
+      dst[base + nt] = b;
+      dst[base + 2 * nt] = c;
+      dst[base + 3 * nt] = d;
+    }
+    for (; base < n; base += nt) dst[base] = src[base];
+  }
+}
+
+// Histogram of local_topk (row self of Omega) as the sum of the histogram
+// blocks' partials: thread (e, g) sums its share of the blocks with eight
+// loads in flight; scratch needs max(E, (blockDim / E) * E) words.
+__device__ void hist_from_partials(const Plan &p, int *hs, int *scratch) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb;
+  if ((E & 3) == 0) {
+    // thread (e4, g): four experts, a share of the blocks, 16-byte loads
+    const int E4 = E >> 2;
+    const int groups = imax(1, nt / E4);
+    const int per = (nb + groups - 1) / groups;
+    const int4 *part4 = reinterpret_cast<const int4 *>(p.partials);
+    int4 *scr4 = reinterpret_cast<int4 *>(scratch);
+    for (int t = tid; t < groups * E4; t += nt) {
+      const int g = t / E4, e4 = t - g * E4;
+      const int b0 = g * per, b1 = imin(nb, b0 + per);
+      int4 run = make_int4(0, 0, 0, 0);
+      for (int b = b0; b < b1; b += 8) {
+        int4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? part4[(int64_t)(b + u) * E4 + e4] : make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          run.x += v[u].x;
+          run.y += v[u].y;
+          run.z += v[u].z;
+          run.w += v[u].w;
+        }
+      }
+      scr4[t] = run;
+    }
+    lds_barrier();
+    for (int e = tid; e < E; e += nt) {
+      int sum = 0;
+      for (int g = 0; g < groups; ++g) sum += scratch[g * E + e];
+      hs[e] = sum;
+    }
+    lds_barrier();
+    return;
+  }
+  const int groups = imax(1, nt / E);
+  const int per = (nb + groups - 1) / groups;
+  for (int t = tid; t < groups * E; t += nt) {
+    const int g = (int)fdiv((uint32_t)t, p.fE), e = t - g * E;
+    const int b0 = g * per, b1 = imin(nb, b0 + per);
+    int run = 0;
+    for (int b = b0; b < b1; b += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) run += v[u];
+    }
+    scratch[t] = run;
+  }
+  lds_barrier();
+  for (int e = tid; e < E; e += nt) {
+    int sum = 0;
+    for (int g = 0; g < groups; ++g) sum += scratch[g * E + e];
+    hs[e] = sum;
+  }
+  lds_barrier();
+}
+
+// Exclusive per-expert offset of every histogram block, for the reroute
+// (offset workgroup h of n_helpers handles kOffsetExperts experts at a time).
+__device__ void block_offsets(const Plan &p, int h, int *scratch) {
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, E = p.E, nb = p.nb;
+  const int el = tid & 63, g = tid >> 6;
+  const int per = (nb + nw - 1) / nw;
+  const int b0 = g * per, b1 = imin(nb, b0 + per);
+  for (int e0 = h * kOffsetExperts; e0 < E; e0 += p.n_helpers * kOffsetExperts) {
+    const int e = e0 + el;
+    int run = 0;
+    if (e < E) {
+      for (int b = b0; b < b1; b += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) run += v[u];
+      }
+    }
+    scratch[g * 64 + el] = run;
+    __syncthreads();
+    int base = 0;
+    for (int g2 = 0; g2 < g; ++g2) base += scratch[g2 * 64 + el];
+    if (e < E) {
+      for (int b = b0; b < b1; b += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (b + u < b1) p.offsets[(int64_t)(b + u) * E + e] = base;
+          base += v[u];
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Exact-range check: the total load fits int32 and 4 S total c + c W < 2^62
+// (c = max(c_intra, c_inter, 1)), so every benefit and cost change is exact.
+__device__ inline bool out_of_range(const Plan &p, uint64_t total) {
+  const uint64_t lim = 1ull << 62;
+  const uint64_t cm = (uint64_t)imax(imax(p.cI, p.cX), 1);
+  if (total > 0x7FFFFFFFull) return true;
+  // 4 S total cm and cm W with overflow checks (every factor is nonnegative)
+  uint64_t tok = 0, rep = 0;
+  if (__builtin_mul_overflow((uint64_t)p.S, 4ull * total, &tok)) return true;
+  if (__builtin_mul_overflow(tok, cm, &tok)) return true;
+  if (__builtin_mul_overflow((uint64_t)p.W, cm, &rep)) return true;
+  if (tok >= lim || rep >= lim) return true;
+  return tok + rep >= lim;
+}
+
+// Grid barrier of the per-domain solver workgroups: all of them are
+// resident (at most kMaxSolveGroups), and the wait is bounded so the kernel
+// always exits.
 __device__ bool grid_barrier(uint32_t *count, uint32_t groups, uint32_t spin_limit, int *flag) {
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -253,21 +495,85 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
   if (tid == 0) p.blk_err[b] = bad;
 }
 
-// ---------------------------------------------------------------- solver
+// ---------------------------------------------------------------- solver steps
+
+// Routing construction (Section 4.3) for NI instances, instance i of domain
+// dom_of(i) holding expert e_of[i] (-1 = empty).  The unique instance of e
+// inside dom(s) takes all of omega[s][e]; sources of a domain without an
+// instance of e split omega[s][e] evenly over every instance of e (one per
+// hosting domain, so an instance's position in ascending rank order is the
+// number of hosting domains below its own), the lowest positions taking the
+// remainder; sources of another domain that hosts e send it nothing.  The
+// case is decided once per source domain.  Thread t handles the run of
+// source domains t / NI of instance t % NI; qcol[i * QS + s] = q[s][e][r_i];
+// U[i] += sum_s q (U must be zero on entry).
+template <class WOf, class DomOf>
+__device__ void route_instances(const Plan &p, int NI, FastDiv fNI, const int *e_of, const uint32_t *mask,
+                                int *qcol, int *U, WOf w_of, DomOf dom_of) {
+  const int tid = threadIdx.x, nt = blockDim.x, G = p.G, M = p.M;
+  const int chunks = imax(1, imin(M, nt / imax(NI, 1)));
+  const int dpc = (M + chunks - 1) / chunks;
+  for (int t = tid; t < NI * chunks; t += nt) {
+    const int c = (int)fdiv((uint32_t)t, fNI), i = t - c * NI;
+    const int e = e_of[i];
+    const int ds0 = c * dpc, ds1 = imin(M, ds0 + dpc);
+    int *row = qcol + i * p.QS;
+    if (e < 0) {
+      for (int s = ds0 * G; s < ds1 * G; ++s) row[s] = 0;
+      continue;
+    }
+    const int d = dom_of(i);
+    const uint32_t *me = mask + e * p.MW;
+    int n = 0, below = 0;
+    for (int wd = 0; wd < p.MW; ++wd) {
+      const uint32_t bits = me[wd];
+      n += __popc(bits);
+      const int lo = wd * 32;
+      if (d >= lo + 32) below += __popc(bits);
+      else if (d > lo) below += __popc(bits & ((1u << (d - lo)) - 1u));
+    }
+    const FastDiv fn = n <= kSmallDiv ? p.fsmall[n] : make_fastdiv((uint32_t)n);
+    int usum = 0;
+    for (int ds = ds0; ds < ds1; ++ds) {
+      const int s0 = ds * G;
+      if (ds == d) {
+#pragma unroll 8
+        for (int j = 0; j < G; ++j) {
+          const int w = w_of(i, s0 + j, e);
+          row[s0 + j] = w;
+          usum += w;
+        }
+      } else if ((me[ds >> 5] >> (ds & 31)) & 1u) {
+        for (int j = 0; j < G; ++j) row[s0 + j] = 0;
+      } else {
+#pragma unroll 8
+        for (int j = 0; j < G; ++j) {
+          const int w = w_of(i, s0 + j, e);
+          const int qq = (int)fdiv((uint32_t)w, fn);
+          const int q = qq + (below < w - qq * n ? 1 : 0);
+          row[s0 + j] = q;
+          usum += q;
+        }
+      }
+    }
+    if (usum) atomicAdd(&U[i], usum);
+  }
+}
 
 // Instance index of expert e on local rank j of domain d, or -1.
 __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int *slots,
                                   const int *used) {
   const int rank = d * p.G + j;
-  if (e / p.P == rank) return j * p.PN + (e - rank * p.P);
+  if ((int)fdiv((uint32_t)e, p.fP) == rank) return j * p.PN + (e - rank * p.P);
   const int u = used[j];
   for (int t = 0; t < u; ++t)
     if (slots[j * p.Neff + t] == e) return j * p.PN + p.P + t;
   return -1;
 }
 
-// Intra-node refinement of domain d (Section 4.3, Eq. 10), by wave 0.
-// Each iteration picks the busiest rank rb (ties to the lowest rank), scores
+// Intra-node refinement of domain d (Section 4.3, Eq. 10), by one wave.
+// e_of/U/qcol/slots/used/Lr point at the domain's own state.  Each
+// iteration picks the busiest rank rb (ties to the lowest rank), scores
 // every (instance of rb, other rank of the domain) candidate with key
 // (delta desc, L[rt] asc, cost change asc, e asc, rt asc), and commits the
 // best one.  The moved assignments come from sources in ascending
@@ -278,10 +584,11 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                               int *Lr, uint32_t *flags) {
   const int lane = lane_id();
-  const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff;
+  const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS;
   if (G < 2) return;
   const int r0 = d * G;
   const int ncand = PN * (G - 1);
+  const FastDiv fG1 = p.fG1;
   const int64_t twoS = 2 * p.S;
   for (uint32_t it = 0;; ++it) {
     if (it >= p.iter_limit) {
@@ -297,14 +604,14 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
     const int rb = r0 + rbj;
     uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull;
     for (int c = lane; c < ncand; c += 64) {
-      const int ai = c / (G - 1), jj = c - ai * (G - 1);
+      const int ai = (int)fdiv((uint32_t)c, fG1), jj = c - ai * (G - 1);
       const int rtj = jj < rbj ? jj : jj + 1;
       const int a = rbj * PN + ai;
       const int e = e_of[a];
       const int u = U[a];
       if (e < 0 || u <= 0) continue;
       const int rt = r0 + rtj;
-      const int me = e / P;
+      const int me = (int)fdiv((uint32_t)e, p.fP);
       bool hosts = me == rt;
       const int urt = used[rtj];
       for (int t = 0; t < urt && !hosts; ++t) hosts = slots[rtj * Neff + t] == e;
@@ -315,14 +622,14 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
       const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
       int64_t dtok = 0;
       if (p.cI > 0) {
-        const int qrt = qcol[a * R + rt], qrb = qcol[a * R + rb];
+        const int qrt = qcol[a * QS + rt], qrb = qcol[a * QS + rb];
         const int m_rt = imin(delta, qrt);
         const int rest = delta - m_rt;
         const int m_oth = imin(rest, u - qrt - qrb);
         const int m_rb = rest - m_oth;
         dtok = (int64_t)p.cI * (int64_t)(m_rb - m_rt);
       }
-      const int64_t crep = (me / G == d) ? p.cI : p.cX;   // me != rt when !hosts
+      const int64_t crep = ((int)fdiv((uint32_t)me, p.fG) == d) ? p.cI : p.cX;   // me != rt when !hosts
       const int64_t dcost = twoS * dtok + (hosts ? 0 : crep * p.W);
       const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
       const uint64_t c2 = (uint64_t)dcost ^ (1ull << 63);
@@ -357,8 +664,8 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
       }
     }
     wave_sync();
-    int *qa = qcol + a * R;
-    int *qb = qcol + a2 * R;
+    int *qa = qcol + a * QS;
+    int *qb = qcol + a2 * QS;
     int rest = delta;
     if (p.cI > 0) {
       const int m_rt = imin(rest, qa[rt]);
@@ -381,7 +688,7 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
         qa[s] -= m;
         qb[s] += m;
       }
-      const int total = __shfl(incl, 63);
+      const int total = readlane_i32(incl, 63);
       rest -= total < rest ? total : rest;
     }
     wave_sync();
@@ -399,13 +706,132 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
   }
 }
 
+// Stage-1 candidate key: (D descending, e ascending) as one unsigned
+// 64-bit value, smaller first.  This is the order of the benefit
+// b = 2 D S - W descending (S > 0), ties to the lower expert id.
+__device__ inline uint64_t cand_key(int D, int e) {
+  return ((uint64_t)(uint32_t)(0x7FFFFFFF - D) << 32) | (uint32_t)e;
+}
+
+// Rank of candidate c among the nc keys of its domain (keys are distinct);
+// the first cap ranks name the domain's stage-1 replicas.
+__device__ inline void rank_candidates(int c, int nc, int cap, const uint64_t *keys, int *out) {
+  const uint64_t kc = keys[c];
+  int rank = 0;
+  int c2 = 0;
+  for (; c2 + 8 <= nc; c2 += 8) {
+    uint64_t k[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) k[u] = keys[c2 + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) rank += k[u] < kc;
+  }
+  for (; c2 < nc; ++c2) rank += keys[c2] < kc;
+  if (rank < cap) out[rank] = (int)(uint32_t)kc;
+}
+
+// Builds this rank's per-expert instance list (instances with a nonzero
+// share of its assignments, ascending rank, cumulative shares) from the
+// q columns of every domain, and writes it to the workspace.  All LDS.
+// e_of/qcol address instance (d, a) as d * I + a; scratch holds
+// E + 2 + E * RW + 2 * nent_cap + 64 words.
+__device__ void build_instance_list(const Plan &p, const int *e_of, const int *qcol, int *scratch) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int E = p.E, I = p.I, G = p.G;
+  int *cnt = scratch;                                              // E + 1
+  uint32_t *bm = reinterpret_cast<uint32_t *>(scratch + E + 2);   // E * RW
+  int *ent_r = scratch + E + 2 + E * p.RW;                         // nent_cap
+  int *ent_q = ent_r + p.nent_cap;                                 // nent_cap
+  int *tmp = ent_q + p.nent_cap;                                   // scan scratch
+  for (int e = tid; e <= E; e += nt) cnt[e] = 0;
+  for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
+  lds_barrier();
+  const int n_inst = p.M * I;
+  for (int idx = tid; idx < n_inst; idx += nt) {
+    const int e = e_of[idx];
+    if (e < 0) continue;
+    const int q = qcol[idx * p.QS + p.self];
+    if (q <= 0) continue;
+    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+    const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
+    atomicAdd(&cnt[e], 1);
+    atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
+  }
+  lds_barrier();
+  block_excl_scan(cnt, E + 1, tmp);
+  for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
+  for (int idx = tid; idx < n_inst; idx += nt) {
+    const int e = e_of[idx];
+    if (e < 0) continue;
+    const int q = qcol[idx * p.QS + p.self];
+    if (q <= 0) continue;
+    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+    const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
+    const uint32_t *row = bm + e * p.RW;
+    int pos = 0;
+    for (int w = 0; w < (r >> 5); ++w) pos += __popc(row[w]);
+    pos += __popc(row[r >> 5] & ((1u << (r & 31)) - 1u));
+    const int j = cnt[e] + pos;
+    ent_r[j] = r;
+    ent_q[j] = q;
+  }
+  lds_barrier();
+  for (int e = tid; e < E; e += nt) {
+    int run = 0;
+    for (int j = cnt[e]; j < cnt[e + 1]; ++j) {
+      run += ent_q[j];
+      p.csr_r[j] = ent_r[j];
+      p.csr_end[j] = run;
+    }
+  }
+}
+
+// Status bits and the sum of positive loads of Omega' (row self replaced by
+// the histogram hs) over rows [r0, r1) held at rows[(s - r0) * E + e];
+// wave-reduced, then one LDS atomic per wave into misc[0] (bits) and
+// misc[8..9] (total).  Called by every thread of the workgroup.
+__device__ void scan_rows(const Plan &p, int r0, int r1, const int *rows, const int *hs, int *misc) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
+  bool neg = false, diff = false;
+  uint64_t tot = 0;
+  const int n = (r1 - r0) * E;
+  for (int i = tid; i < n; i += nt) {
+    const int g = rows[i];
+    neg |= g < 0;
+    if (g > 0) tot += (uint64_t)g;
+  }
+  if (p.self >= r0 && p.self < r1) {
+    // row self: the plan uses the histogram instead of the gathered row
+    for (int e = tid; e < E; e += nt) {
+      const int g = rows[(p.self - r0) * E + e];
+      if (g > 0) tot -= (uint64_t)g;
+      if (hs[e] > 0) tot += (uint64_t)hs[e];
+      diff |= g != hs[e];
+    }
+  }
+  tot = wave_sum_u64(tot);
+  const uint64_t any_neg = __ballot(neg);
+  const uint64_t any_diff = __ballot(diff);
+  if (lane_id() == 0) {
+    const uint32_t w = (any_neg ? TOPOEP_ST_NEG_LOAD : 0u) | (any_diff ? TOPOEP_ST_SELF_DIFF : 0u);
+    if (w) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), w);
+    if (tot) atomicAdd(reinterpret_cast<unsigned long long *>(misc + 8), (unsigned long long)tot);
+  }
+}
+
+// ---------------------------------------------------------------- solver: one workgroup per domain
+
 __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   extern __shared__ int64_t smem_s[];
   int *sm = reinterpret_cast<int *>(smem_s);
-  const SolveLds lay = solve_lds(p);
-  int64_t *cb = reinterpret_cast<int64_t *>(sm + lay.cb);
+  if ((int)blockIdx.x >= p.n_solvers) {
+    block_offsets(p, blockIdx.x - p.n_solvers, sm);
+    return;
+  }
+  const DomainLds lay = domain_lds(p);
+  uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
   int *hs = sm + lay.hs;
-  int *ce = sm + lay.ce;
+  int *rows = sm + lay.rows;
   uint32_t *mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
   int *slots = sm + lay.slots;
   int *used = sm + lay.used;
@@ -415,124 +841,54 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   int *misc = sm + lay.misc;
   int *qcol = sm + lay.qcol;
   const int tid = threadIdx.x, nt = blockDim.x;
-  const int wg = blockIdx.x, nwg = gridDim.x;
+  const int wg = blockIdx.x, nwg = p.n_solvers;
   const int E = p.E, G = p.G, R = p.R, M = p.M, I = p.I, P = p.P, PN = p.PN, Neff = p.Neff;
   const int cap = p.cap1;
-  uint64_t *mtotal = reinterpret_cast<uint64_t *>(sm + lay.misc + 8);
 
-  // ---- row self of Omega: the histogram of local_topk (sum of the block
-  // partials); workgroup 0 also leaves the exclusive per-block offsets.
-  for (int e = tid; e < E; e += nt) {
-    int run = 0;
-    for (int b = 0; b < p.nb; ++b) {
-      const int v = p.partials[(int64_t)b * E + e];
-      if (wg == 0) p.offsets[(int64_t)b * E + e] = run;
-      run += v;
-    }
-    hs[e] = run;
-    if (wg == 0) p.hist[e] = run;
-  }
-  if (tid == 0) {
-    misc[0] = 0;
-    *mtotal = 0;
-  }
-  __syncthreads();
-  uint32_t st = 0;
-  if (wg == 0) {
+  if (tid < 16) misc[tid] = 0;
+  // ---- row self of Omega: the histogram of local_topk
+  hist_from_partials(p, hs, qcol);
+  if (wg == 0)
     for (int b = tid; b < p.nb; b += nt)
-      if (p.blk_err[b]) st |= TOPOEP_ST_BAD_ID;
-    for (int e = tid; e < E; e += nt)
-      if (p.gl[(int64_t)p.self * E + e] != hs[e]) st |= TOPOEP_ST_SELF_DIFF;
-  }
-  uint64_t tot = 0;
-  for (int d = wg; d < M; d += nwg) {
-    for (int i = tid; i < G * E; i += nt) {
-      const int s = d * G + i / E, e = i % E;
-      const int g = p.gl[(int64_t)s * E + e];
-      if (g < 0) st |= TOPOEP_ST_NEG_LOAD;
-      const int w = s == p.self ? hs[e] : g;
-      if (w > 0) tot += (uint64_t)w;
-    }
-  }
-  if (st) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), st);
-  if (tot) atomicAdd(reinterpret_cast<unsigned long long *>(mtotal), (unsigned long long)tot);
-  __syncthreads();
-  if (tid == 0) {
-    if (misc[0]) atomicOr(&p.ctrl[kCtrlStatus], (uint32_t)misc[0]);
-    if (*mtotal)
-      atomicAdd(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal), (unsigned long long)*mtotal);
-  }
+      if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
 
-  // ---- inter-node placement (Eq. 9), each domain independently.
+  // ---- inter-node placement (Eq. 9), each domain independently
   for (int d = wg; d < M; d += nwg) {
-    __syncthreads();
+    copy_to_lds(rows, p.gl + (int64_t)d * G * E, G * E);
     if (tid == 0) misc[1] = 0;
-    __syncthreads();
+    lds_barrier();
+    scan_rows(p, d * G, (d + 1) * G, rows, hs, misc);
     for (int e = tid; e < E; e += nt) {
-      if ((e / P) / G == d) continue;   // main inside the domain: never a candidate
-      uint64_t D = 0;
+      if ((int)fdiv((uint32_t)e, p.fGP) == d) continue;   // main inside the domain
+      int D = 0;
+#pragma unroll 8
       for (int j = 0; j < G; ++j) {
         const int s = d * G + j;
-        D += (uint64_t)(int64_t)(s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]);
+        D += s == p.self ? hs[e] : rows[j * E + e];
       }
-      // wrapping arithmetic: out-of-range inputs are flagged later and get no plan
-      const int64_t b = (int64_t)(2ull * D * (uint64_t)p.S - (uint64_t)p.W);
-      if (b > 0) {
+      if ((int64_t)2 * D * p.S > p.W) {
         const int pos = atomicAdd(&misc[1], 1);
-        ce[pos] = e;
-        cb[pos] = b;
+        ck[pos] = cand_key(D, e);
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int nc = misc[1];
-    // rank of each candidate in (b descending, e ascending) order; the i-th
-    // goes to rank d G + (i mod G), slot i / G: the domain rank with the
-    // fewest used slots, ties to the lowest rank
-    for (int c = tid; c < nc; c += nt) {
-      const int64_t bc = cb[c];
-      const int ec = ce[c];
-      int rank = 0;
-      for (int c2 = 0; c2 < nc; ++c2) {
-        const int64_t b2 = cb[c2];
-        rank += (b2 > bc) || (b2 == bc && ce[c2] < ec);
-      }
-      if (rank < cap) p.repl1[(int64_t)d * cap + rank] = ec;
-    }
+    for (int c = tid; c < nc; c += nt) rank_candidates(c, nc, cap, ck, p.repl1 + (int64_t)d * cap);
     for (int i = imin(nc, cap) + tid; i < cap; i += nt) p.repl1[(int64_t)d * cap + i] = -1;
+    lds_barrier();
+  }
+  if (tid == 0) {
+    if (misc[0]) atomicOr(&p.ctrl[kCtrlStatus], (uint32_t)misc[0]);
+    const unsigned long long t = *reinterpret_cast<unsigned long long *>(misc + 8);
+    if (t) atomicAdd(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal), t);
   }
 
   // ---- every domain's replicas are needed by every routing construction
   const bool synced = grid_barrier(&p.ctrl[kCtrlBar], (uint32_t)nwg, p.spin_limit, &misc[2]);
   uint32_t gst = __hip_atomic_load(&p.ctrl[kCtrlStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t total =
-      __hip_atomic_load(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal), __ATOMIC_RELAXED,
-                        __HIP_MEMORY_SCOPE_AGENT);
-  {
-    // exact-range check: total <= INT32_MAX and 4 S total c + c W < 2^62
-    const uint64_t lim = 1ull << 62;
-    const uint64_t cm = (uint64_t)imax(imax(p.cI, p.cX), 1);
-    bool range = total > 0x7FFFFFFFull;
-    uint64_t tokterm = 0;
-    if (!range && total > 0) {
-      uint64_t a = (uint64_t)p.S;
-      if (a > lim / 4) range = true;
-      else {
-        a *= 4;
-        if (a > lim / total) range = true;
-        else {
-          a *= total;
-          if (a > lim / cm) range = true;
-          else tokterm = a * cm;
-        }
-      }
-    }
-    if (!range) {
-      const uint64_t w = (uint64_t)p.W;
-      if (w > lim / cm) range = true;
-      else if (tokterm + w * cm >= lim) range = true;
-    }
-    if (range) gst |= TOPOEP_ST_RANGE;
-  }
+  const uint64_t total = __hip_atomic_load(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (out_of_range(p, total)) gst |= TOPOEP_ST_RANGE;
   if (!synced) gst |= TOPOEP_ST_SYNC;
   const bool noplan = (gst & kNoPlan) != 0 || !synced;
 
@@ -541,13 +897,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     for (int i = tid; i < E * p.MW; i += nt) mask[i] = 0;
     __syncthreads();
     for (int e = tid; e < E; e += nt) {
-      const int dm = (e / P) / G;
+      const int dm = (int)fdiv((uint32_t)e, p.fGP);
       atomicOr(&mask[e * p.MW + (dm >> 5)], 1u << (dm & 31));
     }
     for (int i = tid; i < M * cap; i += nt) {
       const int e = p.repl1[i];
       if ((unsigned)e < (unsigned)E) {
-        const int dd = i / cap;
+        const int dd = (int)fdiv((uint32_t)i, p.fCap);
         atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
       }
     }
@@ -572,78 +928,57 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       while (nsel < cap && (unsigned)p.repl1[(int64_t)d * cap + nsel] < (unsigned)E) ++nsel;
       misc[3] = nsel;
     }
-    __syncthreads();
+    lds_barrier();
     const int nsel = misc[3];
     for (int j = tid; j < G; j += nt) {
-      const int u = nsel > j ? (nsel - j + G - 1) / G : 0;
+      const int u = nsel > j ? (int)fdiv((uint32_t)(nsel - j + G - 1), p.fG) : 0;
       used[j] = u;
       for (int t = 0; t < Neff; ++t) slots[j * Neff + t] = t < u ? p.repl1[(int64_t)d * cap + t * G + j] : -1;
     }
-    __syncthreads();
+    lds_barrier();
     for (int a = tid; a < I; a += nt) {
-      const int j = a / PN, pos = a - j * PN;
+      const int j = (int)fdiv((uint32_t)a, p.fPN), pos = a - j * PN;
       int e;
       if (pos < P) e = (d * G + j) * P + pos;
       else e = (pos - P) < used[j] ? slots[j * Neff + pos - P] : -1;
       e_of[a] = e;
       U[a] = 0;
     }
-    __syncthreads();
-    // routing construction: the unique instance of e inside dom(s) takes all
-    // of omega[s][e]; sources of a domain without an instance split evenly
-    // over every instance (one per hosting domain, so the position in
-    // ascending rank order is the number of hosting domains below d)
-    for (int idx = tid; idx < I * R; idx += nt) {
-      const int s = idx / I, a = idx - s * I;
+    lds_barrier();
+    // the columns omega[s][e] of the domain's instances, then q in place
+    for (int t = tid; t < I * R; t += nt) {
+      const int s = (int)fdiv((uint32_t)t, p.fI), a = t - s * I;
       const int e = e_of[a];
-      int q = 0;
-      if (e >= 0) {
-        const int w = s == p.self ? hs[e] : p.gl[(int64_t)s * E + e];
-        if (w > 0) {
-          const int ds = s / G;
-          const uint32_t *me = mask + e * p.MW;
-          if (ds == d) {
-            q = w;
-          } else if (!((me[ds >> 5] >> (ds & 31)) & 1u)) {
-            int n = 0, below = 0;
-            for (int wd = 0; wd < p.MW; ++wd) {
-              const uint32_t bits = me[wd];
-              n += __popc(bits);
-              const int lo = wd * 32;
-              if (d >= lo + 32) below += __popc(bits);
-              else if (d > lo) below += __popc(bits & ((1u << (d - lo)) - 1u));
-            }
-            q = w / n + (below < w % n ? 1 : 0);
-          }
-        }
-      }
-      qcol[a * R + s] = q;
-      if (q) atomicAdd(&U[a], q);
+      qcol[a * p.QS + s] = e < 0 ? 0 : (s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]);
     }
-    __syncthreads();
+    lds_barrier();
+    route_instances(
+        p, I, p.fI, e_of, mask, qcol, U, [&](int i, int s, int) { return qcol[i * p.QS + s]; },
+        [&](int) { return d; });
+    lds_barrier();
     for (int j = tid; j < G; j += nt) {
       int l = 0;
       for (int pos = 0; pos < PN; ++pos) l += U[j * PN + pos];
       Lr[j] = l;
     }
-    __syncthreads();
+    lds_barrier();
     if (tid < 64) refine_domain(p, d, e_of, U, qcol, slots, used, Lr, &flags);
-    __syncthreads();
+    lds_barrier();
     // outputs of the domain's ranks
     for (int i = tid; i < G * p.N; i += nt) {
-      const int j = i / p.N, t = i - j * p.N;
+      const int j = (int)fdiv((uint32_t)i, p.fN), t = i - j * p.N;
       p.slots_out[(int64_t)(d * G + j) * p.N + t] = (t < used[j]) ? slots[j * Neff + t] : -1;
     }
     for (int j = tid; j < G; j += nt) {
       int sc = 0;
-      for (int pos = 0; pos < PN; ++pos) sc += qcol[(j * PN + pos) * R + p.self];
+      for (int pos = 0; pos < PN; ++pos) sc += qcol[(j * PN + pos) * p.QS + p.self];
       p.send_out[d * G + j] = sc;
     }
     for (int a = tid; a < I; a += nt) {
       p.seg_e[(int64_t)d * I + a] = e_of[a];
-      p.seg_q[(int64_t)d * I + a] = e_of[a] >= 0 ? qcol[a * R + p.self] : 0;
+      p.seg_q[(int64_t)d * I + a] = e_of[a] >= 0 ? qcol[a * p.QS + p.self] : 0;
     }
-    __syncthreads();
+    lds_barrier();
   }
   if (tid == 0 && (flags || !synced)) atomicOr(&p.ctrl[kCtrlStatus], flags | (synced ? 0u : TOPOEP_ST_SYNC));
 
@@ -666,21 +1001,20 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   for (int idx = tid; idx < M * I; idx += nt) {
     const int e = p.seg_e[idx], q = p.seg_q[idx];
     if ((unsigned)e < (unsigned)E && q > 0) {
-      const int d = idx / I, a = idx - d * I;
-      const int r = d * G + a / PN;
+      const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+      const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
       atomicAdd(&cnt[e], 1);
       atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
     }
   }
   __syncthreads();
-  const int nent = block_excl_scan(cnt, E + 1, tmp);
-  (void)nent;
+  block_excl_scan(cnt, E + 1, tmp);
   for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
   for (int idx = tid; idx < M * I; idx += nt) {
     const int e = p.seg_e[idx], q = p.seg_q[idx];
     if ((unsigned)e < (unsigned)E && q > 0) {
-      const int d = idx / I, a = idx - d * I;
-      const int r = d * G + a / PN;
+      const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+      const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
       const uint32_t *row = bm + e * p.RW;
       int pos = 0;
       for (int w = 0; w < (r >> 5); ++w) pos += __popc(row[w]);
@@ -706,6 +1040,160 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     p.status_out[0] = (int32_t)fin;
     p.ctrl[kCtrlBar] = 0;
     p.ctrl[kCtrlTicket] = 0;
+  }
+}
+
+// ---------------------------------------------------------------- solver: one workgroup for every domain
+
+// The same steps with every domain's state in the LDS of one CU; each
+// domain's refinement runs on its own wave.  Used when Omega and all q
+// columns fit in LDS.
+__global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
+  extern __shared__ int64_t smem_1[];
+  int *sm = reinterpret_cast<int *>(smem_1);
+  if (blockIdx.x > 0) {
+    block_offsets(p, blockIdx.x - 1, sm);
+    return;
+  }
+  const SingleLds lay = single_lds(p);
+  uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
+  int *hs = sm + lay.hs;
+  int *ccnt = sm + lay.cnt;
+  uint32_t *mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
+  int *repl = sm + lay.repl;
+  int *nsel = sm + lay.nsel;
+  int *slots = sm + lay.slots;
+  int *used = sm + lay.used;
+  int *Lr = sm + lay.L;
+  int *e_of = sm + lay.e_of;
+  int *U = sm + lay.U;
+  int *misc = sm + lay.misc;
+  int *om = sm + lay.om;
+  int *qcol = sm + lay.qcol;
+  const int tid = threadIdx.x, nt = blockDim.x, wave = tid >> 6, nw = nt >> 6;
+  const int E = p.E, G = p.G, R = p.R, M = p.M, I = p.I, P = p.P, PN = p.PN, Neff = p.Neff;
+  const int cap = p.cap1;
+
+  if (tid < 16) misc[tid] = 0;
+  for (int d = tid; d < M; d += nt) ccnt[d] = 0;
+  // ---- Omega to LDS; histogram of local_topk from the blocks' partials
+  copy_to_lds(om, p.gl, R * E);
+  hist_from_partials(p, hs, qcol);
+  for (int b = tid; b < p.nb; b += nt)
+    if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
+  scan_rows(p, 0, R, om, hs, misc);
+  lds_barrier();
+  for (int e = tid; e < E; e += nt) om[p.self * E + e] = hs[e];
+  uint32_t gst = (uint32_t)misc[0];
+  if (out_of_range(p, *reinterpret_cast<unsigned long long *>(misc + 8))) gst |= TOPOEP_ST_RANGE;
+  if (gst & kNoPlan) {
+    for (int i = tid; i < R * p.N; i += nt) p.slots_out[i] = -1;
+    for (int r = tid; r < R; r += nt) p.send_out[r] = 0;
+    if (tid == 0) {
+      p.ctrl[kCtrlFinal] = gst;
+      p.status_out[0] = (int32_t)gst;
+    }
+    return;
+  }
+  lds_barrier();
+
+  // ---- inter-node placement (Eq. 9), every domain at once
+  for (int idx = tid; idx < M * E; idx += nt) {
+    const int d = (int)fdiv((uint32_t)idx, p.fE), e = idx - d * E;
+    if ((int)fdiv((uint32_t)e, p.fGP) == d) continue;   // main inside the domain
+    int D = 0;
+#pragma unroll 8
+    for (int j = 0; j < G; ++j) D += om[(d * G + j) * E + e];
+    if ((int64_t)2 * D * p.S > p.W) {
+      const int pos = atomicAdd(&ccnt[d], 1);
+      ck[d * E + pos] = cand_key(D, e);
+    }
+  }
+  lds_barrier();
+  for (int idx = tid; idx < M * E; idx += nt) {
+    const int d = (int)fdiv((uint32_t)idx, p.fE), c = idx - d * E;
+    const int nc = ccnt[d];
+    if (c < nc) rank_candidates(c, nc, cap, ck + d * E, repl + d * cap);
+  }
+  for (int i = tid; i < M * cap; i += nt) {
+    const int d = (int)fdiv((uint32_t)i, p.fCap), c = i - d * cap;
+    if (c >= ccnt[d]) repl[i] = -1;
+  }
+  for (int i = tid; i < E * p.MW; i += nt) mask[i] = 0;
+  lds_barrier();
+
+  // ---- hosting domains per expert; every rank's slots and instances
+  for (int e = tid; e < E; e += nt) {
+    const int dm = (int)fdiv((uint32_t)e, p.fGP);
+    atomicOr(&mask[e * p.MW + (dm >> 5)], 1u << (dm & 31));
+  }
+  for (int i = tid; i < M * cap; i += nt) {
+    const int e = repl[i];
+    if (e >= 0) {
+      const int dd = (int)fdiv((uint32_t)i, p.fCap);
+      atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
+    }
+  }
+  for (int d = tid; d < M; d += nt) nsel[d] = imin(ccnt[d], cap);
+  lds_barrier();
+  for (int r = tid; r < R; r += nt) {
+    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+    const int ns = nsel[d];
+    const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
+    used[r] = u;
+    for (int t = 0; t < Neff; ++t) slots[r * Neff + t] = t < u ? repl[d * cap + t * G + j] : -1;
+  }
+  lds_barrier();
+  for (int idx = tid; idx < M * I; idx += nt) {
+    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+    const int j = (int)fdiv((uint32_t)a, p.fPN), pos = a - j * PN;
+    const int r = d * G + j;
+    int e;
+    if (pos < P) e = r * P + pos;
+    else e = (pos - P) < used[r] ? slots[r * Neff + pos - P] : -1;
+    e_of[idx] = e;
+    U[idx] = 0;
+  }
+  lds_barrier();
+
+  // ---- routing construction (Section 4.3) for every domain's instances
+  route_instances(
+      p, M * I, p.fMI, e_of, mask, qcol, U, [&](int, int s, int e) { return om[s * E + e]; },
+      [&](int i) { return (int)fdiv((uint32_t)i, p.fI); });
+  lds_barrier();
+  for (int r = tid; r < R; r += nt) {
+    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+    int l = 0;
+    for (int pos = 0; pos < PN; ++pos) l += U[d * I + j * PN + pos];
+    Lr[r] = l;
+  }
+  lds_barrier();
+
+  // ---- intra-node refinement (Eq. 10): one wave per domain
+  uint32_t flags = 0;
+  for (int d = wave; d < M; d += nw)
+    refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff, used + d * G,
+                  Lr + d * G, &flags);
+  if (flags && lane_id() == 0) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
+  lds_barrier();
+
+  // ---- outputs
+  for (int i = tid; i < R * p.N; i += nt) {
+    const int r = (int)fdiv((uint32_t)i, p.fN), t = i - r * p.N;
+    p.slots_out[i] = t < used[r] ? slots[r * Neff + t] : -1;
+  }
+  for (int r = tid; r < R; r += nt) {
+    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+    int sc = 0;
+    for (int pos = 0; pos < PN; ++pos) sc += qcol[(d * I + j * PN + pos) * p.QS + p.self];
+    p.send_out[r] = sc;
+  }
+  build_instance_list(p, e_of, qcol, om);
+  lds_barrier();
+  if (tid == 0) {
+    const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
+    p.ctrl[kCtrlFinal] = fin;
+    p.status_out[0] = (int32_t)fin;
   }
 }
 
@@ -802,6 +1290,7 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 
 struct Shape {
   int ipt, bt, st;
+  int single;     // 1: one workgroup plans every domain
   size_t lds_hist, lds_solve, lds_reroute;
   int solve_groups;
 };
@@ -841,6 +1330,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.nbits = ceil_log2(E);
   q.cap1 = G * q.Neff;
   q.nent_cap = E + R * q.Neff;
+  q.QS = R | 1;   // odd row stride of the q columns: no LDS bank conflicts
   q.cI = t->cost_intra;
   q.cX = t->cost_inter;
   q.S = t->tok_bytes;
@@ -848,30 +1338,63 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.n = (int64_t)T * k;
   q.spin_limit = kSpinLimit;
   q.iter_limit = kIterLimit;
+  if ((int64_t)q.M * q.I * q.QS >= (1 << 30) || (int64_t)R * E >= (1 << 30)) return TOPOEP_ELIMIT;
+  q.fE = make_fastdiv((uint32_t)E);
+  q.fG = make_fastdiv((uint32_t)G);
+  q.fGP = make_fastdiv((uint32_t)(G * q.P));
+  q.fP = make_fastdiv((uint32_t)q.P);
+  q.fI = make_fastdiv((uint32_t)q.I);
+  q.fPN = make_fastdiv((uint32_t)q.PN);
+  q.fCap = make_fastdiv((uint32_t)imax(q.cap1, 1));
+  q.fG1 = make_fastdiv((uint32_t)imax(G - 1, 1));
+  q.fN = make_fastdiv((uint32_t)imax(N, 1));
+  q.fMI = make_fastdiv((uint32_t)(q.M * q.I));
+  for (int i = 1; i <= kSmallDiv; ++i) q.fsmall[i] = make_fastdiv((uint32_t)i);
+  q.fsmall[0] = q.fsmall[1];
 
   Shape s;
   s.ipt = lc && lc->items_per_thread ? lc->items_per_thread : 4;
   s.bt = lc && lc->block_threads ? lc->block_threads : 256;
-  s.st = lc && lc->solve_threads ? lc->solve_threads : 256;
+  s.st = lc && lc->solve_threads ? lc->solve_threads : 0;
+  const int solver = lc ? lc->solver : 0;
+  if (solver < 0 || solver > 2) return TOPOEP_EINVAL;
   if (!(s.ipt == 1 || s.ipt == 2 || s.ipt == 4 || s.ipt == 8)) return TOPOEP_EINVAL;
-  if (s.bt < 64 || s.bt > 1024 || s.bt % 64 || s.st < 64 || s.st > 1024 || s.st % 64) return TOPOEP_EINVAL;
+  if (s.bt < 64 || s.bt > 1024 || s.bt % 64) return TOPOEP_EINVAL;
+  if (s.st != 0 && (s.st < 64 || s.st > 1024 || s.st % 64)) return TOPOEP_EINVAL;
+  if (lc && lc->tiles_per_block < 0) return TOPOEP_EINVAL;
   const int64_t tile = (int64_t)s.bt * s.ipt;
   const int64_t tiles = (q.n + tile - 1) / tile;
   int64_t tpb = lc && lc->tiles_per_block > 0 ? lc->tiles_per_block
                                               : (tiles + kTargetBlocks - 1) / kTargetBlocks;
-  if (lc && lc->tiles_per_block < 0) return TOPOEP_EINVAL;
   if (tpb < 1) tpb = 1;
   q.chunk = tpb * tile;
   const int64_t nb = q.n > 0 ? (q.n + q.chunk - 1) / q.chunk : 1;
   if (nb > (1 << 24)) return TOPOEP_ELIMIT;
   q.nb = (int)nb;
+  q.n_helpers = (E + kOffsetExperts - 1) / kOffsetExperts;
 
-  const SolveLds lay = solve_lds(q);
-  s.lds_solve = (size_t)lay.words * 4;
+  // the single-workgroup solver when its whole state fits in LDS
+  const int64_t single_words = (int64_t)single_lds(q).words;
+  const int64_t multi_words = (int64_t)domain_lds(q).words;
+  const bool single_fits = single_words * 4 <= kLdsLimit;
+  const bool multi_fits = multi_words * 4 <= kLdsLimit;
+  if (solver == 1) {
+    if (!single_fits) return TOPOEP_ELIMIT;
+    s.single = 1;
+  } else if (solver == 2) {
+    if (!multi_fits) return TOPOEP_ELIMIT;
+    s.single = 0;
+  } else {
+    if (!single_fits && !multi_fits) return TOPOEP_ELIMIT;
+    s.single = single_fits ? 1 : 0;
+  }
+  if (s.st == 0) s.st = s.single ? 1024 : 512;
+  s.lds_solve = (size_t)(s.single ? single_words : multi_words) * 4;
+  q.n_solvers = s.single ? 1 : imin(q.M, kMaxSolveGroups);
+  s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
   s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap) * 4;
-  if (s.lds_solve > (size_t)kLdsLimit || s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
-  s.solve_groups = imin(q.M, kMaxSolveGroups);
+  if (s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
 
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -883,7 +1406,6 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   const size_t o_part = take((size_t)q.nb * E * 4);
   const size_t o_offs = take((size_t)q.nb * E * 4);
   const size_t o_berr = take((size_t)q.nb * 4);
-  const size_t o_hist = take((size_t)E * 4);
   const size_t o_repl = take((size_t)q.M * imax(q.cap1, 1) * 4);
   const size_t o_sege = take((size_t)q.M * q.I * 4);
   const size_t o_segq = take((size_t)q.M * q.I * 4);
@@ -896,7 +1418,6 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     q.partials = reinterpret_cast<int32_t *>(ws + o_part);
     q.offsets = reinterpret_cast<int32_t *>(ws + o_offs);
     q.blk_err = reinterpret_cast<int32_t *>(ws + o_berr);
-    q.hist = reinterpret_cast<int32_t *>(ws + o_hist);
     q.repl1 = reinterpret_cast<int32_t *>(ws + o_repl);
     q.seg_e = reinterpret_cast<int32_t *>(ws + o_sege);
     q.seg_q = reinterpret_cast<int32_t *>(ws + o_segq);
@@ -928,6 +1449,7 @@ void set_attrs() {
   allow_lds(reroute_kernel<4>);
   allow_lds(reroute_kernel<8>);
   allow_lds(solve_kernel);
+  allow_lds(solve_single_kernel);
   g_attrs_set = true;
 }
 
@@ -952,7 +1474,8 @@ void launch_reroute(const Plan &p, const Shape &s, hipStream_t st) {
 }
 
 void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
-  hipLaunchKernelGGL(solve_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
+  if (s.single) hipLaunchKernelGGL(solve_single_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
+  else hipLaunchKernelGGL(solve_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
 }
 
 int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_load,

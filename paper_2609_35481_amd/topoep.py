@@ -43,7 +43,8 @@ class Topology(ctypes.Structure):
 class Launch(ctypes.Structure):
     """topoep_launch: launch shape (results do not depend on it)."""
     _fields_ = [("items_per_thread", ctypes.c_int32), ("block_threads", ctypes.c_int32),
-                ("tiles_per_block", ctypes.c_int32), ("solve_threads", ctypes.c_int32)]
+                ("tiles_per_block", ctypes.c_int32), ("solve_threads", ctypes.c_int32),
+                ("solver", ctypes.c_int32)]
 
 
 class TopoepError(RuntimeError):

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol(tp):
 def test_struct_layout_matches_header(tp):
     assert ctypes.sizeof(tp.Topology) == 6 * 4 + 2 * 8
     assert tp.Topology.tok_bytes.offset == 24
-    assert ctypes.sizeof(tp.Launch) == 16
+    assert ctypes.sizeof(tp.Launch) == 20
 
 
 def base(tp, **kw):

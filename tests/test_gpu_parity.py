@@ -89,19 +89,25 @@ def test_worked_example(self_rank):
 
 # ---------------------------------------------------------------- random tiny
 
+SOLVERS = {"single": (0, 0, 0, 0, 1), "perdomain": (0, 0, 0, 0, 2)}
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
 @pytest.mark.parametrize("seed", range(150))
-def test_random_tiny(seed):
+def test_random_tiny(seed, solver):
     rng = np.random.default_rng(7000 + seed)
     t, omega, topks = random_instance(7000 + seed, big=bool(seed % 2))
     s = int(rng.integers(t.R))
     tk = topks[s]
     if tk.shape[0] == 0:
         tk = np.zeros((0, topks[0].shape[1] if topks[0].ndim == 2 else 1), np.int32)
-    both(t.R, t.G, t.E, s, t.cI, t.cX, t.S, t.W, t.N, omega, tk, what="tiny seed %d" % seed)
+    both(t.R, t.G, t.E, s, t.cI, t.cX, t.S, t.W, t.N, omega, tk, launch=SOLVERS[solver],
+         what="tiny seed %d %s" % (seed, solver))
 
 
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
 @pytest.mark.parametrize("seed", range(40))
-def test_random_refinement_heavy(seed):
+def test_random_refinement_heavy(seed, solver):
     """Several slots per rank, one hot expert per domain: long refinement."""
     rng = np.random.default_rng(9000 + seed)
     G = int(rng.choice([2, 4, 8]))
@@ -119,7 +125,8 @@ def test_random_refinement_heavy(seed):
     S = int(rng.integers(1, 64))
     W = int(rng.integers(1, 2 * S * 400))
     s = int(rng.integers(R))
-    both(R, G, E, s, cI, cX, S, W, N, omega, topks[s], what="refine seed %d" % seed)
+    both(R, G, E, s, cI, cX, S, W, N, omega, topks[s], launch=SOLVERS[solver],
+         what="refine seed %d %s" % (seed, solver))
 
 
 # ---------------------------------------------------------------- configurations
@@ -133,6 +140,15 @@ def test_config_full_size(name, layer, mb):
     cfg = workload.get(name)
     gl, tk = workload.make_layer(cfg, layer, mb, 0)
     both(*cfg_args(cfg, 0, gl, tk), what="%s layer %d mb %d" % (name, layer, mb))
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("name,layer", [("tiny", 0), ("mixtral", 3), ("qwen3", 2), ("dsv3", 1)])
+def test_config_both_solvers(name, layer, solver):
+    cfg = workload.get(name)
+    gl, tk = workload.make_layer(cfg, layer, 0, 0)
+    both(*cfg_args(cfg, 0, gl, tk, N=cfg.N + 2), launch=SOLVERS[solver],
+         what="%s layer %d %s" % (name, layer, solver))
 
 
 @pytest.mark.parametrize("name,N", [("dsv3", 4), ("dsv3", 8), ("qwen3", 6), ("mixtral", 3), ("stress", 8)])
@@ -253,8 +269,8 @@ def test_many_domains_more_than_solver_groups():
 
 # ---------------------------------------------------------------- determinism
 
-LAUNCHES = [(1, 64, 0, 64), (2, 128, 1, 128), (4, 256, 0, 256), (8, 256, 2, 512), (8, 1024, 0, 1024),
-            (1, 1024, 3, 64), (4, 512, 1, 256)]
+LAUNCHES = [(1, 64, 0, 64, 2), (2, 128, 1, 128, 1), (4, 256, 0, 256, 2), (8, 256, 2, 512, 1),
+            (8, 1024, 0, 1024, 2), (1, 1024, 3, 64, 1), (4, 512, 1, 256, 0)]
 
 
 @pytest.mark.parametrize("launch", LAUNCHES)
