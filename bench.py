@@ -183,7 +183,10 @@ def run_bench(args):
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
     dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev))
                   for gl, tk in inputs]
-    planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev) for _ in range(layers)]
+    launch = None
+    if args.solver or args.ipt or args.block_threads or args.tiles_per_block or args.solve_threads:
+        launch = (args.ipt, args.block_threads, args.tiles_per_block, args.solve_threads, args.solver)
+    planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev, launch=launch) for _ in range(layers)]
 
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
@@ -251,6 +254,7 @@ def run_bench(args):
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
+        "launch": launch,
         "config": {"workload": DESCR[cfg.name], "layers_per_step": layers, "tokens_per_rank": cfg.T,
                    "top_k": cfg.k, "ranks": cfg.R, "experts": cfg.E, "replica_slots": N,
                    "assignments_per_layer": cfg.T * cfg.k},
@@ -330,6 +334,11 @@ def main():
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-max-log2", type=int, default=28)
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")
+    ap.add_argument("--solver", type=int, default=0, help="0 auto, 1 one workgroup, 2 one per domain")
+    ap.add_argument("--ipt", type=int, default=0, help="ids per thread per tile (0 = default)")
+    ap.add_argument("--block-threads", type=int, default=0)
+    ap.add_argument("--tiles-per-block", type=int, default=0)
+    ap.add_argument("--solve-threads", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the planner is replicated per rank and has no "

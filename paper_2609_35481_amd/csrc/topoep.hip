@@ -58,7 +58,6 @@ constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
 constexpr int kOffsetExperts = 64;      // experts per offset workgroup
 constexpr uint32_t kSpinLimit = 1u << 24;
 constexpr uint32_t kIterLimit = 1u << 22;
-constexpr int kSmallDiv = 64;
 
 // ---------------------------------------------------------------- plan
 
@@ -70,7 +69,6 @@ struct Plan {
   int nb, n_solvers, n_helpers;
   uint32_t spin_limit, iter_limit;
   FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
-  FastDiv fsmall[kSmallDiv + 1];   // divisors 1..kSmallDiv (hosting-domain counts)
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   uint32_t *ctrl;
@@ -82,13 +80,14 @@ __host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
 
 // LDS layout of the one-workgroup-per-domain solver, in int32 words.
 struct DomainLds {
-  int ck, hs, rows, mask, slots, used, L, e_of, U, misc, qcol, words;
+  int ck, fdt, hs, rows, mask, slots, used, L, e_of, U, misc, qcol, words;
 };
 
 __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
   DomainLds l;
   int o = 0;
   l.ck = o;    o += 2 * p.E;                 // uint64 stage-1 candidate keys
+  l.fdt = o;   o += 2 * (p.M + 1);           // divisors 1..M
   l.hs = o;    o += p.E;                     // row self of Omega (histogram)
   l.rows = o;  o += p.G * p.E;               // Omega rows of the domain's sources
   l.mask = o;  o += p.E * p.MW;              // per expert: domains hosting it
@@ -107,13 +106,14 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
 
 // LDS layout of the single-workgroup solver: every domain's state at once.
 struct SingleLds {
-  int ck, hs, cnt, mask, repl, nsel, slots, used, L, e_of, U, misc, om, qcol, words;
+  int ck, fdt, hs, cnt, mask, repl, nsel, slots, used, L, e_of, U, misc, om, qcol, words;
 };
 
 __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   SingleLds l;
   int o = 0;
   l.ck = o;    o += 2 * p.M * p.E;            // uint64 stage-1 candidate keys per domain
+  l.fdt = o;   o += 2 * (p.M + 1);            // divisors 1..M
   l.hs = o;    o += p.E;                      // histogram of local_topk
   l.cnt = o;   o += p.M;                      // candidates per domain
   l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
@@ -309,6 +309,35 @@ __device__ void copy_to_lds(int *dst, const int *src, int n) {
   }
 }
 
+// make_fastdiv on the device without a 64-bit integer division: for
+// d < 2^21 the quotient 2^(31+l) / d is formed in double precision and
+// corrected to the exact floor with integer arithmetic.
+__device__ inline FastDiv make_fastdiv_dev(uint32_t d) {
+  if (d >= (1u << 21)) return make_fastdiv(d);
+  const uint32_t l = d <= 1 ? 0u : 32u - (uint32_t)__clz(d - 1);
+  const uint64_t x = 1ull << (31 + l);
+  uint64_t q = (uint64_t)((double)x / (double)d);
+  int64_t r = (int64_t)(x - q * d);
+  while (r < 0) {
+    --q;
+    r += d;
+  }
+  while (r >= (int64_t)d) {
+    ++q;
+    r -= d;
+  }
+  FastDiv f;
+  f.m = (uint32_t)(q + (r != 0));
+  f.sh = 31 + l;
+  return f;
+}
+
+// x / d with one high multiply (x < 2^31): m < 2^32 and sh >= 32 except for
+// d = 1, where the quotient is x.
+__device__ inline uint32_t fdiv_hi(uint32_t x, FastDiv f) {
+  return f.sh >= 32 ? (__umulhi(x, f.m) >> (f.sh - 32)) : x;
+}
+
 // Histogram of local_topk (row self of Omega) as the sum of the histogram
 // blocks' partials: thread (e, g) sums its share of the blocks with eight
 // loads in flight; scratch needs max(E, (blockDim / E) * E) words.
@@ -368,6 +397,84 @@ __device__ void hist_from_partials(const Plan &p, int *hs, int *scratch) {
     int sum = 0;
     for (int g = 0; g < groups; ++g) sum += scratch[g * E + e];
     hs[e] = sum;
+  }
+  lds_barrier();
+}
+
+// Load phase of the single-workgroup solver when the sizes are small
+// (E % 4 == 0, Omega at most 4 int4 and the partials at most 8 int4 per
+// thread): every global load (the histogram blocks' partials, Omega and the
+// blocks' error flags) is issued before any is used, branch-free with
+// clamped indices.  Fills om (Omega, row self replaced by the histogram) and
+// hs, and accumulates status bits and the total load in misc.
+__device__ inline bool load_fast_ok(const Plan &p) {
+  const int nt = blockDim.x, E4 = p.E >> 2;
+  if ((p.E & 3) || E4 > nt || ((reinterpret_cast<uintptr_t>(p.gl)) & 15)) return false;
+  const int G4 = nt / E4;
+  return (p.R * p.E) / 4 <= 4 * nt && (p.nb + G4 - 1) / G4 <= 8 && p.nb <= nt;
+}
+
+__device__ void load_fast(const Plan &p, int *om, int *hs, int *scratch, int *misc) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, R = p.R, nb = p.nb;
+  const int E4 = E >> 2, G4 = nt / E4;
+  const int n4 = (R * E) >> 2;
+  const int g = tid / E4, e4 = tid - g * E4;
+  const int4 *part4 = reinterpret_cast<const int4 *>(p.partials);
+  const int4 *gl4 = reinterpret_cast<const int4 *>(p.gl);
+  const int4 z = make_int4(0, 0, 0, 0);
+  int4 pv[8], ov[4];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int b = g + u * G4;
+    pv[u] = part4[(int64_t)imin(b, nb - 1) * E4 + e4];
+    if (b >= nb || g >= G4) pv[u] = z;
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) ov[u] = gl4[imin(tid + u * nt, n4 - 1)];
+  const int be = p.blk_err[imin(tid, nb - 1)];
+  // Omega to LDS; negative entries and the total of positive loads
+  int4 *om4 = reinterpret_cast<int4 *>(om);
+  bool neg = false;
+  uint64_t tot = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = tid + u * nt;
+    if (i < n4) {
+      om4[i] = ov[u];
+      neg |= (ov[u].x | ov[u].y | ov[u].z | ov[u].w) < 0;
+      tot += (uint64_t)(ov[u].x > 0 ? ov[u].x : 0) + (uint64_t)(ov[u].y > 0 ? ov[u].y : 0) +
+             (uint64_t)(ov[u].z > 0 ? ov[u].z : 0) + (uint64_t)(ov[u].w > 0 ? ov[u].w : 0);
+    }
+  }
+  int4 s = z;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    s.x += pv[u].x;
+    s.y += pv[u].y;
+    s.z += pv[u].z;
+    s.w += pv[u].w;
+  }
+  if (g < G4) reinterpret_cast<int4 *>(scratch)[g * E4 + e4] = s;
+  lds_barrier();
+  // histogram; row self of Omega := histogram
+  bool diff = false;
+  for (int e = tid; e < E; e += nt) {
+    int h = 0;
+    for (int gg = 0; gg < G4; ++gg) h += scratch[gg * E + e];
+    hs[e] = h;
+    const int gself = om[p.self * E + e];
+    diff |= gself != h;
+    if (gself > 0) tot -= (uint64_t)gself;
+    if (h > 0) tot += (uint64_t)h;
+    om[p.self * E + e] = h;
+  }
+  tot = wave_sum_u64(tot);
+  const uint64_t any_neg = __ballot(neg), any_diff = __ballot(diff), any_bad = __ballot(tid < nb && be != 0);
+  if (lane_id() == 0) {
+    const uint32_t w = (any_neg ? TOPOEP_ST_NEG_LOAD : 0u) | (any_diff ? TOPOEP_ST_SELF_DIFF : 0u) |
+                       (any_bad ? TOPOEP_ST_BAD_ID : 0u);
+    if (w) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), w);
+    if (tot) atomicAdd(reinterpret_cast<unsigned long long *>(misc + 8), (unsigned long long)tot);
   }
   lds_barrier();
 }
@@ -509,7 +616,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
 // U[i] += sum_s q (U must be zero on entry).
 template <class WOf, class DomOf>
 __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, const int *e_of, const uint32_t *mask,
-                                int *qcol, int *U, WOf w_of, DomOf dom_of) {
+                                const FastDiv *fdt, int *qcol, int *U, WOf w_of, DomOf dom_of) {
   const int tid = threadIdx.x, nt = blockDim.x, G = p.G, M = p.M;
   const int chunks = imax(1, imin(M, nt / imax(NI, 1)));
   const int dpc = (M + chunks - 1) / chunks;
@@ -532,32 +639,32 @@ __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, const int *e
       if (d >= lo + 32) below += __popc(bits);
       else if (d > lo) below += __popc(bits & ((1u << (d - lo)) - 1u));
     }
-    const FastDiv fn = n <= kSmallDiv ? p.fsmall[n] : make_fastdiv((uint32_t)n);
+    const FastDiv fn = fdt[n];
     int usum = 0;
     for (int ds = ds0; ds < ds1; ++ds) {
       const int s0 = ds * G;
-      if (ds == d) {
+      // local: the unique instance in the source's domain takes w; another
+      // hosting domain: nothing; otherwise the even split
+      const bool local = ds == d;
+      const bool zero = !local && ((me[ds >> 5] >> (ds & 31)) & 1u);
 #pragma unroll 8
-        for (int j = 0; j < G; ++j) {
-          const int w = w_of(i, s0 + j, e);
-          row[s0 + j] = w;
-          usum += w;
-        }
-      } else if ((me[ds >> 5] >> (ds & 31)) & 1u) {
-        for (int j = 0; j < G; ++j) row[s0 + j] = 0;
-      } else {
-#pragma unroll 8
-        for (int j = 0; j < G; ++j) {
-          const int w = w_of(i, s0 + j, e);
-          const int qq = (int)fdiv((uint32_t)w, fn);
-          const int q = qq + (below < w - qq * n ? 1 : 0);
-          row[s0 + j] = q;
-          usum += q;
-        }
+      for (int j = 0; j < G; ++j) {
+        const int w = w_of(i, s0 + j, e);
+        const int qq = (int)fdiv_hi((uint32_t)w, fn);
+        const int split = qq + (below < w - qq * n ? 1 : 0);
+        const int q = local ? w : (zero ? 0 : split);
+        row[s0 + j] = q;
+        usum += q;
       }
     }
     if (usum) atomicAdd(&U[i], usum);
   }
+}
+
+// Divisors 1..M (hosting-domain counts) for the routing's even splits,
+// built once per workgroup into fdt[0..M].
+__device__ inline void build_divisors(int M, FastDiv *fdt) {
+  for (int n = threadIdx.x; n <= M; n += blockDim.x) fdt[n] = make_fastdiv_dev((uint32_t)(n > 0 ? n : 1));
 }
 
 // Instance index of expert e on local rank j of domain d, or -1.
@@ -572,24 +679,43 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 }
 
 // Intra-node refinement of domain d (Section 4.3, Eq. 10), by one wave.
-// e_of/U/qcol/slots/used/Lr point at the domain's own state.  Each
-// iteration picks the busiest rank rb (ties to the lowest rank), scores
-// every (instance of rb, other rank of the domain) candidate with key
-// (delta desc, L[rt] asc, cost change asc, e asc, rt asc), and commits the
-// best one.  The moved assignments come from sources in ascending
-// (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt itself,
-// then the other sources ascending, then rb (or plain ascending when the
-// intra-domain cost is zero).  The loop ends when no candidate has
+// e_of/U/qcol/slots/used/Lr point at the domain's own state; em (E words of
+// 64 bits, scratch) receives, per expert, the mask of the domain's local
+// ranks hosting it.  Each iteration picks the busiest rank rb (ties to the
+// lowest rank), scores every (instance of rb, other rank of the domain)
+// candidate with key (delta desc, L[rt] asc, cost change asc, e asc, rt asc),
+// and commits the best one.  The moved assignments come from sources in
+// ascending (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt
+// itself, then the other sources ascending, then rb (or plain ascending when
+// the intra-domain cost is zero).  The loop ends when no candidate has
 // delta >= 1.
 __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
-                              int *Lr, uint32_t *flags) {
+                              int *Lr, uint64_t *em, uint32_t *flags) {
   const int lane = lane_id();
-  const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS;
+  const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return;
   const int r0 = d * G;
+  // hosting masks per expert
+  for (int e = lane; e < E; e += 64) em[e] = 0;
+  wave_sync();
+  for (int a = lane; a < I; a += 64) {
+    const int e = e_of[a];
+    if (e >= 0) atomicOr(reinterpret_cast<unsigned long long *>(&em[e]), 1ull << (uint32_t)fdiv((uint32_t)a, p.fPN));
+  }
+  wave_sync();
   const int ncand = PN * (G - 1);
-  const FastDiv fG1 = p.fG1;
-  const int64_t twoS = 2 * p.S;
+  // the lane's first two candidates (instance position ai on rb, target index jj)
+  int ai0 = 0, jj0 = 0, ai1 = 0, jj1 = 0;
+  if (lane < ncand) {
+    ai0 = (int)fdiv((uint32_t)lane, p.fG1);
+    jj0 = lane - ai0 * (G - 1);
+  }
+  if (lane + 64 < ncand) {
+    ai1 = (int)fdiv((uint32_t)(lane + 64), p.fG1);
+    jj1 = lane + 64 - ai1 * (G - 1);
+  }
+  const int64_t tokc = 2 * p.S * (int64_t)p.cI;   // cost change per moved assignment and unit of (m_rb - m_rt)
+  const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
   for (uint32_t it = 0;; ++it) {
     if (it >= p.iter_limit) {
       if (lane == 0) *flags |= TOPOEP_ST_ITER;
@@ -603,34 +729,42 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
     const int Lrb = (int)(bkey >> 32);
     const int rb = r0 + rbj;
     uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull;
-    for (int c = lane; c < ncand; c += 64) {
-      const int ai = (int)fdiv((uint32_t)c, fG1), jj = c - ai * (G - 1);
+    int best_a = 0;
+    for (int c = lane, round = 0; c - lane < ncand; c += 64, ++round) {
+      if (c >= ncand) continue;
+      int ai, jj;
+      if (round == 0) {
+        ai = ai0;
+        jj = jj0;
+      } else if (round == 1) {
+        ai = ai1;
+        jj = jj1;
+      } else {
+        ai = (int)fdiv((uint32_t)c, p.fG1);
+        jj = c - ai * (G - 1);
+      }
       const int rtj = jj < rbj ? jj : jj + 1;
       const int a = rbj * PN + ai;
       const int e = e_of[a];
       const int u = U[a];
-      if (e < 0 || u <= 0) continue;
-      const int rt = r0 + rtj;
-      const int me = (int)fdiv((uint32_t)e, p.fP);
-      bool hosts = me == rt;
-      const int urt = used[rtj];
-      for (int t = 0; t < urt && !hosts; ++t) hosts = slots[rtj * Neff + t] == e;
-      if (!hosts && urt >= Neff) continue;
       const int Lrt = Lr[rtj];
+      const int urt = used[rtj];
+      if (e < 0 || u <= 0) continue;
       const int64_t gap = (int64_t)Lrb - Lrt;
       if (gap < 2) continue;
+      const bool hosts = (em[e] >> rtj) & 1ull;
+      if (!hosts && urt >= Neff) continue;
+      const int rt = r0 + rtj;
       const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
-      int64_t dtok = 0;
+      int64_t dcost = 0;
       if (p.cI > 0) {
         const int qrt = qcol[a * QS + rt], qrb = qcol[a * QS + rb];
         const int m_rt = imin(delta, qrt);
         const int rest = delta - m_rt;
-        const int m_oth = imin(rest, u - qrt - qrb);
-        const int m_rb = rest - m_oth;
-        dtok = (int64_t)p.cI * (int64_t)(m_rb - m_rt);
+        const int m_rb = rest - imin(rest, u - qrt - qrb);
+        dcost = tokc * (int64_t)(m_rb - m_rt);
       }
-      const int64_t crep = ((int)fdiv((uint32_t)me, p.fG) == d) ? p.cI : p.cX;   // me != rt when !hosts
-      const int64_t dcost = twoS * dtok + (hosts ? 0 : crep * p.W);
+      if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
       const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
       const uint64_t c2 = (uint64_t)dcost ^ (1ull << 63);
       const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)rt;
@@ -638,20 +772,28 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
         k1 = c1;
         k2 = c2;
         k3 = c3;
+        best_a = a;
       }
     }
-    wave_argmin3(k1, k2, k3);
-    if (k1 == ~0ull) break;
-    const int delta = 0x7FFFFFFF - (int)(k1 >> 32);
-    const int e = (int)(k3 >> 32);
-    const int rt = (int)(uint32_t)k3;
-    const int rtj = rt - r0;
-    const int a = instance_of(p, d, rbj, e, slots, used);
-    int a2 = instance_of(p, d, rtj, e, slots, used);
-    if (a < 0) {   // cannot happen: the candidate came from an instance of rb
-      if (lane == 0) *flags |= TOPOEP_ST_ITER;
-      break;
+    const uint64_t m1 = wave_min_u64(k1);
+    if (m1 == ~0ull) break;
+    uint64_t win = __ballot(k1 == m1);
+    if (__popcll(win) != 1) {
+      const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
+      win &= __ballot(k2 == m2);
+      if (__popcll(win) != 1) {
+        const uint64_t m3 = wave_min_u64((k1 == m1 && k2 == m2) ? k3 : ~0ull);
+        win &= __ballot(k3 == m3);
+      }
     }
+    const int wl = __ffsll((long long)win) - 1;
+    const int delta = 0x7FFFFFFF - (int)(readlane64(k1, wl) >> 32);
+    const uint64_t kw = readlane64(k3, wl);
+    const int e = (int)(kw >> 32);
+    const int rt = (int)(uint32_t)kw;
+    const int rtj = rt - r0;
+    const int a = readlane_i32(best_a, wl);
+    int a2 = instance_of(p, d, rtj, e, slots, used);
     wave_sync();
     if (a2 < 0) {
       // new replica in the first free slot of rt
@@ -661,6 +803,7 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
         slots[rtj * Neff + t] = e;
         used[rtj] = t + 1;
         e_of[a2] = e;
+        em[e] |= 1ull << rtj;
       }
     }
     wave_sync();
@@ -830,6 +973,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   }
   const DomainLds lay = domain_lds(p);
   uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
+  FastDiv *fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
   int *hs = sm + lay.hs;
   int *rows = sm + lay.rows;
   uint32_t *mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
@@ -846,6 +990,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   const int cap = p.cap1;
 
   if (tid < 16) misc[tid] = 0;
+  build_divisors(M, fdt);
   // ---- row self of Omega: the histogram of local_topk
   hist_from_partials(p, hs, qcol);
   if (wg == 0)
@@ -953,7 +1098,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     }
     lds_barrier();
     route_instances(
-        p, I, p.fI, e_of, mask, qcol, U, [&](int i, int s, int) { return qcol[i * p.QS + s]; },
+        p, I, p.fI, e_of, mask, fdt, qcol, U, [&](int i, int s, int) { return qcol[i * p.QS + s]; },
         [&](int) { return d; });
     lds_barrier();
     for (int j = tid; j < G; j += nt) {
@@ -962,7 +1107,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       Lr[j] = l;
     }
     lds_barrier();
-    if (tid < 64) refine_domain(p, d, e_of, U, qcol, slots, used, Lr, &flags);
+    if (tid < 64) refine_domain(p, d, e_of, U, qcol, slots, used, Lr, ck, &flags);
     lds_barrier();
     // outputs of the domain's ranks
     for (int i = tid; i < G * p.N; i += nt) {
@@ -1057,6 +1202,7 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
   }
   const SingleLds lay = single_lds(p);
   uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
+  FastDiv *fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
   int *hs = sm + lay.hs;
   int *ccnt = sm + lay.cnt;
   uint32_t *mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
@@ -1076,14 +1222,20 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
 
   if (tid < 16) misc[tid] = 0;
   for (int d = tid; d < M; d += nt) ccnt[d] = 0;
+  build_divisors(M, fdt);
   // ---- Omega to LDS; histogram of local_topk from the blocks' partials
-  copy_to_lds(om, p.gl, R * E);
-  hist_from_partials(p, hs, qcol);
-  for (int b = tid; b < p.nb; b += nt)
-    if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
-  scan_rows(p, 0, R, om, hs, misc);
   lds_barrier();
-  for (int e = tid; e < E; e += nt) om[p.self * E + e] = hs[e];
+  if (load_fast_ok(p)) {
+    load_fast(p, om, hs, qcol, misc);
+  } else {
+    copy_to_lds(om, p.gl, R * E);
+    hist_from_partials(p, hs, qcol);
+    for (int b = tid; b < p.nb; b += nt)
+      if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
+    scan_rows(p, 0, R, om, hs, misc);
+    lds_barrier();
+    for (int e = tid; e < E; e += nt) om[p.self * E + e] = hs[e];
+  }
   uint32_t gst = (uint32_t)misc[0];
   if (out_of_range(p, *reinterpret_cast<unsigned long long *>(misc + 8))) gst |= TOPOEP_ST_RANGE;
   if (gst & kNoPlan) {
@@ -1158,7 +1310,7 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
 
   // ---- routing construction (Section 4.3) for every domain's instances
   route_instances(
-      p, M * I, p.fMI, e_of, mask, qcol, U, [&](int, int s, int e) { return om[s * E + e]; },
+      p, M * I, p.fMI, e_of, mask, fdt, qcol, U, [&](int, int s, int e) { return om[s * E + e]; },
       [&](int i) { return (int)fdiv((uint32_t)i, p.fI); });
   lds_barrier();
   for (int r = tid; r < R; r += nt) {
@@ -1173,7 +1325,7 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
   uint32_t flags = 0;
   for (int d = wave; d < M; d += nw)
     refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff, used + d * G,
-                  Lr + d * G, &flags);
+                  Lr + d * G, ck + (int64_t)d * E, &flags);
   if (flags && lane_id() == 0) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
   lds_barrier();
 
@@ -1349,8 +1501,6 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.fG1 = make_fastdiv((uint32_t)imax(G - 1, 1));
   q.fN = make_fastdiv((uint32_t)imax(N, 1));
   q.fMI = make_fastdiv((uint32_t)(q.M * q.I));
-  for (int i = 1; i <= kSmallDiv; ++i) q.fsmall[i] = make_fastdiv((uint32_t)i);
-  q.fsmall[0] = q.fsmall[1];
 
   Shape s;
   s.ipt = lc && lc->items_per_thread ? lc->items_per_thread : 4;
