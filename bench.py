@@ -1,17 +1,20 @@
 """Benchmark of the TopoEP planner on one MI355X.
 
-A step plans every MoE layer of one microbatch: for each layer, the
-histogram, solver and reroute kernels run back to back on one stream, all
-layers captured in one HIP graph (the layers are planned one after another,
-as they would be in a forward pass).  Inputs (the synthetic routing matrix
-and this rank's top-k ids of every layer) are resident in HBM before the
-timed region.
+A step plans every MoE layer of one microbatch: for each layer the plan's
+kernels (one launch when the single-workgroup solver fits, else histogram,
+solver and reroute) run on one stream, all layers captured in one HIP graph
+(the layers are planned one after another, as they would be in a forward
+pass).  Inputs (the synthetic routing matrix and this rank's top-k ids of
+every layer) are resident in HBM before the timed region.
 
 Printed JSON line: value = rerouted assignments per second over the whole
 step; plan_latency_us_per_layer = step time / layers.  ``roofline`` covers
 the kernel with the longest average duration, timed with HIP events on the
-stream it runs on; ``cpu_baseline`` times the CPU oracle on a bounded sample
-of the same workload on this host.
+stream it runs on; ``launch_floor_us_per_layer`` is the same graph of empty
+kernels with the plan's grid, threads and LDS; ``cpu_baseline`` times the
+CPU oracle on a bounded sample of the same workload on this host (one
+thread, then every core, then the host-planning path of Eq. 1: copy the
+inputs to the host, plan there, copy the outputs back).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config dsv3]
        python bench.py --sweep    (histogram/reroute bandwidth sweep)
@@ -59,13 +62,22 @@ def make_inputs(cfg, layers, mb=0, workers=None):
     return [_gen(j) for j in jobs]
 
 
-def algorithmic_bytes(cfg, N):
-    """Bytes the method must move per layer, by kernel."""
+STAGE_NAMES = {1: ("plan",), 3: ("hist", "solve", "reroute")}
+
+
+def algorithmic_bytes(cfg, N, kernels):
+    """Bytes the method must move per layer, by kernel: the ids once per
+    kernel that reads them, Omega, the destinations and the small outputs
+    (slots, send counts, two status words)."""
     a = cfg.T * cfg.k
+    omega = 4 * cfg.R * cfg.E
+    outs = 4 * cfg.R * (N + 1) + 8
+    if kernels == 1:
+        return {"plan": 4 * a + omega + 4 * a + outs}   # ids read once, held in registers
     return {
-        "hist": 4 * a,                                   # read the ids
-        "solve": 4 * cfg.R * cfg.E + 4 * cfg.R * (N + 1),  # read Omega, write slots and counts
-        "reroute": 8 * a,                                # read the ids, write destinations
+        "hist": 4 * a,              # read the ids
+        "solve": omega + outs,      # read Omega, write slots, counts, status
+        "reroute": 8 * a,           # read the ids again, write destinations
     }
 
 
@@ -98,6 +110,13 @@ def measured_traffic(workload_name, kernel):
     return val
 
 
+def launch_from_args(args):
+    """The launch shape the options ask for (None = the library's choice)."""
+    if args.solver or args.ipt or args.block_threads or args.tiles_per_block or args.solve_threads:
+        return (args.ipt, args.block_threads, args.tiles_per_block, args.solve_threads, args.solver)
+    return None
+
+
 def run_pmc_pass(args):
     """Workload for counter runs: one plan of every layer, then each kernel
     of the plan alone over every layer (--stage-reps times), then a plain
@@ -112,10 +131,11 @@ def run_pmc_pass(args):
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
     dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev))
                   for gl, tk in inputs]
-    planners = [topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=dev) for _ in range(layers)]
+    launch = launch_from_args(args)
+    planners = [topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=dev, launch=launch) for _ in range(layers)]
     for p, (g, t) in zip(planners, dev_inputs):
         p.plan(g, t)
-    for sid in (0, 1, 2):
+    for sid in range(planners[0].shape.kernels):
         for _ in range(args.stage_reps):
             for p, (g, t) in zip(planners, dev_inputs):
                 p.stage(sid, g, t)
@@ -128,7 +148,26 @@ def run_pmc_pass(args):
                       "copy_bytes": src.numel() * 4, "kernel_source_sha1": source_digest()}), flush=True)
 
 
-def cpu_baseline(cfg, inputs, budget_s=15.0):
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cpu_baseline(cfg, inputs, budget_s=15.0, dev_inputs=None):
+    """The oracle timed on this host: (i) one thread, layers back to back
+    (the reported value); (ii) layers spread over every core this process
+    may use (threads: the oracle call releases the GIL); (iii) the
+    host-planning path of Eq. 1 for the same layers: synchronise and copy
+    Omega and the ids to pinned host memory, plan on the CPU, copy the
+    outputs back to the GPU."""
+    import concurrent.futures as cf
+
     import oracle
     n = 0
     t0 = time.perf_counter()
@@ -138,9 +177,55 @@ def cpu_baseline(cfg, inputs, budget_s=15.0):
         if time.perf_counter() - t0 > budget_s:
             break
     dt = time.perf_counter() - t0
-    return {"value": n * cfg.T * cfg.k / dt, "unit": "assignments/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d layers of the %s workload (planned back to back, one thread): "
-                      "%.0f us per layer" % (n, len(inputs), cfg.name, dt / n * 1e6)}
+    per_layer = dt / n
+    out = {"value": n * cfg.T * cfg.k / dt, "unit": "assignments/s", "cores": 1, "kind": "oracle",
+           "sample": "%d of %d layers of the %s workload (planned back to back, one thread): "
+                     "%.0f us per layer" % (n, len(inputs), cfg.name, per_layer * 1e6),
+           "cpu_model": _cpu_model()}
+    # (ii) every core: about budget/2 seconds of work
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    cores = max(1, min(cores, 64))
+    tasks = max(cores, min(20000, int(0.5 * budget_s / per_layer * cores)))
+    jobs = [inputs[i % len(inputs)] for i in range(tasks)]
+    t0 = time.perf_counter()
+    with cf.ThreadPoolExecutor(cores) as ex:
+        list(ex.map(lambda a: oracle.plan_cfg(cfg, a[0], a[1], 0), jobs))
+    dt2 = time.perf_counter() - t0
+    out["all_cores"] = {"value": tasks * cfg.T * cfg.k / dt2, "unit": "assignments/s", "threads": cores,
+                        "us_per_layer": dt2 / tasks * 1e6, "layers_planned": tasks}
+    # (iii) Eq. 1 host-planning path
+    if dev_inputs is not None:
+        import torch
+        dev = dev_inputs[0][0].device
+        m = min(len(dev_inputs), max(1, int(0.25 * budget_s / per_layer)))
+        gl_h = torch.empty(dev_inputs[0][0].shape, dtype=torch.int32, pin_memory=True)
+        tk_h = torch.empty(dev_inputs[0][1].shape, dtype=torch.int32, pin_memory=True)
+        slots_d = torch.empty((cfg.R, cfg.N), dtype=torch.int32, device=dev)
+        dest_d = torch.empty(dev_inputs[0][1].shape, dtype=torch.int32, device=dev)
+        sc_d = torch.empty((cfg.R,), dtype=torch.int32, device=dev)
+        t_sync = t_cpu = t_ret = 0.0
+        for i in range(m):
+            gd, td = dev_inputs[i]
+            torch.cuda.synchronize()
+            a = time.perf_counter()
+            gl_h.copy_(gd, non_blocking=True)
+            tk_h.copy_(td, non_blocking=True)
+            torch.cuda.synchronize()
+            b = time.perf_counter()
+            ref = oracle.plan_cfg(cfg, gl_h.numpy(), tk_h.numpy(), 0)
+            c = time.perf_counter()
+            slots_d.copy_(torch.from_numpy(ref["replica_slots"]))
+            dest_d.copy_(torch.from_numpy(ref["token_dest"]))
+            sc_d.copy_(torch.from_numpy(ref["send_counts"]))
+            torch.cuda.synchronize()
+            d = time.perf_counter()
+            t_sync += b - a
+            t_cpu += c - b
+            t_ret += d - c
+        out["host_plan_path"] = {"us_per_layer": (t_sync + t_cpu + t_ret) / m * 1e6,
+                                 "t_sync_us": t_sync / m * 1e6, "t_cpu_us": t_cpu / m * 1e6,
+                                 "t_return_us": t_ret / m * 1e6, "layers": m}
+    return out
 
 
 def time_stage(torch, planners, dev_inputs, stage, reps):
@@ -183,9 +268,7 @@ def run_bench(args):
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
     dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev))
                   for gl, tk in inputs]
-    launch = None
-    if args.solver or args.ipt or args.block_threads or args.tiles_per_block or args.solve_threads:
-        launch = (args.ipt, args.block_threads, args.tiles_per_block, args.solve_threads, args.solver)
+    launch = launch_from_args(args)
     planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev, launch=launch) for _ in range(layers)]
 
     stream = torch.cuda.Stream()
@@ -219,20 +302,26 @@ def run_bench(args):
     value = assign / (ms_per_step / 1e3)
 
     # every plan of the last replay must be a valid plan (status 0)
-    st = torch.stack([p.status for p in planners]).cpu().numpy().ravel()
-    if (st & ~topoep.ST_SELF_DIFF).any():
-        raise SystemExit("plan status bits set: %s" % np.unique(st))
+    st = torch.stack([p.status for p in planners]).cpu().numpy()
+    if (st[:, 0] & ~topoep.ST_SELF_DIFF).any():
+        raise SystemExit("plan status bits set: %s" % np.unique(st[:, 0]))
+    moves = st[:, 1].astype(np.int64)
 
-    # per-kernel durations (HIP events around each launch, eager, same stream)
+    # per-kernel durations (a graph of back-to-back launches of one kernel,
+    # HIP events on its stream), and the launch floor (empty kernels, same
+    # shapes, same graph structure)
+    shape = planners[0].shape
+    kernels = shape.kernels
     stages = {}
-    for name, sid in (("hist", 0), ("solve", 1), ("reroute", 2)):
+    for sid, name in enumerate(STAGE_NAMES[kernels]):
         stages[name] = time_stage(torch, planners, dev_inputs, sid, max(1, args.stage_reps))
+    floor_us = time_stage(torch, planners, dev_inputs, topoep.STAGE_FLOOR, max(1, args.stage_reps))
     # restore complete plans in every workspace
     for p, (g, t) in zip(planners, dev_inputs):
         p.plan(g, t)
     torch.cuda.synchronize()
 
-    nbytes = algorithmic_bytes(cfg, N)
+    nbytes = algorithmic_bytes(cfg, N, kernels)
     dom = max(stages, key=lambda k: stages[k])
     avg_us = stages[dom]
     achieved = nbytes[dom] / (avg_us * 1e-6) / 1e9
@@ -255,6 +344,7 @@ def run_bench(args):
         "dtype": "int32",
         "data": "synthetic",
         "launch": launch,
+        "plan_shape": shape.as_dict(),
         "config": {"workload": DESCR[cfg.name], "layers_per_step": layers, "tokens_per_rank": cfg.T,
                    "top_k": cfg.k, "ranks": cfg.R, "experts": cfg.E, "replica_slots": N,
                    "assignments_per_layer": cfg.T * cfg.k},
@@ -262,11 +352,14 @@ def run_bench(args):
         "plan_latency_us_per_layer_p10_p50_p90": [float(np.percentile(step_ms, q)) * 1e3 / layers
                                                   for q in (10, 50, 90)],
         "kernel_avg_us": {k: round(v, 3) for k, v in stages.items()},
+        "launch_floor_us_per_layer": round(floor_us, 3),
+        "refinement_moves_per_layer": {"mean": float(moves.mean()), "max": int(moves.max()),
+                                       "layers_with_moves": int((moves > 0).sum())},
         "roofline": roof,
         "input_generation_s": round(t_gen, 2),
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds, dev_inputs)
     return out
 
 
@@ -297,10 +390,11 @@ def run_sweep(args):
             gl = torch.randint(0, 1000, (R, E), dtype=torch.int32, device=dev)
             gl[0] = hist
             topo = topoep.topology(R, G, E, 0, 1, 8, 4096, 9 << 20)
-            pl = topoep.Planner(topo, T, k, 2, device=dev)
+            # the three-kernel path, so the histogram and reroute kernels run alone
+            pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_SINGLE))
             pl.plan(gl, tk_d)
             torch.cuda.synchronize()
-            st = int(pl.status.item())
+            st = int(pl.status[0].item())
             res = {}
             for name, sid, bpa in (("hist", 0, 4), ("reroute", 2, 8)):
                 reps = 5 if n >= (1 << 26) else 20
@@ -334,7 +428,8 @@ def main():
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-max-log2", type=int, default=28)
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")
-    ap.add_argument("--solver", type=int, default=0, help="0 auto, 1 one workgroup, 2 one per domain")
+    ap.add_argument("--solver", type=int, default=0,
+                    help="0 auto, 1 one solver workgroup, 2 one per domain, 3 one launch")
     ap.add_argument("--ipt", type=int, default=0, help="ids per thread per tile (0 = default)")
     ap.add_argument("--block-threads", type=int, default=0)
     ap.add_argument("--tiles-per-block", type=int, default=0)

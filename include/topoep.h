@@ -25,7 +25,9 @@
  *     may be captured in a HIP graph.  Outputs are valid once the stream
  *     reaches them.
  *   - One workspace serves one plan at a time: plans that share a workspace
- *     must be ordered on one stream.
+ *     must be ordered on one stream.  A workspace is zero-filled once before
+ *     its first plan (e.g. hipMemset after allocation); every plan leaves its
+ *     control words zero again, so no later clearing is needed.
  *   - main(e) = e / (E/R) (main instances spread contiguously and evenly,
  *     Section 3.2); dom(r) = r / G.  Cost c(s,r) = 0 if s == r, cost_intra
  *     inside a domain, cost_inter across domains (a two-level instance of
@@ -61,10 +63,33 @@ typedef struct topoep_launch {
   int32_t block_threads;    /* 64..1024, multiple of 64, for histogram/reroute    */
   int32_t tiles_per_block;  /* >= 1; 0 = choose from the problem size             */
   int32_t solve_threads;    /* 64..1024, multiple of 64, for the solver           */
-  int32_t solver;           /* 0 = choose, 1 = one workgroup for all domains       */
-                            /* (needs the whole state in LDS), 2 = one workgroup */
-                            /* per domain with a grid barrier                    */
+  int32_t solver;           /* 0 = choose (3 when it fits, else 1, else 2);       */
+                            /* 1 = three kernels (histogram, solver, reroute)    */
+                            /*     with one solver workgroup for all domains     */
+                            /*     (its whole state in LDS);                     */
+                            /* 2 = three kernels, one solver workgroup per       */
+                            /*     domain with a bounded grid barrier;           */
+                            /* 3 = one kernel: the solver workgroup of 1 plus at */
+                            /*     most 128 workgroups of solve_threads threads  */
+                            /*     holding items_per_thread ids each, which      */
+                            /*     count, wait (bounded) for the solver and      */
+                            /*     reroute; block_threads and tiles_per_block    */
+                            /*     are ignored                                   */
 } topoep_launch;
+
+/* Launch shape a plan will use (topoep_plan_shape). */
+typedef struct topoep_shape {
+  int32_t kernels;          /* kernels one plan enqueues: 1 (solver 3) or 3     */
+  int32_t solver;           /* 1, 2 or 3 as in topoep_launch.solver              */
+  int32_t items_per_thread; /* ids per thread of the histogram/reroute work      */
+  int32_t chunk_blocks;     /* workgroups holding ids                            */
+  int32_t grid[3];          /* workgroups of each kernel, in launch order        */
+  int32_t block[3];         /* threads per workgroup of each kernel              */
+  int32_t lds_bytes[3];     /* dynamic LDS of each kernel                        */
+} topoep_shape;
+
+/* topoep_plan_stage: the plan's kernels with empty bodies (launch floor). */
+#define TOPOEP_STAGE_FLOOR 3
 
 /* Host return codes. */
 #define TOPOEP_OK 0
@@ -85,7 +110,7 @@ typedef struct topoep_launch {
 #define TOPOEP_ST_SYNC 16u       /* a bounded in-kernel wait gave up (outputs wrong) */
 #define TOPOEP_ST_ITER 32u       /* refinement hit its iteration bound               */
 /* With BAD_ID, NEG_LOAD or RANGE no plan is made: replica_slots = -1,
- * send_counts = 0, token_dest = -1. */
+ * send_counts = 0, token_dest = -1, status[1] = 0. */
 
 /*
  * Bytes of device workspace topoep_plan needs for these sizes (default
@@ -99,6 +124,11 @@ int topoep_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k,
 int topoep_workspace_bytes_ex(const topoep_topology *topo, int32_t T, int32_t k,
                               int32_t replica_budget, const topoep_launch *launch,
                               size_t *bytes_out);
+
+/* The launch shape topoep_plan_ex would use for these sizes (host only;
+ * same return codes as topoep_workspace_bytes_ex). */
+int topoep_plan_shape(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
+                      const topoep_launch *launch, topoep_shape *out);
 
 /*
  * Enqueue one plan (Sections 3.1 and 4.3).
@@ -122,10 +152,12 @@ int topoep_workspace_bytes_ex(const topoep_topology *topo, int32_t T, int32_t k,
  *                  sum_{j<i} q[self][e][r_j] <= rho < sum_{j<=i} q[self][e][r_j].
  *                  May be NULL when T == 0.
  *   send_counts    device int32 out [R]: sum_e q[self][e][r].
- *   status         device int32 out [1]: TOPOEP_ST_* bits.
+ *   status         device int32 out [2]: [0] = TOPOEP_ST_* bits; [1] = the
+ *                  number of refinement moves committed (Eq. 10 transfers,
+ *                  summed over domains).
  *   workspace      device memory of at least topoep_workspace_bytes bytes,
- *                  256-byte aligned; its contents need no initialisation and
- *                  are overwritten.
+ *                  256-byte aligned, zero-filled before its first plan (see
+ *                  above); it holds the plan's intermediate state.
  *
  * Host checks (TOPOEP_EINVAL): null pointers; R <= 0; G <= 0 or G does not
  * divide R; R does not divide E; k < 1 or k > E; T < 0 or T * k > INT32_MAX;
@@ -147,12 +179,14 @@ int topoep_plan_ex(const topoep_topology *topo, const int32_t *global_load,
                    const topoep_launch *launch);
 
 /*
- * Enqueue a single kernel of the plan, for measurement: stage 0 = histogram
- * (Eq. 3 row), 1 = solver (Eqs. 4, 9, 10 and routing), 2 = reroute.  The
- * arguments are those of topoep_plan_ex.  A stage reads the workspace state
- * the earlier stages left for the same inputs, so a stage may be repeated
- * after one full plan and gives the same outputs.  TOPOEP_EINVAL for a stage
- * outside [0, 2].
+ * Enqueue one kernel of the plan, for measurement.  With three kernels:
+ * stage 0 = histogram (Eq. 3 row), 1 = solver (Eqs. 4, 9, 10 and routing),
+ * 2 = reroute; a stage reads the workspace state the earlier stages left for
+ * the same inputs, so it may be repeated after one full plan and gives the
+ * same outputs.  With one kernel (solver 3), stage 0 is the whole plan.
+ * TOPOEP_STAGE_FLOOR enqueues every kernel of the plan with an empty body
+ * and the same grid, threads and dynamic LDS (writes nothing).  The
+ * arguments are those of topoep_plan_ex.  TOPOEP_EINVAL for any other stage.
  */
 int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t *global_load,
                       const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,

@@ -88,8 +88,8 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
              debug: bool = False, move_cap: int = 0, raw_rc: bool = False):
     """Run the oracle.  Returns a dict of numpy arrays.
 
-    Keys: replica_slots [R, N], token_dest [T, k], send_counts [R], status,
-    and with ``debug``: hist, demand, x_stage1, q_routed, load_routed,
+    Keys: replica_slots [R, N], token_dest [T, k], send_counts [R], status
+    (the bits), move_count (refinement moves committed), and with ``debug``: hist, demand, x_stage1, q_routed, load_routed,
     x_final, q_final, load_final, iters, moves, move_dcost, move_m, n_moves.
     """
     lib = _load()
@@ -103,7 +103,7 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
     slots = np.full((R, max(N, 0)), -7, dtype=np.int32)
     dest = np.full((T, k), -7, dtype=np.int32)
     sc = np.full(R, -7, dtype=np.int32)
-    st = np.zeros(1, dtype=np.int32)
+    st = np.zeros(2, dtype=np.int32)
     out = {}
     dbgp = None
     if debug:
@@ -131,7 +131,7 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
         return rc
     if rc != 0:
         raise ValueError("topoep_plan_ref returned %d" % rc)
-    out.update(replica_slots=slots, token_dest=dest, send_counts=sc, status=int(st[0]))
+    out.update(replica_slots=slots, token_dest=dest, send_counts=sc, status=int(st[0]), move_count=int(st[1]))
     if debug:
         out["n_moves"] = dbg.n_moves
         nm = min(dbg.n_moves, move_cap)

@@ -181,7 +181,8 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
     for (int i = 0; i < R * N; ++i) replica_slots[i] = -1;
     for (int r = 0; r < R; ++r) send_counts[r] = 0;
     for (int64_t i = 0; i < n_assign; ++i) token_dest[i] = -1;
-    *status = (int32_t)st;
+    status[0] = (int32_t)st;
+    status[1] = 0;
     if (dbg) {
       dbg->n_moves = 0;
       if (dbg->hist) memcpy(dbg->hist, hist, (size_t)E * sizeof(int32_t));
@@ -373,7 +374,8 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
     }
     token_dest[i] = dest;
   }
-  *status = (int32_t)st;
+  status[0] = (int32_t)st;
+  status[1] = n_moves;
 #undef Q
 #undef X
 #undef UU

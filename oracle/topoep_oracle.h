@@ -69,9 +69,11 @@ typedef struct {
 /*
  * All pointers are host pointers, row-major.  Outputs: replica_slots[R*N]
  * (slot j of rank r = the j-th replica created on r, -1 if empty),
- * token_dest[T*k], send_counts[R], status[1].  When status has BAD_ID,
+ * token_dest[T*k], send_counts[R], status[2]: status[0] = REF_ST_* bits,
+ * status[1] = refinement moves committed, summed over domains (each
+ * iteration of the Eq. 10 loop commits one).  When status[0] has BAD_ID,
  * NEG_LOAD or RANGE set, no plan is made: replica_slots = -1,
- * send_counts = 0, token_dest = -1.
+ * send_counts = 0, token_dest = -1, status[1] = 0.
  */
 int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
                     const int32_t *local_topk, int32_t T, int32_t k,

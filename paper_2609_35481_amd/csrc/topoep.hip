@@ -50,12 +50,18 @@ constexpr int kCtrlTicket = 1;   // finish tickets of the solver workgroups
 constexpr int kCtrlStatus = 2;   // status bits accumulated during the plan
 constexpr int kCtrlFinal = 3;    // final status of the plan (read by reroute)
 constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
+constexpr int kCtrlMoves = 6;    // refinement moves of the per-domain solver
+constexpr int kCtrlArrive = 8;   // one-launch plan: chunks whose counts are written
 
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kMaxSolveGroups = 128;    // co-resident by a wide margin (256 CUs)
 constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
 constexpr int kOffsetExperts = 64;      // experts per offset workgroup
+constexpr int kFusedBlocks = 64;        // chunk workgroups the single-launch plan aims for
+constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs)
+constexpr int kPollMax = 16;            // published counts one solver thread polls
+constexpr int kFlagStride = 32;         // words between ready flags (one 128-byte line each)
 constexpr uint32_t kSpinLimit = 1u << 24;
 constexpr uint32_t kIterLimit = 1u << 22;
 
@@ -66,17 +72,23 @@ struct Plan {
   int cI, cX;
   int64_t S, W;
   int64_t n, chunk;
-  int nb, n_solvers, n_helpers;
+  int nb, n_solvers, n_helpers, pgroups;
+  int rchunks_all, rchunks_dom;   // routing: source-domain chunks (divisors of M)
   uint32_t spin_limit, iter_limit;
   FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
+  uint32_t *pub, *flags;   // one-launch plan: published counts, ready flags
 };
 
 __host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
 __host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
+
+// Scratch words of the histogram reduction (hist_from_partials, load_fast)
+// for up to 1024 threads: max(E, 4 * threads).
+__host__ __device__ inline int hist_scratch_words(const Plan &p) { return imax(p.E, 4 * 1024); }
 
 // LDS layout of the one-workgroup-per-domain solver, in int32 words.
 struct DomainLds {
@@ -99,26 +111,26 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
   o = (o + 3) & ~3;
   l.misc = o;  o += 64;
   l.qcol = o;                                // q[s][e][r] of the domain's instances
-  o += imax(p.I * p.QS, imax(2 * p.E + 2 + p.E * p.RW + 64, 1024));
+  o += imax(p.I * p.QS, imax(2 * p.E + 2 + p.E * p.RW + 64, hist_scratch_words(p)));
   l.words = o;
   return l;
 }
 
 // LDS layout of the single-workgroup solver: every domain's state at once.
 struct SingleLds {
-  int ck, fdt, hs, cnt, mask, repl, nsel, slots, used, L, e_of, U, misc, om, qcol, words;
+  int ck, em, fdt, hs, cnt, mask, repl, slots, used, L, e_of, U, misc, om, qcol, words;
 };
 
 __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   SingleLds l;
   int o = 0;
   l.ck = o;    o += 2 * p.M * p.E;            // uint64 stage-1 candidate keys per domain
+  l.em = o;    o += 2 * p.M * p.E;            // uint64 per domain and expert: local ranks hosting it
   l.fdt = o;   o += 2 * (p.M + 1);            // divisors 1..M
   l.hs = o;    o += p.E;                      // histogram of local_topk
   l.cnt = o;   o += p.M;                      // candidates per domain
   l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
   l.repl = o;  o += p.M * imax(p.cap1, 1);    // stage-1 replicas per domain
-  l.nsel = o;  o += p.M;
   l.slots = o; o += p.R * imax(p.Neff, 1);    // replica slots of every rank
   l.used = o;  o += p.R;
   l.L = o;     o += p.R;                      // rank loads
@@ -127,10 +139,28 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   o = (o + 3) & ~3;
   l.misc = o;  o += 64;
   l.om = o;                                   // Omega' [R][E], then list scratch
-  o += imax(p.R * p.E, p.E + 2 + p.E * p.RW + 2 * p.nent_cap + 64);
+  o += imax(p.R * p.E, p.E * p.RW);            // (instance-list rank bitmaps after routing)
   o = (o + 3) & ~3;
   l.qcol = o;                                 // partial-sum scratch, then q columns
-  o += imax(p.M * p.I * p.QS, 1024);
+  o += imax(p.M * p.I * p.QS, hist_scratch_words(p));
+  l.words = o;
+  return l;
+}
+
+// LDS layout of a chunk workgroup of the single-launch plan (nt threads).
+struct ChunkLds {
+  int wc, run, ptr, er, eend, flag, words;
+};
+
+__host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
+  ChunkLds l;
+  int o = 0;
+  l.wc = o;   o += (nt >> 6) * p.E;          // per-wave counts, then offsets in the block
+  l.run = o;  o += p.E;                      // offset of the block per expert
+  l.ptr = o;  o += p.E + 1;                  // instance list: first entry per expert
+  l.er = o;   o += p.nent_cap;               //   instance rank
+  l.eend = o; o += p.nent_cap;               //   cumulative share
+  l.flag = o; o += 4;
   l.words = o;
   return l;
 }
@@ -335,12 +365,14 @@ __device__ inline FastDiv make_fastdiv_dev(uint32_t d) {
 // x / d with one high multiply (x < 2^31): m < 2^32 and sh >= 32 except for
 // d = 1, where the quotient is x.
 __device__ inline uint32_t fdiv_hi(uint32_t x, FastDiv f) {
-  return f.sh >= 32 ? (__umulhi(x, f.m) >> (f.sh - 32)) : x;
+  const uint32_t hi = __umulhi(x, f.m) >> ((f.sh - 32u) & 31u);   // computed for every lane: a select, no branch
+  return f.sh >= 32 ? hi : x;
 }
 
 // Histogram of local_topk (row self of Omega) as the sum of the histogram
 // blocks' partials: thread (e, g) sums its share of the blocks with eight
-// loads in flight; scratch needs max(E, (blockDim / E) * E) words.
+// loads in flight; scratch needs hist_scratch_words(p) = max(E, 4 * blockDim)
+// words (the int4 path keeps blockDim int4 partial sums).
 __device__ void hist_from_partials(const Plan &p, int *hs, int *scratch) {
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb;
   if ((E & 3) == 0) {
@@ -533,13 +565,25 @@ __device__ inline bool out_of_range(const Plan &p, uint64_t total) {
   return tok + rep >= lim;
 }
 
+// Hand-overs between workgroups.  A workgroup barrier orders the waves but
+// does not wait for their global stores, and one wave's agent-scope release
+// (an L2 write-back) only covers stores that have reached the L2.  So before
+// the barrier that precedes a signal every wave waits for its own memory
+// operations to complete (s_waitcnt, no cache operation); then one wave
+// releases and signals.  On the waiting side one wave acquires (the L1 and
+// L2 invalidations cover the whole CU) before the barrier that releases the
+// other waves' loads.
+__device__ inline void drain_then_barrier() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
 // Grid barrier of the per-domain solver workgroups: all of them are
 // resident (at most kMaxSolveGroups), and the wait is bounded so the kernel
 // always exits.
 __device__ bool grid_barrier(uint32_t *count, uint32_t groups, uint32_t spin_limit, int *flag) {
-  __syncthreads();
+  drain_then_barrier();
   if (threadIdx.x == 0) {
-    __threadfence();
     __hip_atomic_fetch_add(count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     uint32_t it = 0;
     int ok = 1;
@@ -550,7 +594,7 @@ __device__ bool grid_barrier(uint32_t *count, uint32_t groups, uint32_t spin_lim
       }
       __builtin_amdgcn_s_sleep(1);
     }
-    __threadfence();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     *flag = ok;
   }
   __syncthreads();
@@ -571,6 +615,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
     p.ctrl[kCtrlTicket] = 0;
     p.ctrl[kCtrlStatus] = 0;
     p.ctrl[kCtrlFinal] = 0;
+    p.ctrl[kCtrlMoves] = 0;
     *reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal) = 0ull;
   }
   for (int e = tid; e < p.E; e += nt) h[e] = 0;
@@ -611,19 +656,43 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
 // hosting domain, so an instance's position in ascending rank order is the
 // number of hosting domains below its own), the lowest positions taking the
 // remainder; sources of another domain that hosts e send it nothing.  The
-// case is decided once per source domain.  Thread t handles the run of
-// source domains t / NI of instance t % NI; qcol[i * QS + s] = q[s][e][r_i];
-// U[i] += sum_s q (U must be zero on entry).
-template <class WOf, class DomOf>
-__device__ void route_instances(const Plan &p, int NI, FastDiv fNI, const int *e_of, const uint32_t *mask,
-                                const FastDiv *fdt, int *qcol, int *U, WOf w_of, DomOf dom_of) {
-  const int tid = threadIdx.x, nt = blockDim.x, G = p.G, M = p.M;
-  const int chunks = imax(1, imin(M, nt / imax(NI, 1)));
-  const int dpc = (M + chunks - 1) / chunks;
+// case is decided once per source domain.  Thread t handles source domains
+// [c * M / chunks, (c + 1) * M / chunks) of instance t % NI, c = t / NI
+// (chunks divides M); omega[s][e] of instance i is src_of(i, e)[s * stride];
+// qcol[i * QS + s] = q[s][e][r_i] (may be the source itself: every value is
+// read before it is written); U[i] += sum_s q (U must be zero on entry).
+struct RouteCase {
+  FastDiv fn;
+  int n, below, keep, take;
+};
+
+template <int B>
+__device__ inline int route_batch(const int *src, int stride, int *dst, const RouteCase &rc) {
+  int w[B];
+#pragma unroll
+  for (int u = 0; u < B; ++u) w[u] = src[u * stride];
+  int sum = 0;
+#pragma unroll
+  for (int u = 0; u < B; ++u) {
+    const int qq = (int)fdiv_hi((uint32_t)w[u], rc.fn);
+    const int split = qq + (rc.below < w[u] - qq * rc.n ? 1 : 0);
+    const int q = (w[u] & rc.keep) + (split & rc.take);   // local: w; hosting domain: 0; else the split
+    dst[u] = q;
+    sum += q;
+  }
+  return sum;
+}
+
+template <class SrcOf, class DomOf>
+__device__ void route_instances(const Plan &p, int NI, FastDiv fNI, int chunks, const int *e_of,
+                                const uint32_t *mask, const FastDiv *fdt, int *qcol, int *U, SrcOf src_of,
+                                int stride, DomOf dom_of) {
+  const int tid = threadIdx.x, nt = blockDim.x, G = p.G;
+  const int dpc = p.M / chunks;
   for (int t = tid; t < NI * chunks; t += nt) {
     const int c = (int)fdiv((uint32_t)t, fNI), i = t - c * NI;
     const int e = e_of[i];
-    const int ds0 = c * dpc, ds1 = imin(M, ds0 + dpc);
+    const int ds0 = c * dpc, ds1 = ds0 + dpc;
     int *row = qcol + i * p.QS;
     if (e < 0) {
       for (int s = ds0 * G; s < ds1 * G; ++s) row[s] = 0;
@@ -631,31 +700,30 @@ __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, const int *e
     }
     const int d = dom_of(i);
     const uint32_t *me = mask + e * p.MW;
-    int n = 0, below = 0;
+    RouteCase rc;
+    rc.n = 0;
+    rc.below = 0;
     for (int wd = 0; wd < p.MW; ++wd) {
       const uint32_t bits = me[wd];
-      n += __popc(bits);
+      rc.n += __popc(bits);
       const int lo = wd * 32;
-      if (d >= lo + 32) below += __popc(bits);
-      else if (d > lo) below += __popc(bits & ((1u << (d - lo)) - 1u));
+      if (d >= lo + 32) rc.below += __popc(bits);
+      else if (d > lo) rc.below += __popc(bits & ((1u << (d - lo)) - 1u));
     }
-    const FastDiv fn = fdt[n];
+    rc.fn = fdt[rc.n];
+    const int *col = src_of(i, e);
     int usum = 0;
     for (int ds = ds0; ds < ds1; ++ds) {
-      const int s0 = ds * G;
-      // local: the unique instance in the source's domain takes w; another
-      // hosting domain: nothing; otherwise the even split
       const bool local = ds == d;
       const bool zero = !local && ((me[ds >> 5] >> (ds & 31)) & 1u);
-#pragma unroll 8
-      for (int j = 0; j < G; ++j) {
-        const int w = w_of(i, s0 + j, e);
-        const int qq = (int)fdiv_hi((uint32_t)w, fn);
-        const int split = qq + (below < w - qq * n ? 1 : 0);
-        const int q = local ? w : (zero ? 0 : split);
-        row[s0 + j] = q;
-        usum += q;
-      }
+      rc.keep = local ? -1 : 0;
+      rc.take = (local || zero) ? 0 : -1;
+      const int *src = col + ds * G * stride;
+      int *dst = row + ds * G;
+      int j = 0;
+      for (; j + 8 <= G; j += 8) usum += route_batch<8>(src + j * stride, stride, dst + j, rc);
+      for (; j + 4 <= G; j += 4) usum += route_batch<4>(src + j * stride, stride, dst + j, rc);
+      for (; j < G; ++j) usum += route_batch<1>(src + j * stride, stride, dst + j, rc);
     }
     if (usum) atomicAdd(&U[i], usum);
   }
@@ -688,19 +756,30 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // ascending (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt
 // itself, then the other sources ascending, then rb (or plain ascending when
 // the intra-domain cost is zero).  The loop ends when no candidate has
-// delta >= 1.
-__device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
-                              int *Lr, uint64_t *em, uint32_t *flags) {
+// delta >= 1.  Returns the number of moves committed.  With prepared, em
+// already holds the masks and the wave sums the rank loads Lr itself;
+// otherwise Lr is given and em is scratch filled here.
+__device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
+                                  int *Lr, uint64_t *em, uint32_t *flags, bool prepared) {
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
-  if (G < 2) return;
+  if (G < 2) return 0;
   const int r0 = d * G;
-  // hosting masks per expert
-  for (int e = lane; e < E; e += 64) em[e] = 0;
-  wave_sync();
-  for (int a = lane; a < I; a += 64) {
-    const int e = e_of[a];
-    if (e >= 0) atomicOr(reinterpret_cast<unsigned long long *>(&em[e]), 1ull << (uint32_t)fdiv((uint32_t)a, p.fPN));
+  if (prepared) {
+    // em already holds the hosting masks; the rank loads are summed here
+    if (lane < G) {
+      int l = 0;
+      for (int pos = 0; pos < PN; ++pos) l += U[lane * PN + pos];
+      Lr[lane] = l;
+    }
+  } else {
+    // hosting masks per expert
+    for (int e = lane; e < E; e += 64) em[e] = 0;
+    wave_sync();
+    for (int a = lane; a < I; a += 64) {
+      const int e = e_of[a];
+      if (e >= 0) atomicOr(reinterpret_cast<unsigned long long *>(&em[e]), 1ull << (uint32_t)fdiv((uint32_t)a, p.fPN));
+    }
   }
   wave_sync();
   const int ncand = PN * (G - 1);
@@ -716,7 +795,8 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
   }
   const int64_t tokc = 2 * p.S * (int64_t)p.cI;   // cost change per moved assignment and unit of (m_rb - m_rt)
   const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
-  for (uint32_t it = 0;; ++it) {
+  uint32_t it = 0;
+  for (;; ++it) {
     if (it >= p.iter_limit) {
       if (lane == 0) *flags |= TOPOEP_ST_ITER;
       break;
@@ -847,6 +927,7 @@ __device__ void refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol
     }
     wave_sync();
   }
+  return it;   // one move per completed iteration
 }
 
 // Stage-1 candidate key: (D descending, e ascending) as one unsigned
@@ -873,58 +954,42 @@ __device__ inline void rank_candidates(int c, int nc, int cap, const uint64_t *k
   if (rank < cap) out[rank] = (int)(uint32_t)kc;
 }
 
-// Builds this rank's per-expert instance list (instances with a nonzero
-// share of its assignments, ascending rank, cumulative shares) from the
-// q columns of every domain, and writes it to the workspace.  All LDS.
-// e_of/qcol address instance (d, a) as d * I + a; scratch holds
-// E + 2 + E * RW + 2 * nent_cap + 64 words.
-__device__ void build_instance_list(const Plan &p, const int *e_of, const int *qcol, int *scratch) {
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const int E = p.E, I = p.I, G = p.G;
-  int *cnt = scratch;                                              // E + 1
-  uint32_t *bm = reinterpret_cast<uint32_t *>(scratch + E + 2);   // E * RW
-  int *ent_r = scratch + E + 2 + E * p.RW;                         // nent_cap
-  int *ent_q = ent_r + p.nent_cap;                                 // nent_cap
-  int *tmp = ent_q + p.nent_cap;                                   // scan scratch
-  for (int e = tid; e <= E; e += nt) cnt[e] = 0;
-  for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
-  lds_barrier();
-  const int n_inst = p.M * I;
-  for (int idx = tid; idx < n_inst; idx += nt) {
-    const int e = e_of[idx];
-    if (e < 0) continue;
-    const int q = qcol[idx * p.QS + p.self];
-    if (q <= 0) continue;
-    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
-    const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
-    atomicAdd(&cnt[e], 1);
-    atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
-  }
-  lds_barrier();
-  block_excl_scan(cnt, E + 1, tmp);
-  for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
-  for (int idx = tid; idx < n_inst; idx += nt) {
-    const int e = e_of[idx];
-    if (e < 0) continue;
-    const int q = qcol[idx * p.QS + p.self];
-    if (q <= 0) continue;
-    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
-    const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
-    const uint32_t *row = bm + e * p.RW;
-    int pos = 0;
-    for (int w = 0; w < (r >> 5); ++w) pos += __popc(row[w]);
-    pos += __popc(row[r >> 5] & ((1u << (r & 31)) - 1u));
-    const int j = cnt[e] + pos;
-    ent_r[j] = r;
-    ent_q[j] = q;
-  }
-  lds_barrier();
-  for (int e = tid; e < E; e += nt) {
+// This rank's per-expert instance list: bm[e * RW ...] marks the ranks
+// whose instance of e has a nonzero share q[self][e][r].  Thread t takes
+// experts [t * K, (t + 1) * K), K = ceil(E / blockDim): it counts their
+// ranks; a wave scan plus the totals of the waves before (one barrier) give
+// each expert's first entry; then it walks the ranks in ascending order
+// writing (rank, cumulative share).  qcol and e_of address instance (d, a)
+// as d * I + a; slots/used are every rank's; tmp holds blockDim / 64 words.
+__device__ void emit_instance_list(const Plan &p, const int *qcol, const int *slots, const int *used,
+                                   const uint32_t *bm, int *tmp) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
+  const int E = p.E, RW = p.RW, K = (E + nt - 1) / nt;
+  const int e0 = imin(E, tid * K), e1 = imin(E, e0 + K);
+  int cnt = 0;
+  for (int e = e0; e < e1; ++e)
+    for (int w = 0; w < RW; ++w) cnt += __popc(bm[e * RW + w]);
+  const int incl = wave_incl_scan(cnt);
+  if (lane == 63) tmp[wave] = incl;
+  __syncthreads();
+  int pos = incl - cnt;
+  for (int w = 0; w < wave; ++w) pos += tmp[w];
+  if (tid == nt - 1) p.csr_ptr[E] = pos + cnt;
+  for (int e = e0; e < e1; ++e) {
+    p.csr_ptr[e] = pos;
     int run = 0;
-    for (int j = cnt[e]; j < cnt[e + 1]; ++j) {
-      run += ent_q[j];
-      p.csr_r[j] = ent_r[j];
-      p.csr_end[j] = run;
+    for (int w = 0; w < RW; ++w) {
+      uint32_t bits = bm[e * RW + w];
+      while (bits) {
+        const int r = w * 32 + __ffs(bits) - 1;
+        bits &= bits - 1u;
+        const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * p.G;
+        const int a = instance_of(p, d, j, e, slots + d * p.G * p.Neff, used + d * p.G);
+        if (a >= 0) run += qcol[(d * p.I + a) * p.QS + p.self];   // a >= 0: bm marks hosts only
+        p.csr_r[pos] = r;
+        p.csr_end[pos] = run;
+        ++pos;
+      }
     }
   }
 }
@@ -1098,7 +1163,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     }
     lds_barrier();
     route_instances(
-        p, I, p.fI, e_of, mask, fdt, qcol, U, [&](int i, int s, int) { return qcol[i * p.QS + s]; },
+        p, I, p.fI, p.rchunks_dom, e_of, mask, fdt, qcol, U, [&](int i, int) { return qcol + i * p.QS; }, 1,
         [&](int) { return d; });
     lds_barrier();
     for (int j = tid; j < G; j += nt) {
@@ -1107,7 +1172,10 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       Lr[j] = l;
     }
     lds_barrier();
-    if (tid < 64) refine_domain(p, d, e_of, U, qcol, slots, used, Lr, ck, &flags);
+    if (tid < 64) {
+      const uint32_t mv = refine_domain(p, d, e_of, U, qcol, slots, used, Lr, ck, &flags, false);
+      if (tid == 0 && mv) atomicAdd(&p.ctrl[kCtrlMoves], mv);
+    }
     lds_barrier();
     // outputs of the domain's ranks
     for (int i = tid; i < G * p.N; i += nt) {
@@ -1128,15 +1196,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   if (tid == 0 && (flags || !synced)) atomicOr(&p.ctrl[kCtrlStatus], flags | (synced ? 0u : TOPOEP_ST_SYNC));
 
   // ---- the last workgroup to finish lists this rank's instances per expert
-  __syncthreads();
+  drain_then_barrier();
   if (tid == 0) {
-    __threadfence();
     const uint32_t t = __hip_atomic_fetch_add(&p.ctrl[kCtrlTicket], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     misc[4] = t == (uint32_t)nwg - 1;
   }
   __syncthreads();
   if (!misc[4]) return;
-  __threadfence();
   int *cnt = qcol;                                            // E + 1
   uint32_t *bm = reinterpret_cast<uint32_t *>(qcol + E + 2);  // E * RW
   int *tmp = qcol + E + 2 + E * p.RW;                         // scan scratch
@@ -1183,6 +1249,10 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     fin |= gst & TOPOEP_ST_RANGE;
     p.ctrl[kCtrlFinal] = fin;
     p.status_out[0] = (int32_t)fin;
+    p.status_out[1] = (fin & (kNoPlan | TOPOEP_ST_SYNC))
+                          ? 0
+                          : (int32_t)__hip_atomic_load(&p.ctrl[kCtrlMoves], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
     p.ctrl[kCtrlBar] = 0;
     p.ctrl[kCtrlTicket] = 0;
   }
@@ -1190,60 +1260,71 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
 
 // ---------------------------------------------------------------- solver: one workgroup for every domain
 
-// The same steps with every domain's state in the LDS of one CU; each
-// domain's refinement runs on its own wave.  Used when Omega and all q
-// columns fit in LDS.
-__global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
-  extern __shared__ int64_t smem_1[];
-  int *sm = reinterpret_cast<int *>(smem_1);
-  if (blockIdx.x > 0) {
-    block_offsets(p, blockIdx.x - 1, sm);
-    return;
-  }
+// LDS state of the single-workgroup solver.
+struct SingleState {
+  uint64_t *ck, *em;
+  FastDiv *fdt;
+  int *hs, *ccnt, *repl, *slots, *used, *Lr, *e_of, *U, *misc, *om, *qcol;
+  uint32_t *mask;
+};
+
+__device__ inline SingleState single_state(const Plan &p, int *sm) {
   const SingleLds lay = single_lds(p);
-  uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
-  FastDiv *fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
-  int *hs = sm + lay.hs;
-  int *ccnt = sm + lay.cnt;
-  uint32_t *mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
-  int *repl = sm + lay.repl;
-  int *nsel = sm + lay.nsel;
-  int *slots = sm + lay.slots;
-  int *used = sm + lay.used;
-  int *Lr = sm + lay.L;
-  int *e_of = sm + lay.e_of;
-  int *U = sm + lay.U;
-  int *misc = sm + lay.misc;
-  int *om = sm + lay.om;
-  int *qcol = sm + lay.qcol;
+  SingleState t;
+  t.ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
+  t.em = reinterpret_cast<uint64_t *>(sm + lay.em);
+  t.fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
+  t.hs = sm + lay.hs;
+  t.ccnt = sm + lay.cnt;
+  t.mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
+  t.repl = sm + lay.repl;
+  t.slots = sm + lay.slots;
+  t.used = sm + lay.used;
+  t.Lr = sm + lay.L;
+  t.e_of = sm + lay.e_of;
+  t.U = sm + lay.U;
+  t.misc = sm + lay.misc;
+  t.om = sm + lay.om;
+  t.qcol = sm + lay.qcol;
+  return t;
+}
+
+// misc[0] status bits, misc[2] wait flag, misc[8..9] total load, misc[12]
+// refinement moves; candidate counts, hosting-domain masks and local
+// hosting masks zero; stage-1 replica lists empty; the divisor table.
+__device__ inline void single_init(const Plan &p, const SingleState &t) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (tid < 16) t.misc[tid] = 0;
+  for (int d = tid; d < p.M; d += nt) t.ccnt[d] = 0;
+  for (int i = tid; i < p.E * p.MW; i += nt) t.mask[i] = 0;
+  for (int i = tid; i < p.M * p.cap1; i += nt) t.repl[i] = -1;
+  for (int i = tid; i < p.M * p.E; i += nt) t.em[i] = 0;
+  build_divisors(p.M, t.fdt);
+}
+
+// Every step after the load: with Omega' in om (row self = the histogram hs)
+// and the status bits gst, plans all domains (Eq. 9 placement, routing,
+// Eq. 10 refinement) and writes replica_slots, send_counts, this rank's
+// instance list and the final status (ctrl word and status_out).  With
+// BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
+__device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
+  uint64_t *ck = t.ck, *em = t.em;
+  FastDiv *fdt = t.fdt;
+  int *hs = t.hs, *ccnt = t.ccnt, *repl = t.repl, *slots = t.slots, *used = t.used;
+  int *Lr = t.Lr, *e_of = t.e_of, *U = t.U, *misc = t.misc, *om = t.om, *qcol = t.qcol;
+  uint32_t *mask = t.mask;
+  (void)hs;
   const int tid = threadIdx.x, nt = blockDim.x, wave = tid >> 6, nw = nt >> 6;
   const int E = p.E, G = p.G, R = p.R, M = p.M, I = p.I, P = p.P, PN = p.PN, Neff = p.Neff;
   const int cap = p.cap1;
-
-  if (tid < 16) misc[tid] = 0;
-  for (int d = tid; d < M; d += nt) ccnt[d] = 0;
-  build_divisors(M, fdt);
-  // ---- Omega to LDS; histogram of local_topk from the blocks' partials
-  lds_barrier();
-  if (load_fast_ok(p)) {
-    load_fast(p, om, hs, qcol, misc);
-  } else {
-    copy_to_lds(om, p.gl, R * E);
-    hist_from_partials(p, hs, qcol);
-    for (int b = tid; b < p.nb; b += nt)
-      if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
-    scan_rows(p, 0, R, om, hs, misc);
-    lds_barrier();
-    for (int e = tid; e < E; e += nt) om[p.self * E + e] = hs[e];
-  }
-  uint32_t gst = (uint32_t)misc[0];
-  if (out_of_range(p, *reinterpret_cast<unsigned long long *>(misc + 8))) gst |= TOPOEP_ST_RANGE;
-  if (gst & kNoPlan) {
+  if (gst & (kNoPlan | TOPOEP_ST_SYNC)) {
     for (int i = tid; i < R * p.N; i += nt) p.slots_out[i] = -1;
     for (int r = tid; r < R; r += nt) p.send_out[r] = 0;
     if (tid == 0) {
       p.ctrl[kCtrlFinal] = gst;
-      p.status_out[0] = (int32_t)gst;
+      if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), gst);
+      else p.status_out[0] = (int32_t)gst;
+      p.status_out[1] = 0;
     }
     return;
   }
@@ -1267,86 +1348,143 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
     const int nc = ccnt[d];
     if (c < nc) rank_candidates(c, nc, cap, ck + d * E, repl + d * cap);
   }
-  for (int i = tid; i < M * cap; i += nt) {
-    const int d = (int)fdiv((uint32_t)i, p.fCap), c = i - d * cap;
-    if (c >= ccnt[d]) repl[i] = -1;
-  }
-  for (int i = tid; i < E * p.MW; i += nt) mask[i] = 0;
   lds_barrier();
 
-  // ---- hosting domains per expert; every rank's slots and instances
-  for (int e = tid; e < E; e += nt) {
-    const int dm = (int)fdiv((uint32_t)e, p.fGP);
-    atomicOr(&mask[e * p.MW + (dm >> 5)], 1u << (dm & 31));
-  }
-  for (int i = tid; i < M * cap; i += nt) {
-    const int e = repl[i];
-    if (e >= 0) {
-      const int dd = (int)fdiv((uint32_t)i, p.fCap);
-      atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
+  // ---- hosting domains per expert; every rank's slots and instances, and
+  // the local ranks hosting each expert in its domain (one pass: stage-1
+  // replica i of domain d sits on local rank i mod G, slot i / G, so rank j
+  // uses ceil((n_sel - j) / G) slots)
+  // (four independent loops over one index space, so each thread runs one
+  // loop body instead of one of each)
+  {
+    const int n1 = M * I, n2 = n1 + E, n3 = n2 + M * cap, n4 = n3 + R;
+    for (int v = tid; v < n4; v += nt) {
+      if (v < n1) {
+        const int idx = v;
+        const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+        const int j = (int)fdiv((uint32_t)a, p.fPN), pos = a - j * PN;
+        int e;
+        if (pos < P) {
+          e = (d * G + j) * P + pos;
+        } else {
+          const int ns = imin(ccnt[d], cap);
+          const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
+          e = (pos - P) < u ? repl[d * cap + (pos - P) * G + j] : -1;
+        }
+        e_of[idx] = e;
+        U[idx] = 0;
+        if (e >= 0) atomicOr(reinterpret_cast<unsigned long long *>(&em[d * E + e]), 1ull << (uint32_t)j);
+      } else if (v < n2) {
+        const int e = v - n1;
+        const int dm = (int)fdiv((uint32_t)e, p.fGP);
+        atomicOr(&mask[e * p.MW + (dm >> 5)], 1u << (dm & 31));
+      } else if (v < n3) {
+        const int i = v - n2;
+        const int e = repl[i];
+        if (e >= 0) {
+          const int dd = (int)fdiv((uint32_t)i, p.fCap);
+          atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
+        }
+      } else {
+        const int r = v - n3;
+        const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+        const int ns = imin(ccnt[d], cap);
+        const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
+        used[r] = u;
+        for (int t = 0; t < Neff; ++t) slots[r * Neff + t] = t < u ? repl[d * cap + t * G + j] : -1;
+      }
     }
-  }
-  for (int d = tid; d < M; d += nt) nsel[d] = imin(ccnt[d], cap);
-  lds_barrier();
-  for (int r = tid; r < R; r += nt) {
-    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
-    const int ns = nsel[d];
-    const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
-    used[r] = u;
-    for (int t = 0; t < Neff; ++t) slots[r * Neff + t] = t < u ? repl[d * cap + t * G + j] : -1;
-  }
-  lds_barrier();
-  for (int idx = tid; idx < M * I; idx += nt) {
-    const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
-    const int j = (int)fdiv((uint32_t)a, p.fPN), pos = a - j * PN;
-    const int r = d * G + j;
-    int e;
-    if (pos < P) e = r * P + pos;
-    else e = (pos - P) < used[r] ? slots[r * Neff + pos - P] : -1;
-    e_of[idx] = e;
-    U[idx] = 0;
   }
   lds_barrier();
 
   // ---- routing construction (Section 4.3) for every domain's instances
   route_instances(
-      p, M * I, p.fMI, e_of, mask, fdt, qcol, U, [&](int, int s, int e) { return om[s * E + e]; },
+      p, M * I, p.fMI, p.rchunks_all, e_of, mask, fdt, qcol, U, [&](int, int e) { return om + e; }, E,
       [&](int i) { return (int)fdiv((uint32_t)i, p.fI); });
   lds_barrier();
-  for (int r = tid; r < R; r += nt) {
-    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
-    int l = 0;
-    for (int pos = 0; pos < PN; ++pos) l += U[d * I + j * PN + pos];
-    Lr[r] = l;
-  }
-  lds_barrier();
 
-  // ---- intra-node refinement (Eq. 10): one wave per domain
-  uint32_t flags = 0;
+  // ---- intra-node refinement (Eq. 10): one wave per domain (it sums its
+  // ranks' loads first); Omega is dead, so its LDS takes the rank bitmaps
+  // of the instance list, cleared meanwhile by the other waves
+  uint32_t *bm = reinterpret_cast<uint32_t *>(om);
+  uint32_t flags = 0, moves = 0;
   for (int d = wave; d < M; d += nw)
-    refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff, used + d * G,
-                  Lr + d * G, ck + (int64_t)d * E, &flags);
-  if (flags && lane_id() == 0) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
+    moves += refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
+                           used + d * G, Lr + d * G, em + (int64_t)d * E, &flags, true);
+  if (lane_id() == 0) {
+    if (flags) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
+    if (moves) atomicAdd(reinterpret_cast<unsigned *>(&misc[12]), moves);
+  }
+  for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
   lds_barrier();
 
-  // ---- outputs
-  for (int i = tid; i < R * p.N; i += nt) {
-    const int r = (int)fdiv((uint32_t)i, p.fN), t = i - r * p.N;
-    p.slots_out[i] = t < used[r] ? slots[r * Neff + t] : -1;
+  // ---- outputs; ranks holding an instance of e with a share of this
+  // rank's assignments, as one bitmap per expert
+  {
+    const int n1 = M * I, n2 = n1 + R, n3 = n2 + R * p.N;
+    for (int v = tid; v < n3; v += nt) {
+      if (v < n1) {
+        const int idx = v;
+        const int e = e_of[idx];
+        if (e >= 0 && qcol[idx * p.QS + p.self] > 0) {
+          const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
+          const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
+          atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
+        }
+      } else if (v < n2) {
+        const int r = v - n1;
+        const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+        int sc = 0;
+        for (int pos = 0; pos < PN; ++pos) sc += qcol[(d * I + j * PN + pos) * p.QS + p.self];
+        p.send_out[r] = sc;
+      } else {
+        const int i = v - n2;
+        const int r = (int)fdiv((uint32_t)i, p.fN), t = i - r * p.N;
+        p.slots_out[i] = t < used[r] ? slots[r * Neff + t] : -1;
+      }
+    }
   }
-  for (int r = tid; r < R; r += nt) {
-    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
-    int sc = 0;
-    for (int pos = 0; pos < PN; ++pos) sc += qcol[(d * I + j * PN + pos) * p.QS + p.self];
-    p.send_out[r] = sc;
-  }
-  build_instance_list(p, e_of, qcol, om);
   lds_barrier();
+  emit_instance_list(p, qcol, slots, used, bm, reinterpret_cast<int *>(ck));
   if (tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;
-    p.status_out[0] = (int32_t)fin;
+    if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
+    else p.status_out[0] = (int32_t)fin;
+    p.status_out[1] = misc[12];
   }
+}
+
+// The same steps with every domain's state in the LDS of one CU; each
+// domain's refinement runs on its own wave.  Used when Omega and all q
+// columns fit in LDS.  Workgroups beyond the first compute the histogram
+// blocks' offsets for the reroute.
+__global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
+  extern __shared__ int64_t smem_1[];
+  int *sm = reinterpret_cast<int *>(smem_1);
+  if (blockIdx.x > 0) {
+    block_offsets(p, blockIdx.x - 1, sm);
+    return;
+  }
+  const SingleState t = single_state(p, sm);
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, R = p.R;
+  single_init(p, t);
+  // ---- Omega to LDS; histogram of local_topk from the blocks' partials
+  lds_barrier();
+  if (load_fast_ok(p)) {
+    load_fast(p, t.om, t.hs, t.qcol, t.misc);
+  } else {
+    copy_to_lds(t.om, p.gl, R * E);
+    hist_from_partials(p, t.hs, t.qcol);
+    for (int b = tid; b < p.nb; b += nt)
+      if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&t.misc[0]), TOPOEP_ST_BAD_ID);
+    scan_rows(p, 0, R, t.om, t.hs, t.misc);
+    lds_barrier();
+    for (int e = tid; e < E; e += nt) t.om[p.self * E + e] = t.hs[e];
+  }
+  uint32_t gst = (uint32_t)t.misc[0];
+  if (out_of_range(p, *reinterpret_cast<unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
+  single_plan(p, t, gst, false);
 }
 
 // ---------------------------------------------------------------- reroute
@@ -1438,12 +1576,333 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   }
 }
 
+// ---------------------------------------------------------------- single-launch plan
+//
+// Workgroup 0 solves; workgroups 1..nb each hold one chunk of ids.
+//   chunk -> solver: chunk b writes its count of every expert to
+//     pub[b * E + e] (bit 31 of expert 0's word: a bad id in the chunk),
+//     then increments the arrival counter with release semantics.  Only the
+//     solver polls the counter (many pollers of one word serialise at the
+//     memory side); it then clears it for the next plan.
+//   solver -> chunk b: after the outputs, this rank's instance list and
+//     every chunk's offset per expert are written, flags[b * kFlagStride]
+//     becomes 1 (release); chunk b polls only its own flag (one 128-byte
+//     line each), then clears it.
+// Between plans the counter and every flag are zero again; a workspace is
+// zero-filled before its first plan.  A bounded wait that gives up sets SYNC
+// and leaves that state undefined (the workspace is zero-filled again).
+
+// Omega to LDS with its status bits and total load (row self included as
+// gathered; the caller swaps in the histogram later).
+__device__ void load_omega(const Plan &p, int *om, int *misc) {
+  const int tid = threadIdx.x, nt = blockDim.x, n = p.R * p.E;
+  bool neg = false;
+  uint64_t tot = 0;
+  if ((p.E & 3) == 0 && (reinterpret_cast<uintptr_t>(p.gl) & 15) == 0) {
+    const int n4 = n >> 2;
+    const int4 *g4 = reinterpret_cast<const int4 *>(p.gl);
+    int4 *o4 = reinterpret_cast<int4 *>(om);
+    for (int i = tid; i < n4; i += 4 * nt) {
+      int4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = g4[imin(i + u * nt, n4 - 1)];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (i + u * nt < n4) {
+          o4[i + u * nt] = v[u];
+          neg |= (v[u].x | v[u].y | v[u].z | v[u].w) < 0;
+          tot += (uint64_t)(v[u].x > 0 ? v[u].x : 0) + (uint64_t)(v[u].y > 0 ? v[u].y : 0) +
+                 (uint64_t)(v[u].z > 0 ? v[u].z : 0) + (uint64_t)(v[u].w > 0 ? v[u].w : 0);
+        }
+      }
+    }
+  } else {
+    for (int i = tid; i < n; i += nt) {
+      const int g = p.gl[i];
+      om[i] = g;
+      neg |= g < 0;
+      if (g > 0) tot += (uint64_t)g;
+    }
+  }
+  tot = wave_sum_u64(tot);
+  const uint64_t any_neg = __ballot(neg);
+  if (lane_id() == 0) {
+    if (any_neg) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_NEG_LOAD);
+    if (tot) atomicAdd(reinterpret_cast<unsigned long long *>(misc + 8), (unsigned long long)tot);
+  }
+}
+
+// Solver side of the first hand-over, once every chunk has arrived: the
+// chunks' counts give hs[e] (the histogram of local_topk), offsets[b * E +
+// e] (the count of e in the chunks before b: chunk b's first occurrence
+// index of e) and BAD_ID into misc[0].  With pgroups == 1 a thread takes
+// whole experts (nb <= kPollMax); otherwise thread (g, e) takes chunks
+// [g * per, ...), per <= kPollMax, and pgroups * E <= blockDim.x; scratch
+// holds pgroups * E words.  All of a thread's loads are in flight at once.
+__device__ void collect_counts(const Plan &p, int *hs, int *scratch, int *misc) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb, groups = p.pgroups;
+  uint32_t v[kPollMax];
+  bool bad = false;
+  if (groups == 1) {
+    for (int e = tid; e < E; e += nt) {
+      // branch-free: every load issued before any is used (clamped rows)
+#pragma unroll
+      for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(j, nb - 1) * E + e];
+      int base = 0;
+#pragma unroll
+      for (int j = 0; j < kPollMax; ++j) {
+        if (j < nb) {
+          p.offsets[j * E + e] = base;
+          base += (int)(v[j] & 0x7FFFFFFFu);
+          bad |= (v[j] >> 31) != 0;
+        }
+      }
+      hs[e] = base;
+    }
+    const uint64_t any_bad = __ballot(bad);
+    if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
+    __syncthreads();
+    return;
+  }
+  const int per = (nb + groups - 1) / groups;
+  const bool active = tid < groups * E;
+  const int g = active ? (int)fdiv((uint32_t)tid, p.fE) : 0;
+  const int e = tid - g * E;
+  const int b0 = g * per;
+  const int cnt = active ? imax(0, imin(nb, b0 + per) - b0) : 0;
+  // branch-free: every load issued before any is used (clamped rows)
+  const int last = imax(0, imin(nb - 1, b0 + cnt - 1));
+#pragma unroll
+  for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(b0 + j, last) * E + e];
+#pragma unroll
+  for (int j = 0; j < kPollMax; ++j) v[j] = j < cnt ? v[j] : 0u;
+  int sum = 0;
+#pragma unroll
+  for (int j = 0; j < kPollMax; ++j) {
+    sum += (int)(v[j] & 0x7FFFFFFFu);
+    bad |= (v[j] >> 31) != 0;
+  }
+  if (active) scratch[tid] = sum;
+  const uint64_t any_bad = __ballot(bad);
+  if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
+  __syncthreads();
+  if (active) {
+    int base = 0, total = 0;
+    for (int g2 = 0; g2 < groups; ++g2) {
+      const int c = scratch[g2 * E + e];
+      if (g2 < g) base += c;
+      total += c;
+    }
+    if (g == 0) hs[e] = total;
+#pragma unroll
+    for (int j = 0; j < kPollMax; ++j) {
+      if (j < cnt) {
+        p.offsets[(b0 + j) * E + e] = base;
+        base += (int)(v[j] & 0x7FFFFFFFu);
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Solver role (workgroup 0): Omega goes to LDS while the chunks count; the
+// histogram and chunk offsets come from the published counts; the plan
+// proceeds as in the single-workgroup solver; then every chunk's flag.
+__device__ void fused_solver(const Plan &p, int *sm) {
+  const SingleState t = single_state(p, sm);
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
+  if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
+  single_init(p, t);
+  lds_barrier();
+  load_omega(p, t.om, t.misc);
+  // wait until every chunk has written its counts
+  if (tid == 0) {
+    uint32_t it = 0;
+    int ok = 1;
+    while (__hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+           (uint32_t)p.nb) {
+      if (++it > p.spin_limit) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (ok) __hip_atomic_store(&p.ctrl[kCtrlArrive], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    t.misc[2] = ok;
+  }
+  __syncthreads();
+  const bool synced = t.misc[2] != 0;
+  if (synced) collect_counts(p, t.hs, t.qcol, t.misc);
+  uint32_t gst = 0;
+  if (synced) {
+    bool diff = false;
+    int64_t adj = 0;
+    for (int e = tid; e < E; e += nt) {
+      const int h = t.hs[e], g = t.om[p.self * E + e];
+      diff |= g != h;
+      adj += (int64_t)(h > 0 ? h : 0) - (int64_t)(g > 0 ? g : 0);
+      t.om[p.self * E + e] = h;
+    }
+    adj = (int64_t)wave_sum_u64((uint64_t)adj);
+    const uint64_t any_diff = __ballot(diff);
+    if (lane_id() == 0) {
+      if (any_diff) atomicOr(reinterpret_cast<unsigned *>(&t.misc[0]), TOPOEP_ST_SELF_DIFF);
+      if (adj) atomicAdd(reinterpret_cast<unsigned long long *>(t.misc + 8), (unsigned long long)adj);
+    }
+    lds_barrier();
+    gst = (uint32_t)t.misc[0];
+    if (out_of_range(p, *reinterpret_cast<unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
+  } else {
+    gst = TOPOEP_ST_SYNC;
+  }
+  single_plan(p, t, gst, true);
+  // release: every output, the instance list and the offsets before the flags
+  drain_then_barrier();
+  if (tid < 64)
+    for (int b = tid; b < p.nb; b += 64)
+      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Chunk role (workgroup 1 + b): ids [b * chunk, (b + 1) * chunk) stay in
+// registers for the whole plan.  Each wave ranks its ids among equal ids
+// (row-major order) and the workgroup writes its counts and arrives; after its flag,
+// each id's occurrence index rho = (offset of the chunk) + (offset of the
+// wave in the chunk) + (rank in the wave) picks the instance from this
+// rank's instance list.  A bounded wait that gives up writes -1 and SYNC.
+template <int IPT>
+__device__ void fused_chunk(const Plan &p, int b, int *sm) {
+  const ChunkLds l = chunk_lds(p, blockDim.x);
+  int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr, *er = sm + l.er, *eend = sm + l.eend;
+  int *flag = sm + l.flag;
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
+  const int E = p.E;
+  const int64_t lo = (int64_t)b * p.chunk;
+  const int64_t hi = lo + p.chunk < p.n ? lo + p.chunk : p.n;
+  const int64_t wbase = lo + (int64_t)wave * 64 * IPT + lane;
+  int ev[IPT], lr[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    ev[i] = idx < hi ? p.topk[idx] : -1;
+  }
+  int *mywc = wc + wave * E;
+  for (int e = lane; e < E; e += 64) mywc[e] = 0;
+  wave_sync();
+  int bad = 0;
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    const bool inr = idx < hi;
+    const bool valid = inr && (unsigned)ev[i] < (unsigned)E;
+    bad |= (inr && !valid) ? 1 : 0;
+    const uint64_t peers = peer_mask(ev[i], valid, p.nbits);
+    const int c = valid ? mywc[ev[i]] : 0;
+    lr[i] = c + __popcll(peers & lanemask_lt());
+    wave_sync();
+    if (valid && (peers & lanemask_lt()) == 0) mywc[ev[i]] = c + __popcll(peers);
+    wave_sync();
+  }
+  bad = __syncthreads_or(bad);
+  // publish the chunk's counts; wc becomes each wave's offset in the chunk
+  for (int e = tid; e < E; e += nt) {
+    int sum = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int c = wc[w * E + e];
+      wc[w * E + e] = sum;
+      sum += c;
+    }
+    p.pub[b * E + e] = (uint32_t)sum | ((e == 0 && bad) ? 0x80000000u : 0u);
+  }
+  drain_then_barrier();
+  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  // wait for this chunk's flag
+  if (tid == 0) {
+    uint32_t *f = p.flags + (int64_t)b * kFlagStride;
+    uint32_t it = 0;
+    int ok = 1;
+    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+      if (++it > p.spin_limit) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (ok) __hip_atomic_store(f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = ok;
+  }
+  __syncthreads();
+  const bool ok = *flag != 0;
+  uint32_t fin = 0;
+  if (ok) {
+    // the chunk's offsets, the instance list and the final status in one
+    // round trip: every load of a pass issued before any is used
+    fin = __hip_atomic_load(&p.ctrl[kCtrlFinal], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int n_ld = imax(E + 1, p.nent_cap);
+    for (int i = tid; i < n_ld; i += nt) {
+      const int ro = p.offsets[b * E + imin(i, E - 1)];
+      const int pv = p.csr_ptr[imin(i, E)];
+      const int rv = p.csr_r[imin(i, p.nent_cap - 1)];
+      const int xv = p.csr_end[imin(i, p.nent_cap - 1)];
+      if (i < E) run[i] = ro;
+      if (i <= E) ptr[i] = pv < 0 ? 0 : (pv > p.nent_cap ? p.nent_cap : pv);
+      if (i < p.nent_cap) {
+        er[i] = rv;
+        eend[i] = xv;
+      }
+    }
+  }
+  if (!ok || (fin & (kNoPlan | TOPOEP_ST_SYNC))) {
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int64_t idx = wbase + i * 64;
+      if (idx < hi) p.dest_out[idx] = -1;
+    }
+    if (!ok && tid == 0) atomicOr(reinterpret_cast<unsigned *>(p.status_out), TOPOEP_ST_SYNC);
+    return;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    if (idx < hi) {
+      int dest = -1;
+      if ((unsigned)ev[i] < (unsigned)E) {
+        const int rho = run[ev[i]] + wc[wave * E + ev[i]] + lr[i];
+        const int j1 = ptr[ev[i] + 1];
+        for (int j = ptr[ev[i]]; j < j1; ++j) {
+          if (rho < eend[j]) {
+            dest = er[j];
+            break;
+          }
+        }
+      }
+      p.dest_out[idx] = dest;
+    }
+  }
+}
+
+// The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold
+// the ids; all are resident at once (nb <= kMaxFusedBlocks) and every wait
+// is bounded.
+template <int IPT>
+__global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
+  extern __shared__ int64_t smem_f[];
+  int *sm = reinterpret_cast<int *>(smem_f);
+  if (blockIdx.x == 0) fused_solver(p, sm);
+  else fused_chunk<IPT>(p, blockIdx.x - 1, sm);
+}
+
+// Same launch shape, empty body: the launch floor of a plan's kernel.
+__global__ __launch_bounds__(1024) void empty_kernel(Plan p) { (void)p; }
+
 // ---------------------------------------------------------------- host side
 
 struct Shape {
   int ipt, bt, st;
-  int single;     // 1: one workgroup plans every domain
-  size_t lds_hist, lds_solve, lds_reroute;
+  int mode;       // 1 single-workgroup solver, 2 per-domain solver (three kernels each), 3 one launch
+  size_t lds_hist, lds_solve, lds_reroute, lds_fused;
   int solve_groups;
 };
 
@@ -1503,15 +1962,63 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.fMI = make_fastdiv((uint32_t)(q.M * q.I));
 
   Shape s;
-  s.ipt = lc && lc->items_per_thread ? lc->items_per_thread : 4;
+  const int ipt_req = lc ? lc->items_per_thread : 0;
+  s.ipt = ipt_req ? ipt_req : 4;
   s.bt = lc && lc->block_threads ? lc->block_threads : 256;
   s.st = lc && lc->solve_threads ? lc->solve_threads : 0;
   const int solver = lc ? lc->solver : 0;
-  if (solver < 0 || solver > 2) return TOPOEP_EINVAL;
+  if (solver < 0 || solver > 3) return TOPOEP_EINVAL;
   if (!(s.ipt == 1 || s.ipt == 2 || s.ipt == 4 || s.ipt == 8)) return TOPOEP_EINVAL;
   if (s.bt < 64 || s.bt > 1024 || s.bt % 64) return TOPOEP_EINVAL;
   if (s.st != 0 && (s.st < 64 || s.st > 1024 || s.st % 64)) return TOPOEP_EINVAL;
   if (lc && lc->tiles_per_block < 0) return TOPOEP_EINVAL;
+
+  // the single-workgroup solver when its whole state fits in LDS
+  const int64_t single_words = (int64_t)single_lds(q).words;
+  const int64_t multi_words = (int64_t)domain_lds(q).words;
+  const bool single_fits = single_words * 4 <= kLdsLimit;
+  const bool multi_fits = multi_words * 4 <= kLdsLimit;
+
+  // one launch: the single-workgroup solver plus at most kMaxFusedBlocks
+  // chunk workgroups of st threads holding ipt ids per thread
+  {
+    const int st = s.st ? s.st : 1024;
+    int ipt = 0;
+    int64_t nbf = 0;
+    // the solver polls the published counts with at most kPollMax chunks per
+    // thread: nb <= kPollMax, or nb <= kPollMax * (st / E) with E <= st
+    const int64_t poll_cap = E <= st ? (int64_t)kPollMax * (st / E) : (int64_t)kPollMax;
+    for (int c = 1; c <= 8; c *= 2) {
+      if (ipt_req && c != ipt_req) continue;
+      const int64_t nbc = q.n > 0 ? (q.n + (int64_t)st * c - 1) / ((int64_t)st * c) : 1;
+      if (nbc <= kMaxFusedBlocks && nbc <= poll_cap && (ipt == 0 || nbf > kFusedBlocks)) {
+        ipt = c;
+        nbf = nbc;
+      }
+    }
+    const int64_t chunk_words = (int64_t)chunk_lds(q, st).words;
+    // (1 KiB left for the kernel's static LDS, which __syncthreads_or uses)
+    const int64_t fused_words = single_words > chunk_words ? single_words : chunk_words;
+    const bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
+    if (solver == 3 && !fused_ok) return TOPOEP_ELIMIT;
+    if (fused_ok && (solver == 3 || solver == 0)) {
+      s.mode = 3;
+      s.ipt = ipt;
+      s.st = st;
+      q.chunk = (int64_t)st * ipt;
+      q.nb = (int)nbf;
+      q.pgroups = nbf <= kPollMax ? 1 : (int)((nbf + kPollMax - 1) / kPollMax);
+      q.n_solvers = 1;
+      q.n_helpers = 0;
+      s.solve_groups = 1;
+      s.lds_hist = s.lds_solve = s.lds_reroute = 0;
+      s.lds_fused = (size_t)fused_words * 4;
+    } else {
+      s.mode = 0;
+    }
+  }
+
+  if (s.mode != 3) {
   const int64_t tile = (int64_t)s.bt * s.ipt;
   const int64_t tiles = (q.n + tile - 1) / tile;
   int64_t tpb = lc && lc->tiles_per_block > 0 ? lc->tiles_per_block
@@ -1522,29 +2029,36 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   if (nb > (1 << 24)) return TOPOEP_ELIMIT;
   q.nb = (int)nb;
   q.n_helpers = (E + kOffsetExperts - 1) / kOffsetExperts;
-
-  // the single-workgroup solver when its whole state fits in LDS
-  const int64_t single_words = (int64_t)single_lds(q).words;
-  const int64_t multi_words = (int64_t)domain_lds(q).words;
-  const bool single_fits = single_words * 4 <= kLdsLimit;
-  const bool multi_fits = multi_words * 4 <= kLdsLimit;
   if (solver == 1) {
     if (!single_fits) return TOPOEP_ELIMIT;
-    s.single = 1;
+    s.mode = 1;
   } else if (solver == 2) {
     if (!multi_fits) return TOPOEP_ELIMIT;
-    s.single = 0;
+    s.mode = 2;
   } else {
     if (!single_fits && !multi_fits) return TOPOEP_ELIMIT;
-    s.single = single_fits ? 1 : 0;
+    s.mode = single_fits ? 1 : 2;
   }
-  if (s.st == 0) s.st = s.single ? 1024 : 512;
-  s.lds_solve = (size_t)(s.single ? single_words : multi_words) * 4;
-  q.n_solvers = s.single ? 1 : imin(q.M, kMaxSolveGroups);
+  if (s.st == 0) s.st = s.mode == 1 ? 1024 : 512;
+  s.lds_solve = (size_t)(s.mode == 1 ? single_words : multi_words) * 4;
+  q.n_solvers = s.mode == 1 ? 1 : imin(q.M, kMaxSolveGroups);
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
   s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap) * 4;
+  s.lds_fused = 0;
   if (s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
+  }
+
+  // routing: the largest divisor c of M with (instances routed at once) * c
+  // <= solver threads, so every thread routes whole source domains
+  auto chunks_for = [&](int64_t ni) {
+    int best = 1;
+    for (int c = 1; c <= q.M; ++c)
+      if (q.M % c == 0 && ni * c <= s.st) best = c;
+    return best;
+  };
+  q.rchunks_all = chunks_for((int64_t)q.M * q.I);
+  q.rchunks_dom = chunks_for(q.I);
 
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -1562,6 +2076,9 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   const size_t o_cptr = take((size_t)(E + 1) * 4);
   const size_t o_cr = take((size_t)q.nent_cap * 4);
   const size_t o_ce = take((size_t)q.nent_cap * 4);
+  const bool one = s.mode == 3;
+  const size_t o_pub = take(one ? (size_t)q.nb * E * 4 : 0);
+  const size_t o_flg = take(one ? (size_t)q.nb * kFlagStride * 4 : 0);
   *ws_bytes = off;
   if (ws) {
     q.ctrl = reinterpret_cast<uint32_t *>(ws + o_ctrl);
@@ -1574,6 +2091,8 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     q.csr_ptr = reinterpret_cast<int32_t *>(ws + o_cptr);
     q.csr_r = reinterpret_cast<int32_t *>(ws + o_cr);
     q.csr_end = reinterpret_cast<int32_t *>(ws + o_ce);
+    q.pub = one ? reinterpret_cast<uint32_t *>(ws + o_pub) : nullptr;
+    q.flags = one ? reinterpret_cast<uint32_t *>(ws + o_flg) : nullptr;
   }
   *p = q;
   *sh = s;
@@ -1600,6 +2119,11 @@ void set_attrs() {
   allow_lds(reroute_kernel<8>);
   allow_lds(solve_kernel);
   allow_lds(solve_single_kernel);
+  allow_lds(plan_fused_kernel<1>);
+  allow_lds(plan_fused_kernel<2>);
+  allow_lds(plan_fused_kernel<4>);
+  allow_lds(plan_fused_kernel<8>);
+  allow_lds(empty_kernel);
   g_attrs_set = true;
 }
 
@@ -1624,9 +2148,41 @@ void launch_reroute(const Plan &p, const Shape &s, hipStream_t st) {
 }
 
 void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
-  if (s.single) hipLaunchKernelGGL(solve_single_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
+  if (s.mode == 1) hipLaunchKernelGGL(solve_single_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
   else hipLaunchKernelGGL(solve_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
 }
+
+void launch_fused(const Plan &p, const Shape &s, hipStream_t st) {
+  const dim3 g(p.nb + 1), b(s.st);
+  switch (s.ipt) {
+    case 1: hipLaunchKernelGGL(plan_fused_kernel<1>, g, b, s.lds_fused, st, p); break;
+    case 2: hipLaunchKernelGGL(plan_fused_kernel<2>, g, b, s.lds_fused, st, p); break;
+    case 4: hipLaunchKernelGGL(plan_fused_kernel<4>, g, b, s.lds_fused, st, p); break;
+    default: hipLaunchKernelGGL(plan_fused_kernel<8>, g, b, s.lds_fused, st, p); break;
+  }
+}
+
+// Kernels of one plan in launch order: grid, threads, dynamic LDS.
+int plan_kernels(const Plan &p, const Shape &s, int grid[3], int block[3], size_t lds[3]) {
+  if (s.mode == 3) {
+    grid[0] = p.nb + 1;
+    block[0] = s.st;
+    lds[0] = s.lds_fused;
+    return 1;
+  }
+  grid[0] = p.nb;
+  block[0] = s.bt;
+  lds[0] = s.lds_hist;
+  grid[1] = s.solve_groups;
+  block[1] = s.st;
+  lds[1] = s.lds_solve;
+  grid[2] = p.nb;
+  block[2] = s.bt;
+  lds[2] = s.lds_reroute;
+  return 3;
+}
+
+constexpr int kFloorMask = 8;
 
 int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_load,
             const int32_t *local_topk, int32_t T, int32_t k, int32_t N, int32_t *replica_slots,
@@ -1652,9 +2208,19 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
   set_attrs();
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  if (stage_mask & 1) launch_hist(p, s, st);
-  if (stage_mask & 2) launch_solve(p, s, st);
-  if (stage_mask & 4) launch_reroute(p, s, st);
+  if (stage_mask == kFloorMask) {
+    int grid[3], block[3];
+    size_t lds[3];
+    const int nk = plan_kernels(p, s, grid, block, lds);
+    for (int i = 0; i < nk; ++i) hipLaunchKernelGGL(empty_kernel, dim3(grid[i]), dim3(block[i]), lds[i], st, p);
+  } else if (s.mode == 3) {
+    if (stage_mask != 7 && stage_mask != 1) return TOPOEP_EINVAL;   // one kernel: the plan, or stage 0
+    launch_fused(p, s, st);
+  } else {
+    if (stage_mask & 1) launch_hist(p, s, st);
+    if (stage_mask & 2) launch_solve(p, s, st);
+    if (stage_mask & 4) launch_reroute(p, s, st);
+  }
   return hipGetLastError() == hipSuccess ? TOPOEP_OK : TOPOEP_EHIP;
 }
 
@@ -1686,6 +2252,30 @@ int topoep_plan_ex(const topoep_topology *topo, const int32_t *global_load, cons
                  send_counts, status, workspace, workspace_bytes, stream, launch);
 }
 
+int topoep_plan_shape(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
+                      const topoep_launch *launch, topoep_shape *out) {
+  if (!out) return TOPOEP_EINVAL;
+  Plan p;
+  Shape s;
+  size_t need = 0;
+  const int rc = setup(topo, T, k, replica_budget, launch, &p, &s, &need, nullptr);
+  if (rc != TOPOEP_OK) return rc;
+  int grid[3] = {0, 0, 0}, block[3] = {0, 0, 0};
+  size_t lds[3] = {0, 0, 0};
+  topoep_shape o = {};
+  o.kernels = plan_kernels(p, s, grid, block, lds);
+  o.solver = s.mode;
+  o.items_per_thread = s.ipt;
+  o.chunk_blocks = p.nb;
+  for (int i = 0; i < 3; ++i) {
+    o.grid[i] = grid[i];
+    o.block[i] = block[i];
+    o.lds_bytes[i] = (int32_t)lds[i];
+  }
+  *out = o;
+  return TOPOEP_OK;
+}
+
 int topoep_plan(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
                 int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots, int32_t *token_dest,
                 int32_t *send_counts, int32_t *status, void *workspace, size_t workspace_bytes,
@@ -1698,7 +2288,7 @@ int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t 
                       const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
                       int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts, int32_t *status,
                       void *workspace, size_t workspace_bytes, void *stream, const topoep_launch *launch) {
-  if (stage < 0 || stage > 2) return TOPOEP_EINVAL;
+  if (stage < 0 || stage > TOPOEP_STAGE_FLOOR) return TOPOEP_EINVAL;
   return enqueue(1 << stage, topo, global_load, local_topk, T, k, replica_budget, replica_slots,
                  token_dest, send_counts, status, workspace, workspace_bytes, stream, launch);
 }

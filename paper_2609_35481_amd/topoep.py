@@ -30,6 +30,12 @@ ST_ITER = 32
 STAGE_HIST = 0
 STAGE_SOLVE = 1
 STAGE_REROUTE = 2
+STAGE_FLOOR = 3
+
+SOLVER_AUTO = 0
+SOLVER_SINGLE = 1
+SOLVER_PER_DOMAIN = 2
+SOLVER_FUSED = 3
 
 
 class Topology(ctypes.Structure):
@@ -45,6 +51,20 @@ class Launch(ctypes.Structure):
     _fields_ = [("items_per_thread", ctypes.c_int32), ("block_threads", ctypes.c_int32),
                 ("tiles_per_block", ctypes.c_int32), ("solve_threads", ctypes.c_int32),
                 ("solver", ctypes.c_int32)]
+
+
+class Shape(ctypes.Structure):
+    """topoep_shape: the kernels one plan enqueues (count, grid, threads, LDS)."""
+    _fields_ = [("kernels", ctypes.c_int32), ("solver", ctypes.c_int32),
+                ("items_per_thread", ctypes.c_int32), ("chunk_blocks", ctypes.c_int32),
+                ("grid", ctypes.c_int32 * 3), ("block", ctypes.c_int32 * 3),
+                ("lds_bytes", ctypes.c_int32 * 3)]
+
+    def as_dict(self):
+        n = self.kernels
+        return {"kernels": n, "solver": self.solver, "items_per_thread": self.items_per_thread,
+                "chunk_blocks": self.chunk_blocks, "grid": list(self.grid)[:n],
+                "block": list(self.block)[:n], "lds_bytes": list(self.lds_bytes)[:n]}
 
 
 class TopoepError(RuntimeError):
@@ -74,9 +94,12 @@ _lib.topoep_plan_ex.restype = ctypes.c_int
 _lib.topoep_plan_ex.argtypes = _PLAN_ARGS + [ctypes.POINTER(Launch)]
 _lib.topoep_plan_stage.restype = ctypes.c_int
 _lib.topoep_plan_stage.argtypes = [_i32] + _PLAN_ARGS + [ctypes.POINTER(Launch)]
+_lib.topoep_plan_shape.restype = ctypes.c_int
+_lib.topoep_plan_shape.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32, ctypes.POINTER(Launch),
+                                   ctypes.POINTER(Shape)]
 
 EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
-           "topoep_plan_ex", "topoep_plan_stage")
+           "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape")
 
 
 def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
@@ -100,6 +123,15 @@ def workspace_bytes(topo: Topology, T: int, k: int, replica_budget: int, launch=
     return out.value
 
 
+def plan_shape(topo: Topology, T: int, k: int, replica_budget: int, launch=None) -> Shape:
+    out = Shape()
+    rc = _lib.topoep_plan_shape(ctypes.byref(topo), T, k, replica_budget, _launch_ptr(launch),
+                                ctypes.byref(out))
+    if rc != OK:
+        raise TopoepError("topoep_plan_shape", rc)
+    return out
+
+
 def _dev_i32(t, name, shape=None):
     if not isinstance(t, torch.Tensor) or t.dtype != torch.int32 or not t.is_cuda:
         raise TypeError("%s must be a CUDA int32 tensor" % name)
@@ -121,14 +153,17 @@ class Planner:
         dev = torch.device(device if device is not None else "cuda")
         R = topo.num_ranks
         self.ws_bytes = workspace_bytes(topo, self.T, self.k, self.N, launch)
-        # 256-byte aligned workspace carved from a byte tensor
-        self._ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
+        self.shape = plan_shape(topo, self.T, self.k, self.N, launch)
+        # 256-byte aligned workspace carved from a byte tensor, zero-filled
+        # once (every plan leaves its control words zero again)
+        self._ws = torch.zeros(self.ws_bytes + 256, dtype=torch.uint8, device=dev)
         base = self._ws.data_ptr()
         self.ws_ptr = (base + 255) & ~255
         self.replica_slots = torch.empty((R, self.N), dtype=torch.int32, device=dev)
         self.token_dest = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
         self.send_counts = torch.empty((R,), dtype=torch.int32, device=dev)
-        self.status = torch.empty((1,), dtype=torch.int32, device=dev)
+        # status[0] = TOPOEP_ST_* bits, status[1] = refinement moves committed
+        self.status = torch.empty((2,), dtype=torch.int32, device=dev)
 
     def _args(self, global_load, local_topk, stream):
         R, E = self.topo.num_ranks, self.topo.num_experts
@@ -153,7 +188,9 @@ class Planner:
         return self.replica_slots, self.token_dest, self.send_counts, self.status
 
     def stage(self, stage: int, global_load, local_topk, stream=None):
-        """Enqueue one kernel of the plan (0 hist, 1 solve, 2 reroute)."""
+        """Enqueue one kernel of the plan (three kernels: 0 hist, 1 solve,
+        2 reroute; one kernel: 0), or STAGE_FLOOR: the plan's kernels with
+        empty bodies."""
         rc = _lib.topoep_plan_stage(stage, *self._args(global_load, local_topk, stream),
                                     _launch_ptr(self.launch))
         if rc != OK:
@@ -167,7 +204,7 @@ class Planner:
 def plan(topo: Topology, global_load, local_topk, replica_budget: int, stream=None, launch=None):
     """One-shot plan: allocates outputs and workspace, enqueues topoep_plan.
 
-    Returns (replica_slots [R, N], token_dest [T, k], send_counts [R], status [1])
+    Returns (replica_slots [R, N], token_dest [T, k], send_counts [R], status [2])
     as CUDA int32 tensors, valid once the stream reaches them.
     """
     T, k = (int(local_topk.shape[0]), int(local_topk.shape[1])) if local_topk is not None else (0, 1)

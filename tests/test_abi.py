@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert "topoep_plan" in names and "topoep_workspace_bytes" in names
-    assert len(names) == 5
+    assert len(names) == 6
 
 
 def test_library_exports_every_declared_symbol(tp):
@@ -39,6 +39,7 @@ def test_struct_layout_matches_header(tp):
     assert ctypes.sizeof(tp.Topology) == 6 * 4 + 2 * 8
     assert tp.Topology.tok_bytes.offset == 24
     assert ctypes.sizeof(tp.Launch) == 20
+    assert ctypes.sizeof(tp.Shape) == 13 * 4
 
 
 def base(tp, **kw):
@@ -92,3 +93,60 @@ def test_plan_rejects_null_and_small_workspace_without_launching(tp):
         tp.workspace_bytes(t, 16, 2, 1, launch=(3, 256, 0, 256))
     with pytest.raises(tp.TopoepError):
         tp.workspace_bytes(t, 16, 2, 1, launch=(4, 96, 0, 256))
+
+
+def test_plan_shape_choices(tp):
+    """One launch when the single-workgroup solver fits and the ids fit 128
+    workgroups; three kernels otherwise (host-side choice only)."""
+    t = tp.topology(32, 8, 256, 0, 1, 8, 14336, 88080384)
+    sh = tp.plan_shape(t, 8192, 8, 2)
+    assert sh.kernels == 1 and sh.solver == tp.SOLVER_FUSED and sh.chunk_blocks == 64
+    assert sh.grid[0] == 65 and sh.block[0] == 1024 and sh.items_per_thread == 1
+    sh = tp.plan_shape(t, 8192, 8, 2, launch=(4, 0, 0, 0, 3))
+    assert sh.chunk_blocks == 16 and sh.items_per_thread == 4
+    # 512 threads, 8 ids each: 16 chunks, one poll group
+    sh = tp.plan_shape(t, 8192, 8, 2, launch=(8, 0, 0, 512, 3))
+    assert sh.chunk_blocks == 16 and sh.block[0] == 512
+    # 256 threads cannot poll 32 chunks of 256 experts (16 per thread)
+    with pytest.raises(tp.TopoepError):
+        tp.plan_shape(t, 8192, 8, 2, launch=(8, 0, 0, 256, 3))
+    sh = tp.plan_shape(t, 8192, 8, 2, launch=(0, 0, 0, 0, 1))
+    assert sh.kernels == 3 and sh.solver == tp.SOLVER_SINGLE
+    # too many ids for 128 one-launch workgroups: three kernels
+    sh = tp.plan_shape(t, 1 << 20, 8, 2)
+    assert sh.kernels == 3
+    with pytest.raises(tp.TopoepError):
+        tp.plan_shape(t, 1 << 20, 8, 2, launch=(0, 0, 0, 0, 3))
+    # a solver state too large for one workgroup: per-domain solver
+    big = tp.topology(256, 8, 512, 0, 1, 16, 4096, 9 << 20)
+    sh = tp.plan_shape(big, 16384, 8, 4)
+    assert sh.kernels == 3 and sh.solver == tp.SOLVER_PER_DOMAIN
+    with pytest.raises(tp.TopoepError):
+        tp.plan_shape(t, 8192, 8, 2, launch=(0, 0, 0, 0, 4))
+
+
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:
+        return True
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="launches on placeholder pointers: only where no GPU is present")
+@pytest.mark.parametrize("solver", [0, 1, 2, 3])
+def test_valid_calls_reach_the_launch(tp, solver):
+    """With no GPU present a valid call passes every host check and fails at
+    the launch (EHIP): argument validation accepts every stage the plan has."""
+    t = base(tp)
+    launch = tp.Launch(0, 0, 0, 0, solver)
+    ws = tp.workspace_bytes(t, 16, 2, 1, launch=launch)
+    args = (ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 4096, 8192, ws, None)
+    assert tp._lib.topoep_plan_ex(*args, ctypes.byref(launch)) == tp.EHIP
+    kernels = tp.plan_shape(t, 16, 2, 1, launch=launch).kernels
+    for stage in range(kernels):
+        assert tp._lib.topoep_plan_stage(stage, *args, ctypes.byref(launch)) == tp.EHIP, stage
+    assert tp._lib.topoep_plan_stage(tp.STAGE_FLOOR, *args, ctypes.byref(launch)) == tp.EHIP
+    for stage in range(kernels, 3):
+        assert tp._lib.topoep_plan_stage(stage, *args, ctypes.byref(launch)) == tp.EINVAL, stage
+    assert tp._lib.topoep_plan_stage(4, *args, ctypes.byref(launch)) == tp.EINVAL

@@ -1,5 +1,6 @@
 """GPU parity: every output of the HIP planner (replica_slots, token_dest,
-send_counts, status) equals the oracle's bit for bit, through the C ABI.
+send_counts, status bits and refinement move count) equals the oracle's bit
+for bit, through the C ABI.
 
 Integer work throughout, so the bar is exact equality.  Cases: the paper's
 worked example, seeded random tiny instances (ragged sizes, every topology
@@ -42,7 +43,7 @@ def gpu_plan(R, G, E, self_rank, cI, cX, S, W, N, gl, tk, launch=None):
     slots, dest, sc, st = p.plan(gl_d, tk_d)
     torch.cuda.synchronize()
     return dict(replica_slots=slots.cpu().numpy(), token_dest=dest.cpu().numpy(),
-                send_counts=sc.cpu().numpy(), status=int(st.item()))
+                send_counts=sc.cpu().numpy(), status=int(st[0].item()), move_count=int(st[1].item()))
 
 
 def ref_plan(R, G, E, self_rank, cI, cX, S, W, N, gl, tk):
@@ -52,6 +53,7 @@ def ref_plan(R, G, E, self_rank, cI, cX, S, W, N, gl, tk):
 
 def assert_same(got, ref, what=""):
     assert got["status"] == ref["status"], (what, got["status"], ref["status"])
+    assert got["move_count"] == ref["move_count"], (what, got["move_count"], ref["move_count"])
     for key in ("replica_slots", "send_counts", "token_dest"):
         a, b = got[key], ref[key]
         assert a.shape == b.shape, (what, key, a.shape, b.shape)
@@ -89,7 +91,7 @@ def test_worked_example(self_rank):
 
 # ---------------------------------------------------------------- random tiny
 
-SOLVERS = {"single": (0, 0, 0, 0, 1), "perdomain": (0, 0, 0, 0, 2)}
+SOLVERS = {"single": (0, 0, 0, 0, 1), "perdomain": (0, 0, 0, 0, 2), "fused": (0, 0, 0, 0, 3)}
 
 
 @pytest.mark.parametrize("solver", sorted(SOLVERS))
@@ -270,7 +272,8 @@ def test_many_domains_more_than_solver_groups():
 # ---------------------------------------------------------------- determinism
 
 LAUNCHES = [(1, 64, 0, 64, 2), (2, 128, 1, 128, 1), (4, 256, 0, 256, 2), (8, 256, 2, 512, 1),
-            (8, 1024, 0, 1024, 2), (1, 1024, 3, 64, 1), (4, 512, 1, 256, 0)]
+            (8, 1024, 0, 1024, 2), (1, 1024, 3, 64, 1), (4, 512, 1, 256, 0),
+            (1, 0, 0, 1024, 3), (2, 0, 0, 1024, 3), (4, 0, 0, 512, 3), (4, 0, 0, 1024, 3), (8, 0, 0, 512, 3)]
 
 
 @pytest.mark.parametrize("launch", LAUNCHES)
@@ -302,14 +305,16 @@ def test_repeated_runs_identical():
     assert np.array_equal(first[1].cpu().numpy(), ref["token_dest"])
 
 
-def test_graph_replay_matches_eager():
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+def test_graph_replay_matches_eager(solver):
     """The enqueue is captured in a HIP graph and replayed with eager work in
     between; every replay equals the oracle."""
+    say("case graph replay", solver)
     cfg = workload.get("qwen3")
     gl, tk = workload.make_layer(cfg, 4, 1, 0)
     ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
-    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV, launch=SOLVERS[solver])
     gl_d = torch.from_numpy(gl).to(DEV)
     tk_d = torch.from_numpy(tk).to(DEV)
     s = torch.cuda.Stream()
@@ -328,7 +333,8 @@ def test_graph_replay_matches_eager():
         g.replay()
         torch.cuda.synchronize()
         got = dict(replica_slots=p.replica_slots.cpu().numpy(), token_dest=p.token_dest.cpu().numpy(),
-                   send_counts=p.send_counts.cpu().numpy(), status=int(p.status.item()))
+                   send_counts=p.send_counts.cpu().numpy(), status=int(p.status[0].item()),
+                   move_count=int(p.status[1].item()))
         assert_same(got, ref, "graph replay %d" % i)
         del junk
 
@@ -339,7 +345,8 @@ def test_single_stages_repeat():
     gl, tk = workload.make_layer(cfg, 0, 0, 0)
     ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
-    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV, launch=SOLVERS["single"])
+    assert p.shape.kernels == 3
     gl_d = torch.from_numpy(gl).to(DEV)
     tk_d = torch.from_numpy(tk).to(DEV)
     p.plan(gl_d, tk_d)
@@ -350,3 +357,52 @@ def test_single_stages_repeat():
             p.stage(2, gl_d, tk_d)
         torch.cuda.synchronize()
         assert np.array_equal(p.token_dest.cpu().numpy(), ref["token_dest"]), stage
+
+
+def test_one_launch_stage_and_control_words():
+    """With one kernel, stage 0 is the whole plan; stages 1 and 2 are
+    rejected; after every plan the hand-over words of the one-launch plan are
+    zero again, so a plan on a reused workspace needs no clearing."""
+    cfg = workload.get("dsv3")
+    gl, tk = workload.make_layer(cfg, 5, 0, 0)
+    ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV, launch=SOLVERS["fused"])
+    assert p.shape.kernels == 1 and p.shape.solver == topoep.SOLVER_FUSED
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    for i in range(4):
+        p.token_dest.fill_(-9)
+        if i % 2:
+            p.stage(0, gl_d, tk_d)
+        else:
+            p.plan(gl_d, tk_d)
+        torch.cuda.synchronize()
+        assert np.array_equal(p.token_dest.cpu().numpy(), ref["token_dest"]), i
+        # the arrival counter (control word 8) and the ready flags (the
+        # last workspace region of the one-launch plan) are zero again
+        nb = p.shape.chunk_blocks
+        tail = -(-nb * 128 // 256) * 256
+        ws = p.workspace_view().cpu().numpy()
+        assert ws[:256].view(np.uint32)[8] == 0
+        assert not ws[len(ws) - tail:].any()
+    for stage in (1, 2):
+        with pytest.raises(topoep.TopoepError):
+            p.stage(stage, gl_d, tk_d)
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+def test_launch_floor_writes_nothing(solver):
+    """The launch-floor stage runs empty kernels of the plan's shapes."""
+    cfg = workload.get("qwen3")
+    gl, tk = workload.make_layer(cfg, 0, 0, 0)
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV, launch=SOLVERS[solver])
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    for t in (p.token_dest, p.send_counts, p.replica_slots, p.status):
+        t.fill_(-9)
+    p.stage(topoep.STAGE_FLOOR, gl_d, tk_d)
+    torch.cuda.synchronize()
+    for t in (p.token_dest, p.send_counts, p.replica_slots, p.status):
+        assert bool((t == -9).all())

@@ -46,6 +46,7 @@ def test_worked_example(self_rank):
     assert out["load_routed"][:2].tolist() == exp["loads_after_stage1_gpu0_gpu1"]
     # refinement: one move, E4 from GPU 0 to a new replica on GPU 1, four assignments
     assert out["n_moves"] == len(exp["refinement_moves"])
+    assert out["move_count"] == len(exp["refinement_moves"])
     d, rb, rt, e, delta, created = out["moves"][0].tolist()
     mv = exp["refinement_moves"][0]
     assert (e, rb, rt, delta, bool(created)) == (mv["e"], mv["from"], mv["to"], mv["delta"], mv["created"])

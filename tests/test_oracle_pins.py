@@ -175,6 +175,8 @@ def test_refinement_steps(seed):
         _, cands = enumerate_candidates(t, x, q, used, d, brute_split=False)
         assert best_candidate(cands) is None
     assert i == out["n_moves"]
+    # the second status word reports the same count (each iteration commits one move)
+    assert out["move_count"] == out["n_moves"] == int(out["iters"].sum())
     assert (q == out["q_final"]).all()
     assert (x == out["x_final"].astype(bool)).all()
     assert (loads(q) == out["load_final"]).all()
