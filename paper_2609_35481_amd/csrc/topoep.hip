@@ -149,7 +149,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
 
 // LDS layout of a chunk workgroup of the single-launch plan (nt threads).
 struct ChunkLds {
-  int wc, run, ptr, er, eend, flag, words;
+  int wc, run, ptr, er, eend, gs, flag, words;
 };
 
 __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
@@ -160,6 +160,7 @@ __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
   l.ptr = o;  o += p.E + 1;                  // instance list: first entry per expert
   l.er = o;   o += p.nent_cap;               //   instance rank
   l.eend = o; o += p.nent_cap;               //   cumulative share
+  l.gs = o;   o += imax(nt, p.E);            // partial sums of the chunk's offsets
   l.flag = o; o += 4;
   l.words = o;
   return l;
@@ -757,8 +758,9 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // itself, then the other sources ascending, then rb (or plain ascending when
 // the intra-domain cost is zero).  The loop ends when no candidate has
 // delta >= 1.  Returns the number of moves committed.  With prepared, em
-// already holds the masks and the wave sums the rank loads Lr itself;
-// otherwise Lr is given and em is scratch filled here.
+// already holds the masks and the wave sums the rank loads Lr itself (and
+// returns at once when no rank of the domain has a free slot); otherwise Lr
+// is given and em is scratch filled here.
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                   int *Lr, uint64_t *em, uint32_t *flags, bool prepared) {
   const int lane = lane_id();
@@ -766,6 +768,12 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
   if (G < 2) return 0;
   const int r0 = d * G;
   if (prepared) {
+    // At the start of refinement every expert has at most one instance in
+    // the domain (stage 1 places one replica per domain and expert, never in
+    // the main's own domain), so a candidate's target must have a free slot:
+    // without one anywhere in the domain no candidate ever exists.
+    const bool free_slot = lane < G && used[lane] < Neff;
+    if (__ballot(free_slot) == 0) return 0;
     // em already holds the hosting masks; the rank loads are summed here
     if (lane < G) {
       int l = 0;
@@ -1584,10 +1592,14 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 //     then increments the arrival counter with release semantics.  Only the
 //     solver polls the counter (many pollers of one word serialise at the
 //     memory side); it then clears it for the next plan.
-//   solver -> chunk b: after the outputs, this rank's instance list and
-//     every chunk's offset per expert are written, flags[b * kFlagStride]
-//     becomes 1 (release); chunk b polls only its own flag (one 128-byte
-//     line each), then clears it.
+//   solver -> chunk b, flag 1 ("every chunk's counts are written"): set as
+//     soon as the counter is complete; chunk b then sums the counts of the
+//     chunks before it (its first occurrence index per expert) while the
+//     solver works.
+//   solver -> chunk b, flag 2 ("plan ready"): after the outputs and this
+//     rank's instance list are written (release).  Chunk b polls only its
+//     own flag word flags[b * kFlagStride] (one 128-byte line each) and
+//     clears it after seeing 2.
 // Between plans the counter and every flag are zero again; a workspace is
 // zero-filled before its first plan.  A bounded wait that gives up sets SYNC
 // and leaves that state undefined (the workspace is zero-filled again).
@@ -1633,12 +1645,11 @@ __device__ void load_omega(const Plan &p, int *om, int *misc) {
 }
 
 // Solver side of the first hand-over, once every chunk has arrived: the
-// chunks' counts give hs[e] (the histogram of local_topk), offsets[b * E +
-// e] (the count of e in the chunks before b: chunk b's first occurrence
-// index of e) and BAD_ID into misc[0].  With pgroups == 1 a thread takes
-// whole experts (nb <= kPollMax); otherwise thread (g, e) takes chunks
-// [g * per, ...), per <= kPollMax, and pgroups * E <= blockDim.x; scratch
-// holds pgroups * E words.  All of a thread's loads are in flight at once.
+// chunks' counts give hs[e], the histogram of local_topk, and BAD_ID into
+// misc[0].  With pgroups == 1 a thread takes whole experts (nb <=
+// kPollMax); otherwise thread (g, e) takes chunks [g * per, ...), per <=
+// kPollMax, and pgroups * E <= blockDim.x; scratch holds pgroups * E words.
+// All of a thread's loads are in flight at once.
 __device__ void collect_counts(const Plan &p, int *hs, int *scratch, int *misc) {
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb, groups = p.pgroups;
   uint32_t v[kPollMax];
@@ -1648,16 +1659,15 @@ __device__ void collect_counts(const Plan &p, int *hs, int *scratch, int *misc) 
       // branch-free: every load issued before any is used (clamped rows)
 #pragma unroll
       for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(j, nb - 1) * E + e];
-      int base = 0;
+      int sum = 0;
 #pragma unroll
       for (int j = 0; j < kPollMax; ++j) {
         if (j < nb) {
-          p.offsets[j * E + e] = base;
-          base += (int)(v[j] & 0x7FFFFFFFu);
+          sum += (int)(v[j] & 0x7FFFFFFFu);
           bad |= (v[j] >> 31) != 0;
         }
       }
-      hs[e] = base;
+      hs[e] = sum;
     }
     const uint64_t any_bad = __ballot(bad);
     if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
@@ -1667,40 +1677,28 @@ __device__ void collect_counts(const Plan &p, int *hs, int *scratch, int *misc) 
   const int per = (nb + groups - 1) / groups;
   const bool active = tid < groups * E;
   const int g = active ? (int)fdiv((uint32_t)tid, p.fE) : 0;
-  const int e = tid - g * E;
+  const int e = active ? tid - g * E : 0;   // inactive: column 0 (loads are unconditional)
   const int b0 = g * per;
   const int cnt = active ? imax(0, imin(nb, b0 + per) - b0) : 0;
-  // branch-free: every load issued before any is used (clamped rows)
   const int last = imax(0, imin(nb - 1, b0 + cnt - 1));
 #pragma unroll
   for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(b0 + j, last) * E + e];
-#pragma unroll
-  for (int j = 0; j < kPollMax; ++j) v[j] = j < cnt ? v[j] : 0u;
   int sum = 0;
 #pragma unroll
   for (int j = 0; j < kPollMax; ++j) {
-    sum += (int)(v[j] & 0x7FFFFFFFu);
-    bad |= (v[j] >> 31) != 0;
+    if (j < cnt) {
+      sum += (int)(v[j] & 0x7FFFFFFFu);
+      bad |= (v[j] >> 31) != 0;
+    }
   }
   if (active) scratch[tid] = sum;
   const uint64_t any_bad = __ballot(bad);
   if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
   __syncthreads();
-  if (active) {
-    int base = 0, total = 0;
-    for (int g2 = 0; g2 < groups; ++g2) {
-      const int c = scratch[g2 * E + e];
-      if (g2 < g) base += c;
-      total += c;
-    }
-    if (g == 0) hs[e] = total;
-#pragma unroll
-    for (int j = 0; j < kPollMax; ++j) {
-      if (j < cnt) {
-        p.offsets[(b0 + j) * E + e] = base;
-        base += (int)(v[j] & 0x7FFFFFFFu);
-      }
-    }
+  for (int e2 = tid; e2 < E; e2 += nt) {
+    int total = 0;
+    for (int g2 = 0; g2 < groups; ++g2) total += scratch[g2 * E + e2];
+    hs[e2] = total;
   }
   __syncthreads();
 }
@@ -1733,6 +1731,12 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   }
   __syncthreads();
   const bool synced = t.misc[2] != 0;
+  // flag 1: every chunk's counts are written; the chunks sum their offsets
+  // while this workgroup plans (a release, so the chunks' own releases reach
+  // the readers through this workgroup's acquire)
+  if (tid < 64)
+    for (int b = tid; b < p.nb; b += 64)
+      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   if (synced) collect_counts(p, t.hs, t.qcol, t.misc);
   uint32_t gst = 0;
   if (synced) {
@@ -1761,20 +1765,46 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   drain_then_barrier();
   if (tid < 64)
     for (int b = tid; b < p.nb; b += 64)
-      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded wait of chunk b's workgroup until its flag reaches `level`; after
+// level 2 it clears the flag for the next plan.  Thread 0 polls, then an
+// acquire orders the workgroup's later loads (the invalidations cover the
+// whole CU).  Returns false (on every thread) if the wait gave up.
+__device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
+  if (threadIdx.x == 0) {
+    uint32_t *f = p.flags + (int64_t)b * kFlagStride;
+    uint32_t it = 0;
+    int ok = 1;
+    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < level) {
+      if (++it > p.spin_limit) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (ok && level == 2u) __hip_atomic_store(f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = ok;
+  }
+  __syncthreads();
+  return *flag != 0;
 }
 
 // Chunk role (workgroup 1 + b): ids [b * chunk, (b + 1) * chunk) stay in
 // registers for the whole plan.  Each wave ranks its ids among equal ids
-// (row-major order) and the workgroup writes its counts and arrives; after its flag,
-// each id's occurrence index rho = (offset of the chunk) + (offset of the
-// wave in the chunk) + (rank in the wave) picks the instance from this
-// rank's instance list.  A bounded wait that gives up writes -1 and SYNC.
+// (row-major order) and the workgroup writes its counts and arrives; once
+// every chunk has, it sums the counts of the chunks before it; after the
+// plan is ready each id's occurrence index rho = (offset of the chunk) +
+// (offset of the wave in the chunk) + (rank in the wave) picks the
+// instance from this rank's instance list.  A bounded wait that gives up
+// writes -1 and SYNC.
 template <int IPT>
 __device__ void fused_chunk(const Plan &p, int b, int *sm) {
   const ChunkLds l = chunk_lds(p, blockDim.x);
   int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr, *er = sm + l.er, *eend = sm + l.eend;
-  int *flag = sm + l.flag;
+  int *gs = sm + l.gs, *flag = sm + l.flag;
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int E = p.E;
   const int64_t lo = (int64_t)b * p.chunk;
@@ -1816,36 +1846,44 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
   }
   drain_then_barrier();
   if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  // wait for this chunk's flag
-  if (tid == 0) {
-    uint32_t *f = p.flags + (int64_t)b * kFlagStride;
-    uint32_t it = 0;
-    int ok = 1;
-    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-      if (++it > p.spin_limit) {
-        ok = 0;
-        break;
+  // flag >= 1: every chunk's counts are written; this chunk's first
+  // occurrence index of e is the sum of the counts of chunks 0 .. b-1
+  bool ok = wait_flag(p, b, 1u, flag);
+  if (ok) {
+    const int groups = imax(1, nt / E);
+    const int per = (b + groups - 1) / groups;
+    for (int t = tid; t < groups * E; t += nt) {
+      const int g = (int)fdiv((uint32_t)t, p.fE), e = t - g * E;
+      const int b0 = g * per, cnt = imax(0, imin(b, b0 + per) - b0);
+      int sum = 0;
+      for (int j0 = 0; j0 < cnt; j0 += 8) {
+        uint32_t w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) w[u] = p.pub[imin(b0 + j0 + u, b0 + cnt - 1) * E + e];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += j0 + u < cnt ? (int)(w[u] & 0x7FFFFFFFu) : 0;
       }
-      __builtin_amdgcn_s_sleep(2);
+      gs[t] = sum;
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if (ok) __hip_atomic_store(f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = ok;
+    __syncthreads();
+    for (int e = tid; e < E; e += nt) {
+      int sum = 0;
+      for (int g = 0; g < groups; ++g) sum += gs[g * E + e];
+      run[e] = sum;
+    }
+    // flag 2: the plan is ready
+    ok = wait_flag(p, b, 2u, flag);
   }
-  __syncthreads();
-  const bool ok = *flag != 0;
   uint32_t fin = 0;
   if (ok) {
-    // the chunk's offsets, the instance list and the final status in one
-    // round trip: every load of a pass issued before any is used
+    // the instance list and the final status in one round trip: every load
+    // of a pass issued before any is used
     fin = __hip_atomic_load(&p.ctrl[kCtrlFinal], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int n_ld = imax(E + 1, p.nent_cap);
     for (int i = tid; i < n_ld; i += nt) {
-      const int ro = p.offsets[b * E + imin(i, E - 1)];
       const int pv = p.csr_ptr[imin(i, E)];
       const int rv = p.csr_r[imin(i, p.nent_cap - 1)];
       const int xv = p.csr_end[imin(i, p.nent_cap - 1)];
-      if (i < E) run[i] = ro;
       if (i <= E) ptr[i] = pv < 0 ? 0 : (pv > p.nent_cap ? p.nent_cap : pv);
       if (i < p.nent_cap) {
         er[i] = rv;
