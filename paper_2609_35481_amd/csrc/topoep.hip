@@ -60,7 +60,6 @@ constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
 constexpr int kOffsetExperts = 64;      // experts per offset workgroup
 constexpr int kFusedBlocks = 64;        // chunk workgroups the single-launch plan aims for
 constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs)
-constexpr int kPollMax = 16;            // published counts one solver thread polls
 constexpr int kFlagStride = 32;         // words between ready flags (one 128-byte line each)
 constexpr uint32_t kSpinLimit = 1u << 24;
 constexpr uint32_t kIterLimit = 1u << 22;
@@ -72,7 +71,7 @@ struct Plan {
   int cI, cX;
   int64_t S, W;
   int64_t n, chunk;
-  int nb, n_solvers, n_helpers, pgroups;
+  int nb, n_solvers, n_helpers;
   int rchunks_all, rchunks_dom;   // routing: source-domain chunks (divisors of M)
   uint32_t spin_limit, iter_limit;
   FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
@@ -80,7 +79,7 @@ struct Plan {
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
-  uint32_t *pub, *flags;   // one-launch plan: published counts, ready flags
+  uint32_t *pub, *flags, *ghist;   // one-launch plan: chunk counts, flags, histogram (E + 1 words)
 };
 
 __host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
@@ -757,23 +756,25 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // ascending (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt
 // itself, then the other sources ascending, then rb (or plain ascending when
 // the intra-domain cost is zero).  The loop ends when no candidate has
-// delta >= 1.  Returns the number of moves committed.  With prepared, em
-// already holds the masks and the wave sums the rank loads Lr itself (and
-// returns at once when no rank of the domain has a free slot); otherwise Lr
-// is given and em is scratch filled here.
+// delta >= 1.  Returns the number of moves committed (at once 0 when no rank
+// of the domain has a free slot).  With prepared, em already holds the masks
+// and the wave sums the rank loads Lr itself; otherwise Lr is given and em is
+// scratch filled here.
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                   int *Lr, uint64_t *em, uint32_t *flags, bool prepared) {
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return 0;
   const int r0 = d * G;
-  if (prepared) {
-    // At the start of refinement every expert has at most one instance in
-    // the domain (stage 1 places one replica per domain and expert, never in
-    // the main's own domain), so a candidate's target must have a free slot:
-    // without one anywhere in the domain no candidate ever exists.
+  // At the start of refinement every expert has at most one instance in the
+  // domain (stage 1 places one replica per domain and expert, never in the
+  // main's own domain), so a candidate's target must have a free slot:
+  // without one anywhere in the domain no candidate ever exists.
+  {
     const bool free_slot = lane < G && used[lane] < Neff;
     if (__ballot(free_slot) == 0) return 0;
+  }
+  if (prepared) {
     // em already holds the hosting masks; the rank loads are summed here
     if (lane < G) {
       int l = 0;
@@ -1588,10 +1589,13 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 //
 // Workgroup 0 solves; workgroups 1..nb each hold one chunk of ids.
 //   chunk -> solver: chunk b writes its count of every expert to
-//     pub[b * E + e] (bit 31 of expert 0's word: a bad id in the chunk),
-//     then increments the arrival counter with release semantics.  Only the
-//     solver polls the counter (many pollers of one word serialise at the
-//     memory side); it then clears it for the next plan.
+//     pub[b * E + e], adds it to the histogram ghist[e] with an agent-scope
+//     atomic (integer adds commute: the sum does not depend on their order;
+//     ghist[E] collects a bad-id flag), then increments the arrival counter
+//     with release semantics.  Only the solver polls the counter (many
+//     pollers of one word serialise at the memory side); it reads the E + 1
+//     histogram words (one CU cannot pull every chunk's counts quickly) and
+//     clears them and the counter for the next plan.
 //   solver -> chunk b, flag 1 ("every chunk's counts are written"): set as
 //     soon as the counter is complete; chunk b then sums the counts of the
 //     chunks before it (its first occurrence index per expert) while the
@@ -1644,62 +1648,20 @@ __device__ void load_omega(const Plan &p, int *om, int *misc) {
   }
 }
 
-// Solver side of the first hand-over, once every chunk has arrived: the
-// chunks' counts give hs[e], the histogram of local_topk, and BAD_ID into
-// misc[0].  With pgroups == 1 a thread takes whole experts (nb <=
-// kPollMax); otherwise thread (g, e) takes chunks [g * per, ...), per <=
-// kPollMax, and pgroups * E <= blockDim.x; scratch holds pgroups * E words.
-// All of a thread's loads are in flight at once.
-__device__ void collect_counts(const Plan &p, int *hs, int *scratch, int *misc) {
-  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb, groups = p.pgroups;
-  uint32_t v[kPollMax];
+// Solver side of the first hand-over, once every chunk has arrived: hs[e] =
+// ghist[e], the histogram of local_topk, BAD_ID from ghist[E]; then the
+// words are cleared for the next plan.
+__device__ void collect_counts(const Plan &p, int *hs, int *misc) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
   bool bad = false;
-  if (groups == 1) {
-    for (int e = tid; e < E; e += nt) {
-      // branch-free: every load issued before any is used (clamped rows)
-#pragma unroll
-      for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(j, nb - 1) * E + e];
-      int sum = 0;
-#pragma unroll
-      for (int j = 0; j < kPollMax; ++j) {
-        if (j < nb) {
-          sum += (int)(v[j] & 0x7FFFFFFFu);
-          bad |= (v[j] >> 31) != 0;
-        }
-      }
-      hs[e] = sum;
-    }
-    const uint64_t any_bad = __ballot(bad);
-    if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
-    __syncthreads();
-    return;
+  for (int e = tid; e <= E; e += nt) {
+    const uint32_t v = p.ghist[e];
+    if (e < E) hs[e] = (int)v;
+    else bad = v != 0;
+    __hip_atomic_store(p.ghist + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  const int per = (nb + groups - 1) / groups;
-  const bool active = tid < groups * E;
-  const int g = active ? (int)fdiv((uint32_t)tid, p.fE) : 0;
-  const int e = active ? tid - g * E : 0;   // inactive: column 0 (loads are unconditional)
-  const int b0 = g * per;
-  const int cnt = active ? imax(0, imin(nb, b0 + per) - b0) : 0;
-  const int last = imax(0, imin(nb - 1, b0 + cnt - 1));
-#pragma unroll
-  for (int j = 0; j < kPollMax; ++j) v[j] = p.pub[imin(b0 + j, last) * E + e];
-  int sum = 0;
-#pragma unroll
-  for (int j = 0; j < kPollMax; ++j) {
-    if (j < cnt) {
-      sum += (int)(v[j] & 0x7FFFFFFFu);
-      bad |= (v[j] >> 31) != 0;
-    }
-  }
-  if (active) scratch[tid] = sum;
   const uint64_t any_bad = __ballot(bad);
   if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
-  __syncthreads();
-  for (int e2 = tid; e2 < E; e2 += nt) {
-    int total = 0;
-    for (int g2 = 0; g2 < groups; ++g2) total += scratch[g2 * E + e2];
-    hs[e2] = total;
-  }
   __syncthreads();
 }
 
@@ -1737,7 +1699,7 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   if (tid < 64)
     for (int b = tid; b < p.nb; b += 64)
       __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  if (synced) collect_counts(p, t.hs, t.qcol, t.misc);
+  if (synced) collect_counts(p, t.hs, t.misc);
   uint32_t gst = 0;
   if (synced) {
     bool diff = false;
@@ -1769,9 +1731,10 @@ __device__ void fused_solver(const Plan &p, int *sm) {
 }
 
 // Bounded wait of chunk b's workgroup until its flag reaches `level`; after
-// level 2 it clears the flag for the next plan.  Thread 0 polls, then an
-// acquire orders the workgroup's later loads (the invalidations cover the
-// whole CU).  Returns false (on every thread) if the wait gave up.
+// level 2 it clears the flag for the next plan.  Thread 0 polls (more
+// pollers per chunk slow every agent-coherent load down), then acquires (the
+// L1 and L2 invalidations cover the whole CU).  Returns false (on every
+// thread) if the wait gave up.
 __device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
   if (threadIdx.x == 0) {
     uint32_t *f = p.flags + (int64_t)b * kFlagStride;
@@ -1842,8 +1805,10 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
       wc[w * E + e] = sum;
       sum += c;
     }
-    p.pub[b * E + e] = (uint32_t)sum | ((e == 0 && bad) ? 0x80000000u : 0u);
+    p.pub[b * E + e] = (uint32_t)sum;
+    if (sum) atomicAdd(p.ghist + e, (uint32_t)sum);
   }
+  if (tid == 0 && bad) atomicOr(p.ghist + E, 1u);
   drain_then_barrier();
   if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   // flag >= 1: every chunk's counts are written; this chunk's first
@@ -1861,7 +1826,7 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) w[u] = p.pub[imin(b0 + j0 + u, b0 + cnt - 1) * E + e];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) sum += j0 + u < cnt ? (int)(w[u] & 0x7FFFFFFFu) : 0;
+        for (int u = 0; u < 8; ++u) sum += j0 + u < cnt ? (int)w[u] : 0;
       }
       gs[t] = sum;
     }
@@ -2023,13 +1988,10 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     const int st = s.st ? s.st : 1024;
     int ipt = 0;
     int64_t nbf = 0;
-    // the solver polls the published counts with at most kPollMax chunks per
-    // thread: nb <= kPollMax, or nb <= kPollMax * (st / E) with E <= st
-    const int64_t poll_cap = E <= st ? (int64_t)kPollMax * (st / E) : (int64_t)kPollMax;
     for (int c = 1; c <= 8; c *= 2) {
       if (ipt_req && c != ipt_req) continue;
       const int64_t nbc = q.n > 0 ? (q.n + (int64_t)st * c - 1) / ((int64_t)st * c) : 1;
-      if (nbc <= kMaxFusedBlocks && nbc <= poll_cap && (ipt == 0 || nbf > kFusedBlocks)) {
+      if (nbc <= kMaxFusedBlocks && (ipt == 0 || nbf > kFusedBlocks)) {
         ipt = c;
         nbf = nbc;
       }
@@ -2045,7 +2007,6 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
       s.st = st;
       q.chunk = (int64_t)st * ipt;
       q.nb = (int)nbf;
-      q.pgroups = nbf <= kPollMax ? 1 : (int)((nbf + kPollMax - 1) / kPollMax);
       q.n_solvers = 1;
       q.n_helpers = 0;
       s.solve_groups = 1;
@@ -2117,6 +2078,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   const bool one = s.mode == 3;
   const size_t o_pub = take(one ? (size_t)q.nb * E * 4 : 0);
   const size_t o_flg = take(one ? (size_t)q.nb * kFlagStride * 4 : 0);
+  const size_t o_gh = take(one ? (size_t)(E + 1) * 4 : 0);
   *ws_bytes = off;
   if (ws) {
     q.ctrl = reinterpret_cast<uint32_t *>(ws + o_ctrl);
@@ -2131,6 +2093,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     q.csr_end = reinterpret_cast<int32_t *>(ws + o_ce);
     q.pub = one ? reinterpret_cast<uint32_t *>(ws + o_pub) : nullptr;
     q.flags = one ? reinterpret_cast<uint32_t *>(ws + o_flg) : nullptr;
+    q.ghist = one ? reinterpret_cast<uint32_t *>(ws + o_gh) : nullptr;
   }
   *p = q;
   *sh = s;

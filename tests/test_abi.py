@@ -104,12 +104,16 @@ def test_plan_shape_choices(tp):
     assert sh.grid[0] == 65 and sh.block[0] == 1024 and sh.items_per_thread == 1
     sh = tp.plan_shape(t, 8192, 8, 2, launch=(4, 0, 0, 0, 3))
     assert sh.chunk_blocks == 16 and sh.items_per_thread == 4
-    # 512 threads, 8 ids each: 16 chunks, one poll group
+    # 512 threads, 8 ids each: 16 chunks
     sh = tp.plan_shape(t, 8192, 8, 2, launch=(8, 0, 0, 512, 3))
     assert sh.chunk_blocks == 16 and sh.block[0] == 512
-    # 256 threads cannot poll 32 chunks of 256 experts (16 per thread)
-    with pytest.raises(tp.TopoepError):
-        tp.plan_shape(t, 8192, 8, 2, launch=(8, 0, 0, 256, 3))
+    # 128 threads, 4 ids each: 128 chunks, the most one launch takes
+    sh = tp.plan_shape(t, 8192, 8, 2, launch=(4, 0, 0, 128, 3))
+    assert sh.chunk_blocks == 128 and sh.grid[0] == 129
+    # 64 threads, 8 ids each would need 128 chunks of 512 ids: still one launch
+    assert tp.plan_shape(t, 8192, 8, 2, launch=(8, 0, 0, 64, 3)).chunk_blocks == 128
+    with pytest.raises(tp.TopoepError):   # 64 threads, 4 ids: 256 chunks
+        tp.plan_shape(t, 8192, 8, 2, launch=(4, 0, 0, 64, 3))
     sh = tp.plan_shape(t, 8192, 8, 2, launch=(0, 0, 0, 0, 1))
     assert sh.kernels == 3 and sh.solver == tp.SOLVER_SINGLE
     # too many ids for 128 one-launch workgroups: three kernels

@@ -273,7 +273,8 @@ def test_many_domains_more_than_solver_groups():
 
 LAUNCHES = [(1, 64, 0, 64, 2), (2, 128, 1, 128, 1), (4, 256, 0, 256, 2), (8, 256, 2, 512, 1),
             (8, 1024, 0, 1024, 2), (1, 1024, 3, 64, 1), (4, 512, 1, 256, 0),
-            (1, 0, 0, 1024, 3), (2, 0, 0, 1024, 3), (4, 0, 0, 512, 3), (4, 0, 0, 1024, 3), (8, 0, 0, 512, 3)]
+            (1, 0, 0, 1024, 3), (2, 0, 0, 1024, 3), (4, 0, 0, 512, 3), (4, 0, 0, 1024, 3), (8, 0, 0, 512, 3),
+            (8, 0, 0, 256, 3), (4, 0, 0, 128, 3)]
 
 
 @pytest.mark.parametrize("launch", LAUNCHES)
