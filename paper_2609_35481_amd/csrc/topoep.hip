@@ -117,7 +117,7 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
 
 // LDS layout of the single-workgroup solver: every domain's state at once.
 struct SingleLds {
-  int ck, em, fdt, hs, cnt, mask, repl, slots, used, L, e_of, U, misc, om, qcol, words;
+  int ck, em, fdt, hs, cnt, dfree, mask, repl, slots, used, L, e_of, U, misc, om, qcol, words;
 };
 
 __host__ __device__ inline SingleLds single_lds(const Plan &p) {
@@ -128,6 +128,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   l.fdt = o;   o += 2 * (p.M + 1);            // divisors 1..M
   l.hs = o;    o += p.E;                      // histogram of local_topk
   l.cnt = o;   o += p.M;                      // candidates per domain
+  l.dfree = o; o += p.M;                      // 1: a rank of the domain has a free slot
   l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
   l.repl = o;  o += p.M * imax(p.cap1, 1);    // stage-1 replicas per domain
   l.slots = o; o += p.R * imax(p.Neff, 1);    // replica slots of every rank
@@ -683,22 +684,52 @@ __device__ inline int route_batch(const int *src, int stride, int *dst, const Ro
   return sum;
 }
 
-template <class SrcOf, class DomOf>
+// q[self][e][r] of an instance of e in domain d, w = omega[self][e]: the
+// routing rule of route_instances for the single source `self`.
+__device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uint32_t *mask, const FastDiv *fdt) {
+  const int ds = (int)fdiv((uint32_t)p.self, p.fG);
+  if (ds == d) return w;                                   // the instance inside dom(self)
+  const uint32_t *me = mask + e * p.MW;
+  if ((me[ds >> 5] >> (ds & 31)) & 1u) return 0;           // dom(self) hosts e itself
+  int n = 0, below = 0;
+  for (int wd = 0; wd < p.MW; ++wd) {
+    const uint32_t bits = me[wd];
+    n += __popc(bits);
+    const int lo = wd * 32;
+    if (d >= lo + 32) below += __popc(bits);
+    else if (d > lo) below += __popc(bits & ((1u << (d - lo)) - 1u));
+  }
+  const FastDiv fn = fdt[n];
+  const int qq = (int)fdiv_hi((uint32_t)w, fn);
+  return qq + (below < w - qq * n ? 1 : 0);
+}
+
+// full(d): whether every source's q is needed for domain d's instances.  A
+// domain whose refinement cannot move anything (no free slot) only needs
+// q[self] (send counts and this rank's instance list read nothing else, and
+// instance loads feed the refinement only): the chunk holding dom(self)
+// writes that one value; the other sources of the column are left unset.
+template <class SrcOf, class DomOf, class Full>
 __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, int chunks, const int *e_of,
                                 const uint32_t *mask, const FastDiv *fdt, int *qcol, int *U, SrcOf src_of,
-                                int stride, DomOf dom_of) {
+                                int stride, DomOf dom_of, Full full) {
   const int tid = threadIdx.x, nt = blockDim.x, G = p.G;
   const int dpc = p.M / chunks;
+  const int c_self = (int)fdiv((uint32_t)p.self, p.fG) / dpc;
   for (int t = tid; t < NI * chunks; t += nt) {
     const int c = (int)fdiv((uint32_t)t, fNI), i = t - c * NI;
     const int e = e_of[i];
     const int ds0 = c * dpc, ds1 = ds0 + dpc;
     int *row = qcol + i * p.QS;
+    const int d = dom_of(i);
+    if (!full(d)) {
+      if (c == c_self) row[p.self] = e < 0 ? 0 : route_self_q(p, d, e, src_of(i, e)[p.self * stride], mask, fdt);
+      continue;
+    }
     if (e < 0) {
       for (int s = ds0 * G; s < ds1 * G; ++s) row[s] = 0;
       continue;
     }
-    const int d = dom_of(i);
     const uint32_t *me = mask + e * p.MW;
     RouteCase rc;
     rc.n = 0;
@@ -1164,16 +1195,31 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       U[a] = 0;
     }
     lds_barrier();
-    // the columns omega[s][e] of the domain's instances, then q in place
-    for (int t = tid; t < I * R; t += nt) {
-      const int s = (int)fdiv((uint32_t)t, p.fI), a = t - s * I;
-      const int e = e_of[a];
-      qcol[a * p.QS + s] = e < 0 ? 0 : (s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]);
+    // whether the domain can refine at all (a rank with a free slot); if not,
+    // only the q[self] column is needed, else the columns omega[s][e] of the
+    // domain's instances, then q in place
+    if (tid < 64) {
+      const bool fr = __ballot(tid < G && used[tid] < Neff) != 0;   // G <= 64
+      if (tid == 0) misc[5] = fr ? 1 : 0;
+    }
+    lds_barrier();
+    const bool full = misc[5] != 0;
+    if (full) {
+      for (int t = tid; t < I * R; t += nt) {
+        const int s = (int)fdiv((uint32_t)t, p.fI), a = t - s * I;
+        const int e = e_of[a];
+        qcol[a * p.QS + s] = e < 0 ? 0 : (s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]);
+      }
+    } else {
+      for (int a = tid; a < I; a += nt) {
+        const int e = e_of[a];
+        qcol[a * p.QS + p.self] = e < 0 ? 0 : hs[e];
+      }
     }
     lds_barrier();
     route_instances(
         p, I, p.fI, p.rchunks_dom, e_of, mask, fdt, qcol, U, [&](int i, int) { return qcol + i * p.QS; }, 1,
-        [&](int) { return d; });
+        [&](int) { return d; }, [&](int) { return full; });
     lds_barrier();
     for (int j = tid; j < G; j += nt) {
       int l = 0;
@@ -1273,7 +1319,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
 struct SingleState {
   uint64_t *ck, *em;
   FastDiv *fdt;
-  int *hs, *ccnt, *repl, *slots, *used, *Lr, *e_of, *U, *misc, *om, *qcol;
+  int *hs, *ccnt, *dfree, *repl, *slots, *used, *Lr, *e_of, *U, *misc, *om, *qcol;
   uint32_t *mask;
 };
 
@@ -1285,6 +1331,7 @@ __device__ inline SingleState single_state(const Plan &p, int *sm) {
   t.fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
   t.hs = sm + lay.hs;
   t.ccnt = sm + lay.cnt;
+  t.dfree = sm + lay.dfree;
   t.mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
   t.repl = sm + lay.repl;
   t.slots = sm + lay.slots;
@@ -1304,7 +1351,10 @@ __device__ inline SingleState single_state(const Plan &p, int *sm) {
 __device__ inline void single_init(const Plan &p, const SingleState &t) {
   const int tid = threadIdx.x, nt = blockDim.x;
   if (tid < 16) t.misc[tid] = 0;
-  for (int d = tid; d < p.M; d += nt) t.ccnt[d] = 0;
+  for (int d = tid; d < p.M; d += nt) {
+    t.ccnt[d] = 0;
+    t.dfree[d] = 0;
+  }
   for (int i = tid; i < p.E * p.MW; i += nt) t.mask[i] = 0;
   for (int i = tid; i < p.M * p.cap1; i += nt) t.repl[i] = -1;
   for (int i = tid; i < p.M * p.E; i += nt) t.em[i] = 0;
@@ -1319,7 +1369,7 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
-  int *hs = t.hs, *ccnt = t.ccnt, *repl = t.repl, *slots = t.slots, *used = t.used;
+  int *hs = t.hs, *ccnt = t.ccnt, *dfree = t.dfree, *repl = t.repl, *slots = t.slots, *used = t.used;
   int *Lr = t.Lr, *e_of = t.e_of, *U = t.U, *misc = t.misc, *om = t.om, *qcol = t.qcol;
   uint32_t *mask = t.mask;
   (void)hs;
@@ -1401,6 +1451,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
         const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
         used[r] = u;
         for (int t = 0; t < Neff; ++t) slots[r * Neff + t] = t < u ? repl[d * cap + t * G + j] : -1;
+        if (u < Neff) dfree[d] = 1;
       }
     }
   }
@@ -1409,7 +1460,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   // ---- routing construction (Section 4.3) for every domain's instances
   route_instances(
       p, M * I, p.fMI, p.rchunks_all, e_of, mask, fdt, qcol, U, [&](int, int e) { return om + e; }, E,
-      [&](int i) { return (int)fdiv((uint32_t)i, p.fI); });
+      [&](int i) { return (int)fdiv((uint32_t)i, p.fI); }, [&](int d) { return dfree[d] != 0; });
   lds_barrier();
 
   // ---- intra-node refinement (Eq. 10): one wave per domain (it sums its
