@@ -117,7 +117,7 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
 
 // LDS layout of the single-workgroup solver: every domain's state at once.
 struct SingleLds {
-  int ck, em, fdt, hs, cnt, dfree, mask, repl, slots, used, L, e_of, U, misc, om, qcol, words;
+  int ck, em, fdt, hs, cnt, dfree, mask, bm, sendl, wt, repl, slots, used, L, e_of, U, misc, om, qcol, words;
 };
 
 __host__ __device__ inline SingleLds single_lds(const Plan &p) {
@@ -130,6 +130,9 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   l.cnt = o;   o += p.M;                      // candidates per domain
   l.dfree = o; o += p.M;                      // 1: a rank of the domain has a free slot
   l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
+  l.bm = o;    o += p.E * p.RW;               // per expert: ranks in this rank's instance list
+  l.sendl = o; o += p.R;                      // send counts being summed
+  l.wt = o;    o += 16;                       // per-wave totals of a scan (up to 1024 threads)
   l.repl = o;  o += p.M * imax(p.cap1, 1);    // stage-1 replicas per domain
   l.slots = o; o += p.R * imax(p.Neff, 1);    // replica slots of every rank
   l.used = o;  o += p.R;
@@ -139,7 +142,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   o = (o + 3) & ~3;
   l.misc = o;  o += 64;
   l.om = o;                                   // Omega' [R][E], then list scratch
-  o += imax(p.R * p.E, p.E * p.RW);            // (instance-list rank bitmaps after routing)
+  o += p.R * p.E;
   o = (o + 3) & ~3;
   l.qcol = o;                                 // partial-sum scratch, then q columns
   o += imax(p.M * p.I * p.QS, hist_scratch_words(p));
@@ -708,11 +711,12 @@ __device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uin
 // domain whose refinement cannot move anything (no free slot) only needs
 // q[self] (send counts and this rank's instance list read nothing else, and
 // instance loads feed the refinement only): the chunk holding dom(self)
-// writes that one value; the other sources of the column are left unset.
-template <class SrcOf, class DomOf, class Full>
+// writes that one value, then calls on_self(i, d, e, q); the other sources
+// of the column are left unset.
+template <class SrcOf, class DomOf, class Full, class OnSelf>
 __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, int chunks, const int *e_of,
                                 const uint32_t *mask, const FastDiv *fdt, int *qcol, int *U, SrcOf src_of,
-                                int stride, DomOf dom_of, Full full) {
+                                int stride, DomOf dom_of, Full full, OnSelf on_self) {
   const int tid = threadIdx.x, nt = blockDim.x, G = p.G;
   const int dpc = p.M / chunks;
   const int c_self = (int)fdiv((uint32_t)p.self, p.fG) / dpc;
@@ -723,7 +727,11 @@ __device__ void route_instances(const Plan &p, int NI, FastDiv fNI, int chunks, 
     int *row = qcol + i * p.QS;
     const int d = dom_of(i);
     if (!full(d)) {
-      if (c == c_self) row[p.self] = e < 0 ? 0 : route_self_q(p, d, e, src_of(i, e)[p.self * stride], mask, fdt);
+      if (c == c_self) {
+        const int q = e < 0 ? 0 : route_self_q(p, d, e, src_of(i, e)[p.self * stride], mask, fdt);
+        row[p.self] = q;
+        on_self(i, d, e, q);
+      }
       continue;
     }
     if (e < 0) {
@@ -1219,7 +1227,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     lds_barrier();
     route_instances(
         p, I, p.fI, p.rchunks_dom, e_of, mask, fdt, qcol, U, [&](int i, int) { return qcol + i * p.QS; }, 1,
-        [&](int) { return d; }, [&](int) { return full; });
+        [&](int) { return d; }, [&](int) { return full; }, [](int, int, int, int) {});
     lds_barrier();
     for (int j = tid; j < G; j += nt) {
       int l = 0;
@@ -1320,7 +1328,8 @@ struct SingleState {
   uint64_t *ck, *em;
   FastDiv *fdt;
   int *hs, *ccnt, *dfree, *repl, *slots, *used, *Lr, *e_of, *U, *misc, *om, *qcol;
-  uint32_t *mask;
+  uint32_t *mask, *bm;
+  int *sendl, *wt;
 };
 
 __device__ inline SingleState single_state(const Plan &p, int *sm) {
@@ -1333,6 +1342,9 @@ __device__ inline SingleState single_state(const Plan &p, int *sm) {
   t.ccnt = sm + lay.cnt;
   t.dfree = sm + lay.dfree;
   t.mask = reinterpret_cast<uint32_t *>(sm + lay.mask);
+  t.bm = reinterpret_cast<uint32_t *>(sm + lay.bm);
+  t.sendl = sm + lay.sendl;
+  t.wt = sm + lay.wt;
   t.repl = sm + lay.repl;
   t.slots = sm + lay.slots;
   t.used = sm + lay.used;
@@ -1346,8 +1358,9 @@ __device__ inline SingleState single_state(const Plan &p, int *sm) {
 }
 
 // misc[0] status bits, misc[2] wait flag, misc[8..9] total load, misc[12]
-// refinement moves; candidate counts, hosting-domain masks and local
-// hosting masks zero; stage-1 replica lists empty; the divisor table.
+// refinement moves, misc[14] a domain with a free slot; candidate counts,
+// hosting-domain masks, local hosting masks, instance-list bitmaps and send
+// counts zero; stage-1 replica lists empty; the divisor table.
 __device__ inline void single_init(const Plan &p, const SingleState &t) {
   const int tid = threadIdx.x, nt = blockDim.x;
   if (tid < 16) t.misc[tid] = 0;
@@ -1356,6 +1369,8 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
     t.dfree[d] = 0;
   }
   for (int i = tid; i < p.E * p.MW; i += nt) t.mask[i] = 0;
+  for (int i = tid; i < p.E * p.RW; i += nt) t.bm[i] = 0;
+  for (int i = tid; i < p.R; i += nt) t.sendl[i] = 0;
   for (int i = tid; i < p.M * p.cap1; i += nt) t.repl[i] = -1;
   for (int i = tid; i < p.M * p.E; i += nt) t.em[i] = 0;
   build_divisors(p.M, t.fdt);
@@ -1451,61 +1466,60 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
         const int u = ns > j ? (int)fdiv((uint32_t)(ns - j + G - 1), p.fG) : 0;
         used[r] = u;
         for (int t = 0; t < Neff; ++t) slots[r * Neff + t] = t < u ? repl[d * cap + t * G + j] : -1;
-        if (u < Neff) dfree[d] = 1;
+        if (u < Neff) {
+          dfree[d] = 1;
+          misc[14] = 1;
+        }
       }
     }
   }
   lds_barrier();
 
-  // ---- routing construction (Section 4.3) for every domain's instances
+  // ---- routing construction (Section 4.3) for every domain's instances;
+  // instances of domains that cannot refine enter this rank's instance-list
+  // bitmaps and send counts at once
+  uint32_t *bm = t.bm;
+  int *sendl = t.sendl;
+  auto mark = [&](int i, int d, int e, int q) {
+    if (q > 0) {
+      const int r = d * G + (int)fdiv((uint32_t)(i - d * I), p.fPN);
+      atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
+      atomicAdd(&sendl[r], q);
+    }
+  };
   route_instances(
       p, M * I, p.fMI, p.rchunks_all, e_of, mask, fdt, qcol, U, [&](int, int e) { return om + e; }, E,
-      [&](int i) { return (int)fdiv((uint32_t)i, p.fI); }, [&](int d) { return dfree[d] != 0; });
+      [&](int i) { return (int)fdiv((uint32_t)i, p.fI); }, [&](int d) { return dfree[d] != 0; }, mark);
   lds_barrier();
 
-  // ---- intra-node refinement (Eq. 10): one wave per domain (it sums its
-  // ranks' loads first); Omega is dead, so its LDS takes the rank bitmaps
-  // of the instance list, cleared meanwhile by the other waves
-  uint32_t *bm = reinterpret_cast<uint32_t *>(om);
-  uint32_t flags = 0, moves = 0;
-  for (int d = wave; d < M; d += nw)
-    moves += refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
-                           used + d * G, Lr + d * G, em + (int64_t)d * E, &flags, true);
-  if (lane_id() == 0) {
-    if (flags) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
-    if (moves) atomicAdd(reinterpret_cast<unsigned *>(&misc[12]), moves);
-  }
-  for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
-  lds_barrier();
-
-  // ---- outputs; ranks holding an instance of e with a share of this
-  // rank's assignments, as one bitmap per expert
-  {
-    const int n1 = M * I, n2 = n1 + R, n3 = n2 + R * p.N;
-    for (int v = tid; v < n3; v += nt) {
-      if (v < n1) {
-        const int idx = v;
-        const int e = e_of[idx];
-        if (e >= 0 && qcol[idx * p.QS + p.self] > 0) {
-          const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
-          const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
-          atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
-        }
-      } else if (v < n2) {
-        const int r = v - n1;
-        const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
-        int sc = 0;
-        for (int pos = 0; pos < PN; ++pos) sc += qcol[(d * I + j * PN + pos) * p.QS + p.self];
-        p.send_out[r] = sc;
-      } else {
-        const int i = v - n2;
-        const int r = (int)fdiv((uint32_t)i, p.fN), t = i - r * p.N;
-        p.slots_out[i] = t < used[r] ? slots[r * Neff + t] : -1;
-      }
+  if (misc[14]) {
+    // ---- intra-node refinement (Eq. 10): one wave per domain (it sums its
+    // ranks' loads first; a domain without a free slot returns at once)
+    uint32_t flags = 0, moves = 0;
+    for (int d = wave; d < M; d += nw)
+      moves += refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
+                             used + d * G, Lr + d * G, em + (int64_t)d * E, &flags, true);
+    if (lane_id() == 0) {
+      if (flags) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
+      if (moves) atomicAdd(reinterpret_cast<unsigned *>(&misc[12]), moves);
     }
+    lds_barrier();
+    // ---- the refined domains' instances enter the bitmaps and send counts
+    for (int idx = tid; idx < M * I; idx += nt) {
+      const int d = (int)fdiv((uint32_t)idx, p.fI);
+      const int e = e_of[idx];
+      if (dfree[d] && e >= 0) mark(idx, d, e, qcol[idx * p.QS + p.self]);
+    }
+    lds_barrier();
   }
-  lds_barrier();
-  emit_instance_list(p, qcol, slots, used, bm, reinterpret_cast<int *>(ck));
+
+  // ---- outputs: replica slots, send counts, this rank's instance list
+  for (int i = tid; i < R * p.N; i += nt) {
+    const int r = (int)fdiv((uint32_t)i, p.fN), t2 = i - r * p.N;
+    p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
+  }
+  for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
+  emit_instance_list(p, qcol, slots, used, bm, t.wt);
   if (tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;

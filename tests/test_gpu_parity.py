@@ -407,3 +407,14 @@ def test_launch_floor_writes_nothing(solver):
     torch.cuda.synchronize()
     for t in (p.token_dest, p.send_counts, p.replica_slots, p.status):
         assert bool((t == -9).all())
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("N", [0, 1, 3])
+def test_single_rank_single_expert(solver, N):
+    """R = G = E = 1: one rank, one expert, no replica possible (the
+    solver's scratch must still fit every wave's share)."""
+    rng = np.random.default_rng(N)
+    tk = np.zeros((int(rng.integers(1, 40)), 1), np.int32)
+    gl = np.array([[tk.shape[0]]], np.int32)
+    both(1, 1, 1, 0, 0, 6, 2, 25, N, gl, tk, launch=SOLVERS[solver], what="R=G=E=1 N=%d %s" % (N, solver))
