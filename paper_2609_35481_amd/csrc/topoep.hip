@@ -51,7 +51,10 @@ constexpr int kCtrlStatus = 2;   // status bits accumulated during the plan
 constexpr int kCtrlFinal = 3;    // final status of the plan (read by reroute)
 constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
 constexpr int kCtrlMoves = 6;    // refinement moves of the per-domain solver
-constexpr int kCtrlArrive = 8;   // one-launch plan: chunks whose counts are written
+constexpr int kCtrlArrive = 8;   // one-launch plan: chunks whose counts are written (+1 by the last)
+constexpr int kCtrlVerdict = 9;  // one-launch plan: the last chunk's histogram check (kVerdict*)
+constexpr uint32_t kVerdictSame = 1;   // histogram == row self of Omega, no bad id; counts cleared
+constexpr uint32_t kVerdictRedo = 2;   // otherwise; the counts stay for the solver
 
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
@@ -1002,6 +1005,41 @@ __device__ inline void rank_candidates(int c, int nc, int cap, const uint64_t *k
   if (rank < cap) out[rank] = (int)(uint32_t)kc;
 }
 
+// Stage 1 (Eq. 9) candidates of domain d, by one wave: the experts whose
+// main is outside d with benefit b = 2 D S - W > 0 (D from om, Omega with
+// row self already the histogram when dom(self) = d), compacted with ballots
+// into keys ck_d; returns their count on every lane.
+__device__ int stage1_candidates_wave(const Plan &p, int d, const int *om, uint64_t *ck_d) {
+  const int lane = lane_id(), E = p.E, G = p.G;
+  int nc = 0;
+  for (int e0 = 0; e0 < E; e0 += 64) {
+    const int e = e0 + lane;
+    bool cand = false;
+    uint64_t key = 0;
+    if (e < E && (int)fdiv((uint32_t)e, p.fGP) != d) {
+      int D = 0;
+#pragma unroll 8
+      for (int j = 0; j < G; ++j) D += om[(d * G + j) * E + e];
+      cand = (int64_t)2 * D * p.S > p.W;
+      key = cand_key(D, e);
+    }
+    const uint64_t m = __ballot(cand);
+    if (cand) ck_d[nc + __popcll(m & lanemask_lt())] = key;
+    nc += __popcll(m);
+  }
+  wave_sync();
+  return nc;
+}
+
+// Stage 1 of domain d by one wave: candidates, then each ranked by key; the
+// first cap ranks fill repl_d (pre-filled with -1) and ccnt[d] = the count.
+__device__ void stage1_domain_wave(const Plan &p, int d, const int *om, uint64_t *ck_d, int *ccnt, int *repl_d) {
+  const int nc = stage1_candidates_wave(p, d, om, ck_d);
+  for (int c = lane_id(); c < nc; c += 64) rank_candidates(c, nc, p.cap1, ck_d, repl_d);
+  if (lane_id() == 0) ccnt[d] = nc;
+}
+
+
 // This rank's per-expert instance list: bm[e * RW ...] marks the ranks
 // whose instance of e has a nonzero share q[self][e][r].  Thread t takes
 // experts [t * K, (t + 1) * K), K = ceil(E / blockDim): it counts their
@@ -1381,7 +1419,8 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 // Eq. 10 refinement) and writes replica_slots, send_counts, this rank's
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
-__device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
+__device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
+                            bool write_status = true) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
   int *hs = t.hs, *ccnt = t.ccnt, *dfree = t.dfree, *repl = t.repl, *slots = t.slots, *used = t.used;
@@ -1404,24 +1443,8 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   }
   lds_barrier();
 
-  // ---- inter-node placement (Eq. 9), every domain at once
-  for (int idx = tid; idx < M * E; idx += nt) {
-    const int d = (int)fdiv((uint32_t)idx, p.fE), e = idx - d * E;
-    if ((int)fdiv((uint32_t)e, p.fGP) == d) continue;   // main inside the domain
-    int D = 0;
-#pragma unroll 8
-    for (int j = 0; j < G; ++j) D += om[(d * G + j) * E + e];
-    if ((int64_t)2 * D * p.S > p.W) {
-      const int pos = atomicAdd(&ccnt[d], 1);
-      ck[d * E + pos] = cand_key(D, e);
-    }
-  }
-  lds_barrier();
-  for (int idx = tid; idx < M * E; idx += nt) {
-    const int d = (int)fdiv((uint32_t)idx, p.fE), c = idx - d * E;
-    const int nc = ccnt[d];
-    if (c < nc) rank_candidates(c, nc, cap, ck + d * E, repl + d * cap);
-  }
+  // ---- inter-node placement (Eq. 9): one wave per domain
+  for (int d = wave; d < M; d += nw) stage1_domain_wave(p, d, om, ck + (int64_t)d * E, ccnt, repl + d * cap);
   lds_barrier();
 
   // ---- hosting domains per expert; every rank's slots and instances, and
@@ -1520,7 +1543,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   }
   for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
   emit_instance_list(p, qcol, slots, used, bm, t.wt);
-  if (tid == 0) {
+  if (write_status && tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;
     if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
@@ -1730,9 +1753,11 @@ __device__ void collect_counts(const Plan &p, int *hs, int *misc) {
   __syncthreads();
 }
 
-// Solver role (workgroup 0): Omega goes to LDS while the chunks count; the
-// histogram and chunk offsets come from the published counts; the plan
-// proceeds as in the single-workgroup solver; then every chunk's flag.
+// Solver role (workgroup 0): Omega goes to LDS and the whole plan is made
+// from it while the chunks count; once the last chunk has compared the
+// histogram with row self of Omega, that plan stands (equal rows, so Omega'
+// = Omega) or is made again from Omega' on fresh state; then every chunk's
+// flag 2.
 __device__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
@@ -1740,12 +1765,23 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   single_init(p, t);
   lds_barrier();
   load_omega(p, t.om, t.misc);
-  // wait until every chunk has written its counts
+  lds_barrier();
+  const uint64_t total0 = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
+  const uint32_t neg0 = (uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD;
+  const uint32_t gst0 = neg0 | (out_of_range(p, total0) ? TOPOEP_ST_RANGE : 0u);
+  // Speculative plan from Omega as gathered while the chunks count: it is
+  // the plan whenever the histogram equals row self (the gathered row is
+  // this rank's own count), else it is redone below; nothing reads the
+  // outputs before the flags say the plan is ready.
+  const bool spec = !(gst0 & kNoPlan);
+  if (spec) single_plan(p, t, gst0, true, false);
+  // wait until every chunk has written its counts and the last one has
+  // checked the histogram
   if (tid == 0) {
     uint32_t it = 0;
     int ok = 1;
     while (__hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-           (uint32_t)p.nb) {
+           (uint32_t)p.nb + 1u) {
       if (++it > p.spin_limit) {
         ok = 0;
         break;
@@ -1753,20 +1789,37 @@ __device__ void fused_solver(const Plan &p, int *sm) {
       __builtin_amdgcn_s_sleep(1);
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if (ok) __hip_atomic_store(&p.ctrl[kCtrlArrive], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t v = 0;
+    if (ok) {
+      v = p.ctrl[kCtrlVerdict];
+      __hip_atomic_store(&p.ctrl[kCtrlArrive], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&p.ctrl[kCtrlVerdict], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     t.misc[2] = ok;
+    t.misc[3] = (int)v;
   }
   __syncthreads();
   const bool synced = t.misc[2] != 0;
-  // flag 1: every chunk's counts are written; the chunks sum their offsets
-  // while this workgroup plans (a release, so the chunks' own releases reach
-  // the readers through this workgroup's acquire)
-  if (tid < 64)
-    for (int b = tid; b < p.nb; b += 64)
-      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  if (synced) collect_counts(p, t.hs, t.misc);
-  uint32_t gst = 0;
-  if (synced) {
+  const uint32_t verdict = (uint32_t)t.misc[3];
+  const bool stands = synced && verdict == kVerdictSame && spec;
+  // a rewrite of the speculative outputs is ordered after their stores
+  if (spec && !stands) drain_then_barrier();
+  if (stands) {
+    // the speculative plan stands (Omega' = Omega): its status
+    if (tid == 0) {
+      const uint32_t fin = (uint32_t)t.misc[0];
+      p.ctrl[kCtrlFinal] = fin;
+      atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
+      p.status_out[1] = t.misc[12];
+    }
+  } else if (synced && verdict == kVerdictSame) {
+    single_plan(p, t, gst0, true);   // Omega itself refused: blank outputs
+  } else if (synced) {
+    // row self differs from the histogram, or a bad id: plan again from
+    // Omega' (row self = the histogram) on fresh state
+    single_init(p, t);
+    lds_barrier();
+    collect_counts(p, t.hs, t.misc);
     bool diff = false;
     int64_t adj = 0;
     for (int e = tid; e < E; e += nt) {
@@ -1778,21 +1831,46 @@ __device__ void fused_solver(const Plan &p, int *sm) {
     adj = (int64_t)wave_sum_u64((uint64_t)adj);
     const uint64_t any_diff = __ballot(diff);
     if (lane_id() == 0) {
-      if (any_diff) atomicOr(reinterpret_cast<unsigned *>(&t.misc[0]), TOPOEP_ST_SELF_DIFF);
+      atomicOr(reinterpret_cast<unsigned *>(&t.misc[0]), (any_diff ? TOPOEP_ST_SELF_DIFF : 0u) | neg0);
       if (adj) atomicAdd(reinterpret_cast<unsigned long long *>(t.misc + 8), (unsigned long long)adj);
     }
     lds_barrier();
-    gst = (uint32_t)t.misc[0];
-    if (out_of_range(p, *reinterpret_cast<unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
+    uint32_t gst = (uint32_t)t.misc[0];
+    if (out_of_range(p, total0 + *reinterpret_cast<const unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
+    single_plan(p, t, gst, true);
   } else {
-    gst = TOPOEP_ST_SYNC;
+    single_plan(p, t, TOPOEP_ST_SYNC, true);
   }
-  single_plan(p, t, gst, true);
-  // release: every output, the instance list and the offsets before the flags
+  // release: every output, the instance list and the final status before
+  // the flags
   drain_then_barrier();
   if (tid < 64)
     for (int b = tid; b < p.nb; b += 64)
       __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The last chunk to arrive (every count is written): flag 1 of every chunk,
+// so they sum their offsets; then the histogram (the summed counts) against
+// row self of Omega and the bad-id word, the verdict in its control word
+// (the counts cleared for the next plan unless the solver needs them), and
+// the arrival counter one past nb.
+__device__ void last_arrival(const Plan &p) {
+  const int tid = threadIdx.x, E = p.E;
+  if (tid < 64)
+    for (int c = tid; c < p.nb; c += 64)
+      __hip_atomic_store(p.flags + (int64_t)c * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  bool diff = false;
+  for (int e = tid; e <= E; e += blockDim.x) {
+    const uint32_t v = p.ghist[e];
+    diff |= e < E ? (int)v != p.gl[(int64_t)p.self * E + e] : v != 0u;
+  }
+  const bool redo = __syncthreads_or(diff) != 0;
+  if (!redo)
+    for (int e = tid; e <= E; e += blockDim.x)
+      __hip_atomic_store(p.ghist + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) p.ctrl[kCtrlVerdict] = redo ? kVerdictRedo : kVerdictSame;
+  drain_then_barrier();
+  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Bounded wait of chunk b's workgroup until its flag reaches `level`; after
@@ -1822,7 +1900,8 @@ __device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
 
 // Chunk role (workgroup 1 + b): ids [b * chunk, (b + 1) * chunk) stay in
 // registers for the whole plan.  Each wave ranks its ids among equal ids
-// (row-major order) and the workgroup writes its counts and arrives; once
+// (row-major order) and the workgroup writes its counts and arrives (the
+// last to arrive sets every chunk's flag 1 and checks the histogram); once
 // every chunk has, it sums the counts of the chunks before it; after the
 // plan is ready each id's occurrence index rho = (offset of the chunk) +
 // (offset of the wave in the chunk) + (rank in the wave) picks the
@@ -1875,7 +1954,16 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
   }
   if (tid == 0 && bad) atomicOr(p.ghist + E, 1u);
   drain_then_barrier();
-  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) {
+    const uint32_t before =
+        __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before + 1u == (uint32_t)p.nb;
+    // the last arrival acquires every other chunk's counts
+    if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    flag[1] = last;
+  }
+  __syncthreads();
+  if (flag[1]) last_arrival(p);
   // flag >= 1: every chunk's counts are written; this chunk's first
   // occurrence index of e is the sum of the counts of chunks 0 .. b-1
   bool ok = wait_flag(p, b, 1u, flag);

@@ -251,6 +251,51 @@ def test_negative_load_and_mismatch():
     assert got["status"] == topoep.ST_SELF_DIFF
 
 
+def _self_row_cases():
+    """Omega's row self against the histogram of local_topk (self = 2 of the
+    tiny configuration): the one-launch plan is first made from Omega as
+    gathered and kept only when that row equals the histogram."""
+    cfg, gl, tk = _tiny()
+    s = 2
+    tk = tk.copy()
+    hist = np.bincount(tk.ravel(), minlength=cfg.E).astype(np.int64)
+    gl = gl.copy()
+    gl[s] = hist
+    out = [("equal rows", gl, tk)]
+    g = gl.copy()
+    g[s] = np.roll(hist, 5) * 3        # a different demand: a different plan
+    out.append(("row self differs", g, tk))
+    g = gl.copy()
+    g[s, 0] = 2**31 - 1                # Omega out of range, Omega' in range
+    out.append(("range only before", g, tk))
+    g = gl.copy()
+    g[s] = 0
+    rest = int(g.astype(np.int64).sum())
+    g[(s + 1) % cfg.R, 0] += 2**31 - 1 - rest - int(hist.sum()) + 1   # Omega' just out of range
+    out.append(("range only after", g, tk))
+    g = gl.copy()
+    g[s, 3] = -1                       # a negative load in row self only
+    out.append(("negative in row self", g, tk))
+    g = gl.copy()
+    g[(s + 3) % cfg.R, 1] = -4         # refused Omega, equal rows
+    out.append(("negative elsewhere", g, tk))
+    t2 = tk.copy()
+    t2[7, 1] = cfg.E + 2               # a bad id; the valid ids' histogram is row self
+    g = gl.copy()
+    g[s] = np.bincount(t2[(t2 >= 0) & (t2 < cfg.E)], minlength=cfg.E)
+    out.append(("bad id", g, t2))
+    return cfg, s, out
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+def test_self_row_against_histogram(solver):
+    cfg, s, cases = _self_row_cases()
+    for what, g, t in cases:
+        assert int(g.max()) < 2**31 and int(g.min()) >= -2**31
+        both(cfg.R, cfg.G, cfg.E, s, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W, cfg.N,
+             g.astype(np.int32), t, launch=SOLVERS[solver], what="%s (%s)" % (what, solver))
+
+
 def test_range_bit():
     cfg, gl, tk = _tiny()
     got, _ = both(cfg.R, cfg.G, cfg.E, 0, 1, 1 << 10, 1 << 50, cfg.W, 1, gl, tk, what="range S")
