@@ -51,10 +51,13 @@ constexpr int kCtrlStatus = 2;   // status bits accumulated during the plan
 constexpr int kCtrlFinal = 3;    // final status of the plan (read by reroute)
 constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
 constexpr int kCtrlMoves = 6;    // refinement moves of the per-domain solver
-constexpr int kCtrlArrive = 8;   // one-launch plan: chunks whose counts are written (+1 by the last)
-constexpr int kCtrlVerdict = 9;  // one-launch plan: the last chunk's histogram check (kVerdict*)
-constexpr uint32_t kVerdictSame = 1;   // histogram == row self of Omega, no bad id; counts cleared
-constexpr uint32_t kVerdictRedo = 2;   // otherwise; the counts stay for the solver
+// one-launch plan: chunks whose counts are written, then the last chunk's
+// verdict on top: nb + kVerdictSame when the histogram equals row self of
+// Omega and no id is bad (the counts are cleared), nb + kVerdictRedo
+// otherwise (the counts stay for the solver)
+constexpr int kCtrlArrive = 8;
+constexpr uint32_t kVerdictSame = 1;
+constexpr uint32_t kVerdictRedo = 2;
 
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
@@ -1420,7 +1423,7 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
 __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
-                            bool write_status = true) {
+                            bool write_status = true, bool read_arrival = false) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
   int *hs = t.hs, *ccnt = t.ccnt, *dfree = t.dfree, *repl = t.repl, *slots = t.slots, *used = t.used;
@@ -1542,7 +1545,13 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
     p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
   }
   for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
+  // (one-launch plan: the arrival word read here is in by the end of the
+  // instance list, so its wait costs no round trip once the chunks are done)
+  uint32_t arrival = 0;
+  if (read_arrival && tid == 0)
+    arrival = __hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   emit_instance_list(p, qcol, slots, used, bm, t.wt);
+  if (read_arrival && tid == 0) misc[6] = (int)arrival;
   if (write_status && tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;
@@ -1697,8 +1706,11 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 // and leaves that state undefined (the workspace is zero-filled again).
 
 // Omega to LDS with its status bits and total load (row self included as
-// gathered; the caller swaps in the histogram later).
-__device__ void load_omega(const Plan &p, int *om, int *misc) {
+// gathered; the caller swaps in the histogram later).  `between` runs on
+// every thread once the first loads are issued (LDS set-up that overlaps
+// their latency); the status words are written after a barrier behind it.
+template <typename Between>
+__device__ void load_omega(const Plan &p, int *om, int *misc, Between between) {
   const int tid = threadIdx.x, nt = blockDim.x, n = p.R * p.E;
   bool neg = false;
   uint64_t tot = 0;
@@ -1706,10 +1718,15 @@ __device__ void load_omega(const Plan &p, int *om, int *misc) {
     const int n4 = n >> 2;
     const int4 *g4 = reinterpret_cast<const int4 *>(p.gl);
     int4 *o4 = reinterpret_cast<int4 *>(om);
-    for (int i = tid; i < n4; i += 4 * nt) {
-      int4 v[4];
+    int4 v[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = g4[imin(i + u * nt, n4 - 1)];
+    for (int u = 0; u < 4; ++u) v[u] = g4[imin(tid + u * nt, n4 - 1)];
+    between();
+    for (int i = tid; i < n4; i += 4 * nt) {
+      if (i != tid) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = g4[imin(i + u * nt, n4 - 1)];
+      }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         if (i + u * nt < n4) {
@@ -1721,6 +1738,7 @@ __device__ void load_omega(const Plan &p, int *om, int *misc) {
       }
     }
   } else {
+    between();
     for (int i = tid; i < n; i += nt) {
       const int g = p.gl[i];
       om[i] = g;
@@ -1730,6 +1748,7 @@ __device__ void load_omega(const Plan &p, int *om, int *misc) {
   }
   tot = wave_sum_u64(tot);
   const uint64_t any_neg = __ballot(neg);
+  lds_barrier();
   if (lane_id() == 0) {
     if (any_neg) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_NEG_LOAD);
     if (tot) atomicAdd(reinterpret_cast<unsigned long long *>(misc + 8), (unsigned long long)tot);
@@ -1762,9 +1781,7 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
   if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
-  single_init(p, t);
-  lds_barrier();
-  load_omega(p, t.om, t.misc);
+  load_omega(p, t.om, t.misc, [&] { single_init(p, t); });
   lds_barrier();
   const uint64_t total0 = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
   const uint32_t neg0 = (uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD;
@@ -1774,26 +1791,26 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   // this rank's own count), else it is redone below; nothing reads the
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
-  if (spec) single_plan(p, t, gst0, true, false);
+  if (spec) single_plan(p, t, gst0, true, false, true);
   // wait until every chunk has written its counts and the last one has
-  // checked the histogram
+  // added its verdict
   if (tid == 0) {
-    uint32_t it = 0;
+    const uint32_t nb = (uint32_t)p.nb;
+    uint32_t v = spec ? (uint32_t)t.misc[6] : 0u, it = 0;
     int ok = 1;
-    while (__hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
-           (uint32_t)p.nb + 1u) {
+    while (v <= nb) {
       if (++it > p.spin_limit) {
         ok = 0;
         break;
       }
       __builtin_amdgcn_s_sleep(1);
+      v = __hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    uint32_t v = 0;
     if (ok) {
-      v = p.ctrl[kCtrlVerdict];
+      v -= nb;
+      // the counts are read only when the plan is redone
+      if (v != kVerdictSame) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       __hip_atomic_store(&p.ctrl[kCtrlArrive], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&p.ctrl[kCtrlVerdict], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     t.misc[2] = ok;
     t.misc[3] = (int)v;
@@ -1851,9 +1868,9 @@ __device__ void fused_solver(const Plan &p, int *sm) {
 
 // The last chunk to arrive (every count is written): flag 1 of every chunk,
 // so they sum their offsets; then the histogram (the summed counts) against
-// row self of Omega and the bad-id word, the verdict in its control word
-// (the counts cleared for the next plan unless the solver needs them), and
-// the arrival counter one past nb.
+// row self of Omega and the bad-id word, and the verdict added to the
+// arrival word (the counts cleared for the next plan unless the solver
+// needs them).
 __device__ void last_arrival(const Plan &p) {
   const int tid = threadIdx.x, E = p.E;
   if (tid < 64)
@@ -1868,9 +1885,10 @@ __device__ void last_arrival(const Plan &p) {
   if (!redo)
     for (int e = tid; e <= E; e += blockDim.x)
       __hip_atomic_store(p.ghist + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (tid == 0) p.ctrl[kCtrlVerdict] = redo ? kVerdictRedo : kVerdictSame;
   drain_then_barrier();
-  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0)
+    __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], redo ? kVerdictRedo : kVerdictSame, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Bounded wait of chunk b's workgroup until its flag reaches `level`; after
