@@ -64,6 +64,12 @@ def load_library(path: str):
     lib.topoep_plan_ref.argtypes = [ctypes.POINTER(RefTopology), _P32, _P32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_int32, _P32, _P32, _P32, _P32,
                                     ctypes.POINTER(RefDebug)]
+    lib.topoep_plan_ref_ex.restype = ctypes.c_int
+    lib.topoep_plan_ref_ex.argtypes = [ctypes.POINTER(RefTopology), _P32, _P32, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_int32, _P32, _P32, _P32, _P32, _P32,
+                                       ctypes.POINTER(RefDebug)]
+    lib.topoep_layout_ref.restype = ctypes.c_int
+    lib.topoep_layout_ref.argtypes = [ctypes.c_int32, _P32, ctypes.c_int64, _P32, _P32, _P32]
     _lib = lib
     return lib
 
@@ -88,9 +94,11 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
              debug: bool = False, move_cap: int = 0, raw_rc: bool = False):
     """Run the oracle.  Returns a dict of numpy arrays.
 
-    Keys: replica_slots [R, N], token_dest [T, k], send_counts [R], status
-    (the bits), move_count (refinement moves committed), and with ``debug``: hist, demand, x_stage1, q_routed, load_routed,
-    x_final, q_final, load_final, iters, moves, move_dcost, move_m, n_moves.
+    Keys: replica_slots [R, N], token_dest [T, k], send_counts [R],
+    recv_counts [R] (what each rank sends to this one under the same plan),
+    status (the bits), move_count (refinement moves committed), and with
+    ``debug``: hist, demand, x_stage1, q_routed, load_routed, x_final,
+    q_final, load_final, iters, moves, move_dcost, move_m, n_moves.
     """
     lib = _load()
     gl = np.ascontiguousarray(global_load, dtype=np.int32)
@@ -103,6 +111,7 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
     slots = np.full((R, max(N, 0)), -7, dtype=np.int32)
     dest = np.full((T, k), -7, dtype=np.int32)
     sc = np.full(R, -7, dtype=np.int32)
+    rcv = np.full(R, -7, dtype=np.int32)
     st = np.zeros(2, dtype=np.int32)
     out = {}
     dbgp = None
@@ -125,13 +134,15 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
                        int(move_cap), _ptr(out["moves"]), _ptr(out["move_dcost"], _P64),
                        _ptr(out["move_m"]), 0)
         dbgp = ctypes.byref(dbg)
-    rc = lib.topoep_plan_ref(ctypes.byref(topo), _ptr(gl), _ptr(tk) if T > 0 else None, T, k, N,
-                             _ptr(slots), _ptr(dest) if T > 0 else None, _ptr(sc), _ptr(st), dbgp)
+    rc = lib.topoep_plan_ref_ex(ctypes.byref(topo), _ptr(gl), _ptr(tk) if T > 0 else None, T, k, N,
+                                _ptr(slots), _ptr(dest) if T > 0 else None, _ptr(sc), _ptr(rcv),
+                                _ptr(st), dbgp)
     if raw_rc:
         return rc
     if rc != 0:
         raise ValueError("topoep_plan_ref returned %d" % rc)
-    out.update(replica_slots=slots, token_dest=dest, send_counts=sc, status=int(st[0]), move_count=int(st[1]))
+    out.update(replica_slots=slots, token_dest=dest, send_counts=sc, recv_counts=rcv, status=int(st[0]),
+               move_count=int(st[1]))
     if debug:
         out["n_moves"] = dbg.n_moves
         nm = min(dbg.n_moves, move_cap)
@@ -139,6 +150,21 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
         out["move_dcost"] = out["move_dcost"][:nm]
         out["move_m"] = out["move_m"][:nm]
     return out
+
+
+def layout_ref(R: int, token_dest, send_counts):
+    """Dispatch layout of a plan's destinations: (send_offsets [R + 1],
+    token_slot with token_dest's shape)."""
+    lib = _load()
+    td = np.ascontiguousarray(token_dest, dtype=np.int32)
+    sc = np.ascontiguousarray(send_counts, dtype=np.int32)
+    offs = np.full(R + 1, -7, dtype=np.int32)
+    slot = np.full(td.shape, -7, dtype=np.int32)
+    rc = lib.topoep_layout_ref(int(R), _ptr(td) if td.size else None, int(td.size), _ptr(sc), _ptr(offs),
+                               _ptr(slot) if td.size else None)
+    if rc != 0:
+        raise ValueError("topoep_layout_ref returned %d" % rc)
+    return offs, slot
 
 
 def plan_cfg(cfg, global_load, local_topk, self_rank: int = 0, **kw):

@@ -97,6 +97,15 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
                     int32_t replica_budget, int32_t *replica_slots,
                     int32_t *token_dest, int32_t *send_counts,
                     int32_t *status, ref_debug *dbg) {
+  return topoep_plan_ref_ex(topo, global_load, local_topk, T, k, replica_budget, replica_slots,
+                            token_dest, send_counts, NULL, status, dbg);
+}
+
+int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
+                       const int32_t *local_topk, int32_t T, int32_t k,
+                       int32_t replica_budget, int32_t *replica_slots,
+                       int32_t *token_dest, int32_t *send_counts,
+                       int32_t *recv_counts, int32_t *status, ref_debug *dbg) {
   if (!topo || !global_load || !replica_slots || !send_counts || !status) return REF_EINVAL;
   if (T < 0 || k < 1 || replica_budget < 0) return REF_EINVAL;
   if (T > 0 && (!local_topk || !token_dest)) return REF_EINVAL;
@@ -180,6 +189,8 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
   if (st & (REF_ST_BAD_ID | REF_ST_NEG_LOAD | REF_ST_RANGE)) {
     for (int i = 0; i < R * N; ++i) replica_slots[i] = -1;
     for (int r = 0; r < R; ++r) send_counts[r] = 0;
+    if (recv_counts)
+      for (int r = 0; r < R; ++r) recv_counts[r] = 0;
     for (int64_t i = 0; i < n_assign; ++i) token_dest[i] = -1;
     status[0] = (int32_t)st;
     status[1] = 0;
@@ -358,6 +369,15 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
     for (int e = 0; e < E; ++e) sc += Q(m.self, e, r);
     send_counts[r] = (int32_t)sc;
   }
+  /* Receive counts: every rank makes the same plan, so what source s sends
+   * to this rank is its share q[s][e][self] summed over the experts (the
+   * count the dispatch of Section 4.3 needs on the receiving side). */
+  if (recv_counts)
+    for (int s2 = 0; s2 < R; ++s2) {
+      int64_t rc = 0;
+      for (int e = 0; e < E; ++e) rc += Q(s2, e, m.self);
+      recv_counts[s2] = (int32_t)rc;
+    }
   for (int64_t i = 0; i < n_assign; ++i) {
     int e = local_topk[i];
     int64_t rho = seen[e]++;
@@ -381,5 +401,36 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
 #undef UU
   free(hist); free(omega); free(D); free(x); free(used); free(slots); free(q); free(U); free(L);
   free(mv); free(best_mv); free(order); free(cand); free(inst); free(seen);
+  return REF_OK;
+}
+
+/* Dispatch layout: the send buffer holds the assignments grouped by
+ * destination rank, ranks ascending, and inside one destination in
+ * row-major (token, k) order.  send_offsets[r] = sum of send_counts[r'] for
+ * r' < r (R + 1 entries); token_slot[i] = send_offsets[dest] + the number of
+ * earlier assignments with the same destination, -1 when token_dest[i] is
+ * not a rank. */
+int topoep_layout_ref(int32_t R, const int32_t *token_dest, int64_t n, const int32_t *send_counts,
+                      int32_t *send_offsets, int32_t *token_slot) {
+  if (R <= 0 || n < 0 || !send_counts || !send_offsets || (n > 0 && (!token_dest || !token_slot)))
+    return REF_EINVAL;
+  int64_t acc = 0;
+  for (int r = 0; r < R; ++r) {
+    send_offsets[r] = (int32_t)acc;
+    acc += send_counts[r];
+  }
+  send_offsets[R] = (int32_t)acc;
+  int64_t *seen = calloc((size_t)R, sizeof(int64_t));
+  if (!seen) return REF_ENOMEM;
+  for (int64_t i = 0; i < n; ++i) {
+    const int d = token_dest[i];
+    if (d < 0 || d >= R) {
+      token_slot[i] = -1;
+      continue;
+    }
+    token_slot[i] = (int32_t)(send_offsets[d] + seen[d]);
+    seen[d]++;
+  }
+  free(seen);
   return REF_OK;
 }

@@ -81,6 +81,22 @@ int topoep_plan_ref(const ref_topology *topo, const int32_t *global_load,
                     int32_t *token_dest, int32_t *send_counts,
                     int32_t *status, ref_debug *dbg);
 
+/* The same plan plus recv_counts[R] (may be NULL): recv_counts[s] = sum over
+ * e of q[s][e][self], what rank s sends to this rank under the replicated
+ * plan (0 when no plan is made). */
+int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
+                       const int32_t *local_topk, int32_t T, int32_t k,
+                       int32_t replica_budget, int32_t *replica_slots,
+                       int32_t *token_dest, int32_t *send_counts,
+                       int32_t *recv_counts, int32_t *status, ref_debug *dbg);
+
+/* Dispatch layout of the rerouted assignments: send_offsets[R + 1] is the
+ * exclusive prefix of send_counts; token_slot[n] = send_offsets[dest] + the
+ * number of earlier assignments (row-major) with the same destination, or
+ * -1 when token_dest is not a rank. */
+int topoep_layout_ref(int32_t R, const int32_t *token_dest, int64_t n, const int32_t *send_counts,
+                      int32_t *send_offsets, int32_t *token_slot);
+
 #ifdef __cplusplus
 }
 #endif

@@ -281,3 +281,71 @@ def test_balanced_static_plan_is_kept(seed):
     assert (out["replica_slots"] == -1).all()
     assert out["n_moves"] == 0
     assert objective(t, out["x_final"], out["q_final"]) == 0
+
+
+# ---------------------------------------------------------------- dispatch layout
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_receive_counts_match_every_senders_plan(seed):
+    """Every rank makes the same plan, so what rank r expects from rank s
+    (its receive count) is what rank s's own plan sends to r; the counts a
+    rank receives add up to its final load."""
+    t, omega, topks = random_instance(5000 + seed, big=True)
+    outs = [run(t, omega, topks[s], s, debug=True) for s in range(t.R)]
+    for r in range(t.R):
+        assert outs[r]["status"] == 0
+        for s in range(t.R):
+            assert outs[r]["recv_counts"][s] == outs[s]["send_counts"][r], (r, s)
+        assert outs[r]["recv_counts"].sum() == outs[r]["load_final"][r]
+
+
+def _layout_by_sort(R, dest, send_counts):
+    """The send buffer by a stable argsort on the destination: position of
+    each assignment in that order, -1 for a non-rank destination."""
+    d = dest.ravel().astype(np.int64)
+    ok = (d >= 0) & (d < R)
+    key = np.where(ok, d, R)              # invalid ones sort last
+    order = np.argsort(key, kind="stable")
+    slot = np.empty(d.size, np.int64)
+    slot[order] = np.arange(d.size)
+    slot[~ok] = -1
+    offs = np.concatenate([[0], np.cumsum(np.bincount(d[ok], minlength=R))])
+    return offs, slot.reshape(dest.shape)
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_dispatch_layout_is_the_stable_sort_by_destination(seed):
+    t, omega, topks = random_instance(6000 + seed, big=True)
+    s = seed % t.R
+    out = run(t, omega, topks[s], s)
+    offs, slot = oracle.layout_ref(t.R, out["token_dest"], out["send_counts"])
+    ref_offs, ref_slot = _layout_by_sort(t.R, out["token_dest"], out["send_counts"])
+    assert (offs == ref_offs).all()
+    assert (slot == ref_slot).all()
+    # every slot of [0, T k) is used once
+    assert np.array_equal(np.sort(slot.ravel()), np.arange(slot.size))
+
+
+def test_dispatch_layout_special_cases():
+    # destinations that are not ranks keep slot -1 and take no room
+    dest = np.array([[2, -1], [0, 2], [5, 0]], np.int32)
+    offs, slot = oracle.layout_ref(3, dest, np.array([2, 0, 2], np.int32))
+    assert offs.tolist() == [0, 2, 2, 4]
+    assert slot.tolist() == [[2, -1], [0, 3], [-1, 1]]
+    # one destination: the slot is the row-major index
+    dest = np.zeros((5, 3), np.int32)
+    offs, slot = oracle.layout_ref(4, dest, np.array([15, 0, 0, 0], np.int32))
+    assert offs.tolist() == [0, 15, 15, 15, 15]
+    assert (slot.ravel() == np.arange(15)).all()
+    # empty batch
+    offs, slot = oracle.layout_ref(2, np.zeros((0, 2), np.int32), np.zeros(2, np.int32))
+    assert offs.tolist() == [0, 0, 0] and slot.shape == (0, 2)
+
+
+def test_receive_counts_without_a_plan():
+    t, omega, topks = random_instance(77, big=True)
+    om = omega.copy()
+    om[0, 0] = -1
+    out = run(t, om, topks[0], 0)
+    assert out["status"] & oracle.ST_NEG_LOAD
+    assert (out["recv_counts"] == 0).all()
