@@ -194,6 +194,73 @@ int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t 
                       int32_t *status, void *workspace, size_t workspace_bytes, void *stream,
                       const topoep_launch *launch);
 
+/*
+ * Dispatch side of a plan (Section 4.3: the expert-parallel dispatch
+ * consumes the per-destination counts q of the plan).  Every rank makes the
+ * same plan from the same Omega, so what a rank receives follows from the
+ * plan without communication, and the send buffer can be laid out before
+ * the all-to-all.
+ *
+ * Send-buffer layout: the assignments grouped by destination rank, ranks
+ * ascending, row-major (token, k) order inside one destination.
+ */
+
+/* Bytes of device workspace topoep_dispatch_layout needs (TOPOEP_EINVAL for
+ * invalid sizes, TOPOEP_ELIMIT for R > 1024). */
+int topoep_layout_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, size_t *bytes_out);
+
+/*
+ * Enqueue the send-buffer layout of a plan's destinations (one kernel).
+ *
+ *   token_dest    device int32 [T, k]: destinations from a plan (values
+ *                 outside [0, R) take no slot).  May be NULL when T == 0.
+ *   send_counts   device int32 [R]: the same plan's send counts (the number
+ *                 of assignments per destination).
+ *   send_offsets  device int32 out [R + 1]: exclusive prefix of send_counts
+ *                 ([R] = the total).
+ *   token_slot    device int32 out [T, k]: send_offsets[dest] + the number of
+ *                 earlier assignments (row-major) with the same destination;
+ *                 -1 where token_dest is not a rank.  May be NULL when T == 0.
+ *   status        device int32 [1] or NULL: TOPOEP_ST_SYNC is ORed in if a
+ *                 bounded wait gave up (slots then wrong; zero-fill the
+ *                 workspace again before the next call).
+ *   workspace     at least topoep_layout_workspace_bytes bytes, 256-byte
+ *                 aligned, zero-filled before its first call; every call
+ *                 leaves it zero again.  Calls sharing a workspace must be
+ *                 ordered on one stream.
+ *
+ * Only topo->num_ranks is read from the topology.  Host checks as
+ * topoep_plan (TOPOEP_EINVAL for null pointers or invalid sizes,
+ * TOPOEP_EWORKSPACE, TOPOEP_EHIP, TOPOEP_ELIMIT for R > 1024).
+ */
+int topoep_dispatch_layout(const topoep_topology *topo, const int32_t *token_dest, int32_t T, int32_t k,
+                           const int32_t *send_counts, int32_t *send_offsets, int32_t *token_slot,
+                           int32_t *status, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of device workspace topoep_plan_dispatch needs: the plan's
+ * (default launch shape), rounded up to 256, plus the layout's. */
+int topoep_dispatch_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k,
+                                    int32_t replica_budget, size_t *bytes_out);
+
+/*
+ * Enqueue one plan (as topoep_plan, default launch shape) and its dispatch
+ * side:
+ *   recv_counts   device int32 out [R] or NULL: recv_counts[s] =
+ *                 sum_e q[s][e][self], the assignments rank s sends to this
+ *                 rank under the same plan (0 when no plan is made).
+ *   send_offsets, token_slot: as topoep_dispatch_layout (both NULL to skip
+ *                 the layout; recv_counts and the layout may not both be
+ *                 skipped).
+ * The workspace is one buffer of topoep_dispatch_workspace_bytes bytes
+ * (256-byte aligned, zero-filled before its first call).  Return codes as
+ * topoep_plan and topoep_dispatch_layout.
+ */
+int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
+                         int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots,
+                         int32_t *token_dest, int32_t *send_counts, int32_t *recv_counts,
+                         int32_t *send_offsets, int32_t *token_slot, int32_t *status, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

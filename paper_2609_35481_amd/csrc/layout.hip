@@ -1,0 +1,326 @@
+// Dispatch layout of the rerouted assignments on gfx950: the send buffer
+// groups the assignments by destination rank (ranks ascending) and keeps
+// row-major (token, k) order inside one destination, so each destination's
+// assignments form one contiguous run that an all-to-all dispatch sends as
+// is (the per-destination counts the dispatch consumes, Section 4.3).
+//
+// One pass over token_dest, one launch:
+//   - each workgroup holds a contiguous chunk of assignments in registers
+//     and ranks them among equal destinations inside each wave (ballots
+//     over the destination bits give each lane its peers), then scans the
+//     per-wave counts across waves in LDS;
+//   - it publishes its per-destination counts (flag 1), then looks back
+//     over up to 64 predecessors at a time: wave 0 waits for their flags in
+//     parallel and stops at the nearest one whose inclusive prefix is
+//     published (flag 2), the whole workgroup sums their counts per
+//     destination, and the workgroup publishes its own inclusive prefix
+//     (flag 2).  Workgroup 0 publishes its counts as its inclusive prefix;
+//   - slot = send_offsets[dest] + (earlier workgroups) + (earlier waves) +
+//     (rank in the wave).
+// The waits are bounded and only on lower workgroup indices, which are
+// dispatched first.  The last workgroup to finish its look-back (a ticket)
+// clears every flag, so the workspace is zero again for the next call.
+// All arithmetic is integer and no atomic decides an order.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "topoep.h"
+#include "wave.h"
+
+namespace {
+
+using namespace topoep_dev;
+
+constexpr int kLayoutThreads = 1024;
+constexpr int kLayoutMaxRanks = 1024;   // per-wave counts of 16 waves fit 64 KB of LDS
+constexpr int kLayoutWindow = 64;       // predecessors examined per look-back step
+constexpr uint32_t kLayoutSpin = 1u << 24;
+constexpr int kLayoutCtrlBytes = 256;
+
+struct Layout {
+  int R, nbits, nb;
+  int64_t n, chunk;
+  const int32_t *dest;
+  const int32_t *send;
+  int32_t *offs_out;   // [R + 1]
+  int32_t *slot_out;   // [n]
+  int32_t *status;     // [1] or null: TOPOEP_ST_SYNC when a wait gave up
+  uint32_t *agg;       // [nb][R] counts of each workgroup
+  uint32_t *incl;      // [nb][R] inclusive prefixes over workgroups
+  uint32_t *flags;     // [nb] 0, 1 counts published, 2 inclusive prefix published
+  uint32_t *ctrl;      // [0] finish ticket
+  uint32_t spin_limit;
+};
+
+// LDS words: per-wave counts (then offsets) [nw][R], the workgroup's counts
+// [R], the exclusive prefix over earlier workgroups [R], send offsets
+// [R + 1], scan scratch and broadcast words.
+struct LayoutLds {
+  int wc, agg, excl, offs, tmp, misc, words;
+};
+
+__host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
+  LayoutLds l;
+  int o = 0;
+  l.wc = o; o += (nt / 64) * R;
+  l.agg = o; o += R;
+  l.excl = o; o += R;
+  l.offs = o; o += R + 1;
+  l.tmp = o; o += nt / 64 + 1;
+  l.misc = o; o += 8;
+  l.words = o;
+  return l;
+}
+
+template <int IPT>
+__global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
+  extern __shared__ int lsm[];
+  const int R = L.R, tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
+  const int b = blockIdx.x;
+  const LayoutLds l = layout_lds(R, nt);
+  int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs;
+  int *tmp = lsm + l.tmp, *misc = lsm + l.misc;
+  const int64_t lo = (int64_t)b * L.chunk;
+  const int64_t hi = lo + L.chunk < L.n ? lo + L.chunk : L.n;
+  const int64_t wbase = lo + (int64_t)wave * 64 * IPT + lane;
+
+  int dv[IPT], lr[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    dv[i] = idx < hi ? L.dest[idx] : -1;
+  }
+  // send offsets (exclusive prefix of the plan's send counts)
+  for (int r = tid; r < R; r += nt) offs[r] = L.send[r];
+  for (int r = lane; r < R; r += 64) wc[wave * R + r] = 0;
+  for (int r = tid; r < R; r += nt) excl[r] = 0;
+  if (tid < 8) misc[tid] = 0;
+  lds_barrier();
+  offs[R] = block_excl_scan(offs, R, tmp);
+  if (b == 0 && L.offs_out)
+    for (int r = tid; r <= R; r += nt) L.offs_out[r] = offs[r];
+
+  // rank of each assignment among the wave's earlier ones with the same
+  // destination (index order: i, then lane)
+  int *mywc = wc + wave * R;
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const bool valid = (unsigned)dv[i] < (unsigned)R;
+    const uint64_t peers = peer_mask(dv[i], valid, L.nbits);
+    const int c = valid ? mywc[dv[i]] : 0;
+    lr[i] = c + __popcll(peers & lanemask_lt());
+    wave_sync();
+    if (valid && (peers & lanemask_lt()) == 0) mywc[dv[i]] = c + __popcll(peers);
+    wave_sync();
+  }
+  lds_barrier();
+  // per destination: offsets of the waves, the workgroup's counts
+  for (int r = tid; r < R; r += nt) {
+    int sum = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int c = wc[w * R + r];
+      wc[w * R + r] = sum;
+      sum += c;
+    }
+    agg[r] = sum;
+    L.agg[(int64_t)b * R + r] = (uint32_t)sum;
+    if (b == 0) L.incl[r] = (uint32_t)sum;
+  }
+  drain_then_barrier();
+  if (tid == 0)
+    __hip_atomic_store(L.flags + b, b == 0 ? 2u : 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+
+  // look-back over the workgroups before b
+  bool ok = true;
+  int jhi = b - 1;
+  while (jhi >= 0) {
+    if (wave == 0) {
+      const int cnt = imin(kLayoutWindow, jhi + 1);
+      const int j = jhi - lane;
+      uint32_t f = 0;
+      bool gave_up = false;
+      if (lane < cnt) {
+        uint32_t it = 0;
+        while ((f = __hip_atomic_load(L.flags + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) == 0u) {
+          if (++it > L.spin_limit) {
+            gave_up = true;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      const uint64_t done = __ballot(lane < cnt && f == 2u);
+      const bool bad = __ballot(gave_up) != 0;
+      // the nearest predecessor with an inclusive prefix, else the window's end
+      const int stop = done ? jhi - (__ffsll((long long)done) - 1) : jhi - cnt + 1;
+      if (lane == 0) {
+        misc[0] = stop;
+        misc[1] = done != 0;
+        misc[2] = bad;
+      }
+    }
+    __syncthreads();
+    const int stop = misc[0];
+    const bool found = misc[1] != 0;
+    if (misc[2]) {
+      ok = false;
+      break;
+    }
+    // excl[r] += counts of stop+1 .. jhi, plus the inclusive prefix (or the
+    // counts) of stop
+    const int span = jhi - stop + 1;
+    for (int x = tid; x < span * R; x += nt) {
+      const int jj = x / R, r = x - jj * R;
+      const int j = stop + jj;
+      const uint32_t v = (j == stop && found) ? L.incl[(int64_t)j * R + r] : L.agg[(int64_t)j * R + r];
+      if (v) atomicAdd(&excl[r], (int)v);
+    }
+    lds_barrier();
+    if (found) break;
+    jhi = stop - 1;
+  }
+  if (b > 0) {
+    for (int r = tid; r < R; r += nt) L.incl[(int64_t)b * R + r] = (uint32_t)(excl[r] + agg[r]);
+    drain_then_barrier();
+    if (tid == 0)
+      __hip_atomic_store(L.flags + b, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // this workgroup has read every flag it needs: the last one to get here
+  // clears them all for the next call
+  if (tid == 0) {
+    const uint32_t t = __hip_atomic_fetch_add(L.ctrl, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    misc[3] = t + 1u == (uint32_t)L.nb;
+    if (!ok && L.status) atomicOr(reinterpret_cast<unsigned *>(L.status), TOPOEP_ST_SYNC);
+  }
+  __syncthreads();
+  if (misc[3]) {
+    for (int j = tid; j < L.nb; j += nt)
+      __hip_atomic_store(L.flags + j, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(L.ctrl, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    if (idx < hi) {
+      const int d = dv[i];
+      const bool valid = ok && (unsigned)d < (unsigned)R;
+      L.slot_out[idx] = valid ? offs[d] + excl[d] + wc[wave * R + d] + lr[i] : -1;
+    }
+  }
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int ceil_log2(int v) {
+  int b = 0;
+  while ((1 << b) < v) ++b;
+  return b;
+}
+
+struct LayoutShape {
+  int ipt;
+  size_t lds;
+};
+
+// Sizes, launch shape and workspace layout (pointers stay null when ws is).
+int layout_setup(const topoep_topology *t, int32_t T, int32_t k, Layout *out, LayoutShape *sh,
+                 size_t *ws_bytes, char *ws) {
+  if (!t) return TOPOEP_EINVAL;
+  const int R = t->num_ranks;
+  if (R <= 0 || T < 0 || k < 1 || (int64_t)T * k > 0x7FFFFFFF) return TOPOEP_EINVAL;
+  if (R > kLayoutMaxRanks) return TOPOEP_ELIMIT;
+  Layout L = {};
+  L.R = R;
+  L.nbits = ceil_log2(R);
+  L.n = (int64_t)T * k;
+  // ids per thread: the fewest that keep the grid at most 4096 workgroups
+  int ipt = 1;
+  while (ipt < 8 && L.n > (int64_t)kLayoutThreads * ipt * 4096) ipt *= 2;
+  if (L.n <= (int64_t)kLayoutThreads * 16) ipt = 1;
+  else if (ipt < 4) ipt = 4;
+  L.chunk = (int64_t)kLayoutThreads * ipt;
+  const int64_t nb = L.n > 0 ? (L.n + L.chunk - 1) / L.chunk : 1;
+  if (nb > (1 << 20)) return TOPOEP_ELIMIT;
+  L.nb = (int)nb;
+  L.spin_limit = kLayoutSpin;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t o_ctrl = take(kLayoutCtrlBytes);
+  const size_t o_flag = take((size_t)L.nb * 4);
+  const size_t o_agg = take((size_t)L.nb * R * 4);
+  const size_t o_incl = take((size_t)L.nb * R * 4);
+  *ws_bytes = off;
+  if (ws) {
+    L.ctrl = reinterpret_cast<uint32_t *>(ws + o_ctrl);
+    L.flags = reinterpret_cast<uint32_t *>(ws + o_flag);
+    L.agg = reinterpret_cast<uint32_t *>(ws + o_agg);
+    L.incl = reinterpret_cast<uint32_t *>(ws + o_incl);
+  }
+  sh->ipt = ipt;
+  sh->lds = (size_t)layout_lds(R, kLayoutThreads).words * 4;
+  *out = L;
+  return TOPOEP_OK;
+}
+
+bool g_layout_attrs = false;
+
+void layout_attrs() {
+  if (g_layout_attrs) return;
+  const void *ks[] = {reinterpret_cast<const void *>(layout_kernel<1>), reinterpret_cast<const void *>(layout_kernel<2>),
+                      reinterpret_cast<const void *>(layout_kernel<4>), reinterpret_cast<const void *>(layout_kernel<8>)};
+  for (const void *kf : ks) (void)hipFuncSetAttribute(kf, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  g_layout_attrs = true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int topoep_layout_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, size_t *bytes_out) {
+  if (!bytes_out) return TOPOEP_EINVAL;
+  Layout L;
+  LayoutShape sh;
+  size_t need = 0;
+  const int rc = layout_setup(topo, T, k, &L, &sh, &need, nullptr);
+  if (rc == TOPOEP_OK) *bytes_out = need;
+  return rc;
+}
+
+int topoep_dispatch_layout(const topoep_topology *topo, const int32_t *token_dest, int32_t T, int32_t k,
+                           const int32_t *send_counts, int32_t *send_offsets, int32_t *token_slot,
+                           int32_t *status, void *workspace, size_t workspace_bytes, void *stream) {
+  Layout L;
+  LayoutShape sh;
+  size_t need = 0;
+  int rc = layout_setup(topo, T, k, &L, &sh, &need, nullptr);
+  if (rc != TOPOEP_OK) return rc;
+  if (!send_counts || !send_offsets || !workspace || (T > 0 && (!token_dest || !token_slot)))
+    return TOPOEP_EINVAL;
+  if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return TOPOEP_EWORKSPACE;
+  rc = layout_setup(topo, T, k, &L, &sh, &need, static_cast<char *>(workspace));
+  if (rc != TOPOEP_OK) return rc;
+  L.dest = token_dest;
+  L.send = send_counts;
+  L.offs_out = send_offsets;
+  L.slot_out = token_slot;
+  L.status = status;
+  layout_attrs();
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const dim3 g(L.nb), bl(kLayoutThreads);
+  switch (sh.ipt) {
+    case 1: hipLaunchKernelGGL(layout_kernel<1>, g, bl, sh.lds, st, L); break;
+    case 2: hipLaunchKernelGGL(layout_kernel<2>, g, bl, sh.lds, st, L); break;
+    case 4: hipLaunchKernelGGL(layout_kernel<4>, g, bl, sh.lds, st, L); break;
+    default: hipLaunchKernelGGL(layout_kernel<8>, g, bl, sh.lds, st, L); break;
+  }
+  return hipGetLastError() == hipSuccess ? TOPOEP_OK : TOPOEP_EHIP;
+}
+
+}  // extern "C"

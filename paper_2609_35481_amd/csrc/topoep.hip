@@ -39,8 +39,11 @@
 
 #include "fastdiv.h"
 #include "topoep.h"
+#include "wave.h"
 
 namespace {
+
+using namespace topoep_dev;
 
 // ---------------------------------------------------------------- constants
 
@@ -83,13 +86,12 @@ struct Plan {
   FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
+  int32_t *recv_out;   // receive counts [R], or null
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
   uint32_t *pub, *flags, *ghist;   // one-launch plan: chunk counts, flags, histogram (E + 1 words)
 };
 
-__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
-__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
 
 // Scratch words of the histogram reduction (hist_from_partials, load_fast)
 // for up to 1024 threads: max(E, 4 * threads).
@@ -173,150 +175,6 @@ __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
   l.flag = o; o += 4;
   l.words = o;
   return l;
-}
-
-// ---------------------------------------------------------------- wave helpers
-
-__device__ inline int lane_id() { return threadIdx.x & 63; }
-
-__device__ inline uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
-
-// Lanes of this wave holding the same (valid) value: one ballot per id bit.
-__device__ inline uint64_t peer_mask(int v, bool valid, int nbits) {
-  uint64_t m = __ballot(valid);
-  for (int b = 0; b < nbits; ++b) {
-    const bool bit = (v >> b) & 1;
-    const uint64_t on = __ballot(bit);
-    m &= bit ? on : ~on;
-  }
-  return m;
-}
-
-// Order LDS traffic of the lanes of one wave (the refinement runs on one
-// wave and needs no workgroup barrier).
-__device__ inline void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-
-// Workgroup barrier that orders LDS only: it does not wait for outstanding
-// global stores (the solver's outputs), unlike __syncthreads.
-__device__ inline void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// Cross-lane moves within rows of 16 lanes (DPP); every lane of the wave
-// must be active.  0x121..0x12F = row_ror:1..15, 0x111..0x11F = row_shr,
-// 0x142/0x143 = row_bcast:15/31.
-template <int C>
-__device__ inline uint32_t dpp_mov(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, C, 0xF, 0xF, true);
-}
-template <int C>
-__device__ inline uint64_t dpp_mov64(uint64_t v) {
-  return ((uint64_t)dpp_mov<C>((uint32_t)(v >> 32)) << 32) | dpp_mov<C>((uint32_t)v);
-}
-__device__ inline uint64_t readlane64(uint64_t v, int l) {
-  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
-         (uint32_t)__builtin_amdgcn_readlane((int)v, l);
-}
-
-// Wave-wide minimum / maximum / sum, the same value in every lane: rotations
-// by 8, 4, 2, 1 inside each row of 16 lanes, then the four row results.
-__device__ inline uint64_t wave_min_u64(uint64_t v) {
-  uint64_t o;
-  o = dpp_mov64<0x128>(v); v = o < v ? o : v;
-  o = dpp_mov64<0x124>(v); v = o < v ? o : v;
-  o = dpp_mov64<0x122>(v); v = o < v ? o : v;
-  o = dpp_mov64<0x121>(v); v = o < v ? o : v;
-  uint64_t a = readlane64(v, 0), b = readlane64(v, 16), c = readlane64(v, 32), d = readlane64(v, 48);
-  a = b < a ? b : a;
-  c = d < c ? d : c;
-  return c < a ? c : a;
-}
-
-__device__ inline uint64_t wave_max_u64(uint64_t v) { return ~wave_min_u64(~v); }
-
-__device__ inline uint64_t wave_sum_u64(uint64_t v) {
-  v += dpp_mov64<0x128>(v);
-  v += dpp_mov64<0x124>(v);
-  v += dpp_mov64<0x122>(v);
-  v += dpp_mov64<0x121>(v);
-  return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
-}
-
-// Inclusive prefix sum over the 64 lanes (row shifts, then row broadcasts).
-__device__ inline int wave_incl_scan(int x) {
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
-  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
-  return x;
-}
-
-__device__ inline int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
-
-__device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t b1, uint64_t b2,
-                                uint64_t b3) {
-  if (a1 != b1) return a1 < b1;
-  if (a2 != b2) return a2 < b2;
-  return a3 < b3;
-}
-
-// Lexicographic minimum of (k1, k2, k3) over the wave, in every lane: one
-// wave minimum per key, the later ones only when the earlier key ties.
-__device__ inline void wave_argmin3(uint64_t &k1, uint64_t &k2, uint64_t &k3) {
-  const uint64_t m1 = wave_min_u64(k1);
-  uint64_t tie = __ballot(k1 == m1);
-  if (__popcll(tie) == 1) {
-    const int l = __ffsll((long long)tie) - 1;
-    k1 = m1;
-    k2 = readlane64(k2, l);
-    k3 = readlane64(k3, l);
-    return;
-  }
-  const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
-  tie = __ballot(k1 == m1 && k2 == m2);
-  const uint64_t m3 = wave_min_u64((k1 == m1 && k2 == m2) ? k3 : ~0ull);
-  k1 = m1;
-  k2 = m2;
-  k3 = m3;
-}
-
-// Exclusive scan of a[0..n) in place by the whole workgroup; returns the total.
-// tmp needs blockDim/64 + 1 words.
-__device__ int block_excl_scan(int *a, int n, int *tmp) {
-  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
-  const int per = (n + nt - 1) / nt;
-  const int lo = imin(n, tid * per), hi = imin(n, lo + per);
-  int s = 0;
-  for (int i = lo; i < hi; ++i) s += a[i];
-  const int incl = wave_incl_scan(s);
-  if (lane == 63) tmp[wave] = incl;
-  lds_barrier();
-  if (tid == 0) {
-    int run = 0;
-    for (int w = 0; w < nw; ++w) {
-      const int t = tmp[w];
-      tmp[w] = run;
-      run += t;
-    }
-    tmp[nw] = run;
-  }
-  lds_barrier();
-  int run = tmp[wave] + incl - s;
-  for (int i = lo; i < hi; ++i) {
-    const int t = a[i];
-    a[i] = run;
-    run += t;
-  }
-  const int total = tmp[nw];
-  lds_barrier();
-  return total;
 }
 
 // Global -> LDS copy by the whole workgroup, four 16-byte loads in flight
@@ -575,19 +433,6 @@ __device__ inline bool out_of_range(const Plan &p, uint64_t total) {
   return tok + rep >= lim;
 }
 
-// Hand-overs between workgroups.  A workgroup barrier orders the waves but
-// does not wait for their global stores, and one wave's agent-scope release
-// (an L2 write-back) only covers stores that have reached the L2.  So before
-// the barrier that precedes a signal every wave waits for its own memory
-// operations to complete (s_waitcnt, no cache operation); then one wave
-// releases and signals.  On the waiting side one wave acquires (the L1 and
-// L2 invalidations cover the whole CU) before the barrier that releases the
-// other waves' loads.
-__device__ inline void drain_then_barrier() {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-}
-
 // Grid barrier of the per-domain solver workgroups: all of them are
 // resident (at most kMaxSolveGroups), and the wait is bounded so the kernel
 // always exits.
@@ -693,13 +538,15 @@ __device__ inline int route_batch(const int *src, int stride, int *dst, const Ro
   return sum;
 }
 
-// q[self][e][r] of an instance of e in domain d, w = omega[self][e]: the
-// routing rule of route_instances for the single source `self`.
-__device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uint32_t *mask, const FastDiv *fdt) {
-  const int ds = (int)fdiv((uint32_t)p.self, p.fG);
-  if (ds == d) return w;                                   // the instance inside dom(self)
+// q[s][e][r] of an instance of e in domain d for one source s of domain ds,
+// w = omega[s][e]: the routing rule of route_instances for a single source
+// (the whole load to the instance in the source's own domain, nothing when
+// another instance sits there, else the even split over the hosting
+// domains, the remainder to the lowest ones).
+__device__ inline int route_q(const Plan &p, int d, int e, int w, int ds, const uint32_t *mask, const FastDiv *fdt) {
+  if (ds == d) return w;                                   // the instance inside dom(s)
   const uint32_t *me = mask + e * p.MW;
-  if ((me[ds >> 5] >> (ds & 31)) & 1u) return 0;           // dom(self) hosts e itself
+  if ((me[ds >> 5] >> (ds & 31)) & 1u) return 0;           // dom(s) hosts e itself
   int n = 0, below = 0;
   for (int wd = 0; wd < p.MW; ++wd) {
     const uint32_t bits = me[wd];
@@ -711,6 +558,31 @@ __device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uin
   const FastDiv fn = fdt[n];
   const int qq = (int)fdiv_hi((uint32_t)w, fn);
   return qq + (below < w - qq * n ? 1 : 0);
+}
+
+__device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uint32_t *mask, const FastDiv *fdt) {
+  return route_q(p, d, e, w, (int)fdiv((uint32_t)p.self, p.fG), mask, fdt);
+}
+
+// Receive counts: recv[s] = sum over the instances on rank self (instance
+// indices i0 .. i0 + PN - 1, expert e_of[i], column qcol + i * QS) of
+// q[s][e][self].  With full, every source's q of those instances is in
+// qcol (and reflects the refinement); otherwise the routing rule gives it
+// from omega(s, e).
+template <class OmegaOf>
+__device__ void write_recv_counts(const Plan &p, int i0, const int *e_of, const int *qcol, bool full,
+                                  const uint32_t *mask, const FastDiv *fdt, OmegaOf omega_of) {
+  const int ds = (int)fdiv((uint32_t)p.self, p.fG);
+  for (int s = threadIdx.x; s < p.R; s += blockDim.x) {
+    const int dsrc = (int)fdiv((uint32_t)s, p.fG);
+    int sum = 0;
+    for (int pos = 0; pos < p.PN; ++pos) {
+      const int i = i0 + pos, e = e_of[i];
+      if (e < 0) continue;
+      sum += full ? qcol[i * p.QS + s] : route_q(p, ds, e, omega_of(s, e), dsrc, mask, fdt);
+    }
+    p.recv_out[s] = sum;
+  }
 }
 
 // full(d): whether every source's q is needed for domain d's instances.  A
@@ -1214,6 +1086,8 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     if (noplan) {
       for (int i = tid; i < G * p.N; i += nt) p.slots_out[(int64_t)d * G * p.N + i] = -1;
       for (int j = tid; j < G; j += nt) p.send_out[d * G + j] = 0;
+      if (p.recv_out && d == (int)fdiv((uint32_t)p.self, p.fG))
+        for (int r = tid; r < R; r += nt) p.recv_out[r] = 0;
       for (int a = tid; a < I; a += nt) {
         p.seg_e[(int64_t)d * I + a] = -1;
         p.seg_q[(int64_t)d * I + a] = 0;
@@ -1295,6 +1169,9 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       p.seg_e[(int64_t)d * I + a] = e_of[a];
       p.seg_q[(int64_t)d * I + a] = e_of[a] >= 0 ? qcol[a * p.QS + p.self] : 0;
     }
+    if (p.recv_out && d == (int)fdiv((uint32_t)p.self, p.fG))
+      write_recv_counts(p, (p.self - d * G) * PN, e_of, qcol, full, mask, fdt,
+                        [&](int s, int e) { return s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]; });
     lds_barrier();
   }
   if (tid == 0 && (flags || !synced)) atomicOr(&p.ctrl[kCtrlStatus], flags | (synced ? 0u : TOPOEP_ST_SYNC));
@@ -1436,6 +1313,8 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   if (gst & (kNoPlan | TOPOEP_ST_SYNC)) {
     for (int i = tid; i < R * p.N; i += nt) p.slots_out[i] = -1;
     for (int r = tid; r < R; r += nt) p.send_out[r] = 0;
+    if (p.recv_out)
+      for (int r = tid; r < R; r += nt) p.recv_out[r] = 0;
     if (tid == 0) {
       p.ctrl[kCtrlFinal] = gst;
       if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), gst);
@@ -1561,6 +1440,16 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   }
 }
 
+// Receive counts from the single-workgroup solver's final LDS state (after
+// single_plan made a plan): the instances on rank self, full columns when
+// its domain was routed for every source.
+__device__ void single_recv_counts(const Plan &p, const SingleState &t) {
+  const int ds = (int)fdiv((uint32_t)p.self, p.fG), E = p.E;
+  const int *om = t.om;
+  write_recv_counts(p, ds * p.I + (p.self - ds * p.G) * p.PN, t.e_of, t.qcol, t.dfree[ds] != 0, t.mask, t.fdt,
+                    [&](int s, int e) { return om[s * E + e]; });
+}
+
 // The same steps with every domain's state in the LDS of one CU; each
 // domain's refinement runs on its own wave.  Used when Omega and all q
 // columns fit in LDS.  Workgroups beyond the first compute the histogram
@@ -1591,6 +1480,7 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
   uint32_t gst = (uint32_t)t.misc[0];
   if (out_of_range(p, *reinterpret_cast<unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
   single_plan(p, t, gst, false);
+  if (p.recv_out && !(gst & kNoPlan)) single_recv_counts(p, t);
 }
 
 // ---------------------------------------------------------------- reroute
@@ -1819,6 +1709,7 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   const bool synced = t.misc[2] != 0;
   const uint32_t verdict = (uint32_t)t.misc[3];
   const bool stands = synced && verdict == kVerdictSame && spec;
+  bool planned = stands;
   // a rewrite of the speculative outputs is ordered after their stores
   if (spec && !stands) drain_then_barrier();
   if (stands) {
@@ -1855,9 +1746,12 @@ __device__ void fused_solver(const Plan &p, int *sm) {
     uint32_t gst = (uint32_t)t.misc[0];
     if (out_of_range(p, total0 + *reinterpret_cast<const unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
     single_plan(p, t, gst, true);
+    planned = !(gst & kNoPlan);
   } else {
     single_plan(p, t, TOPOEP_ST_SYNC, true);
   }
+  // receive counts of a plan that was made (a refused one wrote zeros)
+  if (planned && p.recv_out) single_recv_counts(p, t);
   // release: every output, the instance list and the final status before
   // the flags
   drain_then_barrier();
@@ -2359,7 +2253,8 @@ constexpr int kFloorMask = 8;
 int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_load,
             const int32_t *local_topk, int32_t T, int32_t k, int32_t N, int32_t *replica_slots,
             int32_t *token_dest, int32_t *send_counts, int32_t *status, void *workspace,
-            size_t workspace_bytes, void *stream, const topoep_launch *launch) {
+            size_t workspace_bytes, void *stream, const topoep_launch *launch,
+            int32_t *recv_counts = nullptr) {
   Plan p;
   Shape s;
   size_t need = 0;
@@ -2377,6 +2272,7 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
   p.dest_out = token_dest;
   p.send_out = send_counts;
   p.status_out = status;
+  p.recv_out = recv_counts;
   set_attrs();
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
@@ -2454,6 +2350,41 @@ int topoep_plan(const topoep_topology *topo, const int32_t *global_load, const i
                 void *stream) {
   return enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest,
                  send_counts, status, workspace, workspace_bytes, stream, nullptr);
+}
+
+int topoep_dispatch_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
+                                    size_t *bytes_out) {
+  if (!bytes_out) return TOPOEP_EINVAL;
+  size_t plan_bytes = 0, layout_bytes = 0;
+  int rc = topoep_workspace_bytes_ex(topo, T, k, replica_budget, nullptr, &plan_bytes);
+  if (rc != TOPOEP_OK) return rc;
+  rc = topoep_layout_workspace_bytes(topo, T, k, &layout_bytes);
+  if (rc != TOPOEP_OK) return rc;
+  *bytes_out = align256(plan_bytes) + layout_bytes;
+  return TOPOEP_OK;
+}
+
+int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
+                         int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots,
+                         int32_t *token_dest, int32_t *send_counts, int32_t *recv_counts, int32_t *send_offsets,
+                         int32_t *token_slot, int32_t *status, void *workspace, size_t workspace_bytes,
+                         void *stream) {
+  size_t plan_bytes = 0, layout_bytes = 0, total = 0;
+  int rc = topoep_workspace_bytes_ex(topo, T, k, replica_budget, nullptr, &plan_bytes);
+  if (rc != TOPOEP_OK) return rc;
+  rc = topoep_dispatch_workspace_bytes(topo, T, k, replica_budget, &total);
+  if (rc != TOPOEP_OK) return rc;
+  const bool layout = send_offsets != nullptr || token_slot != nullptr;
+  if (layout && (!send_offsets || (T > 0 && !token_slot))) return TOPOEP_EINVAL;
+  if (!recv_counts && !layout) return TOPOEP_EINVAL;
+  if (!workspace) return TOPOEP_EINVAL;
+  if (workspace_bytes < total || (reinterpret_cast<uintptr_t>(workspace) & 255)) return TOPOEP_EWORKSPACE;
+  layout_bytes = total - align256(plan_bytes);
+  rc = enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
+               status, workspace, plan_bytes, stream, nullptr, recv_counts);
+  if (rc != TOPOEP_OK || !layout) return rc;
+  return topoep_dispatch_layout(topo, token_dest, T, k, send_counts, send_offsets, token_slot, status,
+                                static_cast<char *>(workspace) + align256(plan_bytes), layout_bytes, stream);
 }
 
 int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t *global_load,

@@ -1,0 +1,171 @@
+// Wave64 and workgroup helpers shared by the planner's kernels (gfx950):
+// lane masks, ballot peer groups, DPP reductions and scans, LDS-only
+// barriers and the drain-then-signal hand-over between workgroups.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace topoep_dev {
+
+__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
+__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
+
+// ---------------------------------------------------------------- wave helpers
+
+__device__ inline int lane_id() { return threadIdx.x & 63; }
+
+__device__ inline uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+// Lanes of this wave holding the same (valid) value: one ballot per id bit.
+__device__ inline uint64_t peer_mask(int v, bool valid, int nbits) {
+  uint64_t m = __ballot(valid);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (v >> b) & 1;
+    const uint64_t on = __ballot(bit);
+    m &= bit ? on : ~on;
+  }
+  return m;
+}
+
+// Order LDS traffic of the lanes of one wave (the refinement runs on one
+// wave and needs no workgroup barrier).
+__device__ inline void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Workgroup barrier that orders LDS only: it does not wait for outstanding
+// global stores (the solver's outputs), unlike __syncthreads.
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Cross-lane moves within rows of 16 lanes (DPP); every lane of the wave
+// must be active.  0x121..0x12F = row_ror:1..15, 0x111..0x11F = row_shr,
+// 0x142/0x143 = row_bcast:15/31.
+template <int C>
+__device__ inline uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, C, 0xF, 0xF, true);
+}
+template <int C>
+__device__ inline uint64_t dpp_mov64(uint64_t v) {
+  return ((uint64_t)dpp_mov<C>((uint32_t)(v >> 32)) << 32) | dpp_mov<C>((uint32_t)v);
+}
+__device__ inline uint64_t readlane64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+
+// Wave-wide minimum / maximum / sum, the same value in every lane: rotations
+// by 8, 4, 2, 1 inside each row of 16 lanes, then the four row results.
+__device__ inline uint64_t wave_min_u64(uint64_t v) {
+  uint64_t o;
+  o = dpp_mov64<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x121>(v); v = o < v ? o : v;
+  uint64_t a = readlane64(v, 0), b = readlane64(v, 16), c = readlane64(v, 32), d = readlane64(v, 48);
+  a = b < a ? b : a;
+  c = d < c ? d : c;
+  return c < a ? c : a;
+}
+
+__device__ inline uint64_t wave_max_u64(uint64_t v) { return ~wave_min_u64(~v); }
+
+__device__ inline uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp_mov64<0x128>(v);
+  v += dpp_mov64<0x124>(v);
+  v += dpp_mov64<0x122>(v);
+  v += dpp_mov64<0x121>(v);
+  return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
+}
+
+// Inclusive prefix sum over the 64 lanes (row shifts, then row broadcasts).
+__device__ inline int wave_incl_scan(int x) {
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
+  return x;
+}
+
+__device__ inline int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+
+__device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t b1, uint64_t b2,
+                                uint64_t b3) {
+  if (a1 != b1) return a1 < b1;
+  if (a2 != b2) return a2 < b2;
+  return a3 < b3;
+}
+
+// Lexicographic minimum of (k1, k2, k3) over the wave, in every lane: one
+// wave minimum per key, the later ones only when the earlier key ties.
+__device__ inline void wave_argmin3(uint64_t &k1, uint64_t &k2, uint64_t &k3) {
+  const uint64_t m1 = wave_min_u64(k1);
+  uint64_t tie = __ballot(k1 == m1);
+  if (__popcll(tie) == 1) {
+    const int l = __ffsll((long long)tie) - 1;
+    k1 = m1;
+    k2 = readlane64(k2, l);
+    k3 = readlane64(k3, l);
+    return;
+  }
+  const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
+  tie = __ballot(k1 == m1 && k2 == m2);
+  const uint64_t m3 = wave_min_u64((k1 == m1 && k2 == m2) ? k3 : ~0ull);
+  k1 = m1;
+  k2 = m2;
+  k3 = m3;
+}
+
+// Exclusive scan of a[0..n) in place by the whole workgroup; returns the total.
+// tmp needs blockDim/64 + 1 words.
+__device__ inline int block_excl_scan(int *a, int n, int *tmp) {
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
+  const int per = (n + nt - 1) / nt;
+  const int lo = imin(n, tid * per), hi = imin(n, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += a[i];
+  const int incl = wave_incl_scan(s);
+  if (lane == 63) tmp[wave] = incl;
+  lds_barrier();
+  if (tid == 0) {
+    int run = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int t = tmp[w];
+      tmp[w] = run;
+      run += t;
+    }
+    tmp[nw] = run;
+  }
+  lds_barrier();
+  int run = tmp[wave] + incl - s;
+  for (int i = lo; i < hi; ++i) {
+    const int t = a[i];
+    a[i] = run;
+    run += t;
+  }
+  const int total = tmp[nw];
+  lds_barrier();
+  return total;
+}
+
+// Hand-overs between workgroups.  A workgroup barrier orders the waves but
+// does not wait for their global stores, and one wave's agent-scope release
+// (an L2 write-back) only covers stores that have reached the L2.  So before
+// the barrier that precedes a signal every wave waits for its own memory
+// operations to complete (s_waitcnt, no cache operation); then one wave
+// releases and signals.  On the waiting side one wave acquires (the L1 and
+// L2 invalidations cover the whole CU) before the barrier that releases the
+// other waves' loads.
+__device__ inline void drain_then_barrier() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
+}  // namespace topoep_dev

@@ -98,8 +98,23 @@ _lib.topoep_plan_shape.restype = ctypes.c_int
 _lib.topoep_plan_shape.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32, ctypes.POINTER(Launch),
                                    ctypes.POINTER(Shape)]
 
+_lib.topoep_layout_workspace_bytes.restype = ctypes.c_int
+_lib.topoep_layout_workspace_bytes.argtypes = [ctypes.POINTER(Topology), _i32, _i32,
+                                               ctypes.POINTER(ctypes.c_size_t)]
+_lib.topoep_dispatch_layout.restype = ctypes.c_int
+_lib.topoep_dispatch_layout.argtypes = [ctypes.POINTER(Topology), _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp,
+                                        ctypes.c_size_t, _vp]
+_lib.topoep_dispatch_workspace_bytes.restype = ctypes.c_int
+_lib.topoep_dispatch_workspace_bytes.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32,
+                                                 ctypes.POINTER(ctypes.c_size_t)]
+_lib.topoep_plan_dispatch.restype = ctypes.c_int
+_lib.topoep_plan_dispatch.argtypes = [ctypes.POINTER(Topology), _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp,
+                                      _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+
 EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
-           "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape")
+           "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape",
+           "topoep_layout_workspace_bytes", "topoep_dispatch_layout",
+           "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch")
 
 
 def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
@@ -130,6 +145,34 @@ def plan_shape(topo: Topology, T: int, k: int, replica_budget: int, launch=None)
     if rc != OK:
         raise TopoepError("topoep_plan_shape", rc)
     return out
+
+
+def layout_workspace_bytes(topo: Topology, T: int, k: int) -> int:
+    out = ctypes.c_size_t(0)
+    rc = _lib.topoep_layout_workspace_bytes(ctypes.byref(topo), T, k, ctypes.byref(out))
+    if rc != OK:
+        raise TopoepError("topoep_layout_workspace_bytes", rc)
+    return out.value
+
+
+def dispatch_workspace_bytes(topo: Topology, T: int, k: int, replica_budget: int) -> int:
+    out = ctypes.c_size_t(0)
+    rc = _lib.topoep_dispatch_workspace_bytes(ctypes.byref(topo), T, k, replica_budget, ctypes.byref(out))
+    if rc != OK:
+        raise TopoepError("topoep_dispatch_workspace_bytes", rc)
+    return out.value
+
+
+def _aligned_workspace(nbytes, dev):
+    """A zero-filled byte tensor and the 256-byte aligned address inside it."""
+    ws = torch.zeros(nbytes + 256, dtype=torch.uint8, device=dev)
+    return ws, (ws.data_ptr() + 255) & ~255
+
+
+def _stream_ptr(stream, dev):
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
 def _dev_i32(t, name, shape=None):
@@ -199,6 +242,76 @@ class Planner:
     def workspace_view(self) -> torch.Tensor:
         off = self.ws_ptr - self._ws.data_ptr()
         return self._ws[off:off + self.ws_bytes]
+
+
+class DispatchPlanner:
+    """Plan plus its dispatch side (receive counts, send offsets, send-buffer
+    slot of every assignment) with preallocated outputs and workspace."""
+
+    def __init__(self, topo: Topology, T: int, k: int, replica_budget: int, device=None):
+        self.topo = topo
+        self.T, self.k, self.N = int(T), int(k), int(replica_budget)
+        dev = torch.device(device if device is not None else "cuda")
+        R = topo.num_ranks
+        self.ws_bytes = dispatch_workspace_bytes(topo, self.T, self.k, self.N)
+        self._ws, self.ws_ptr = _aligned_workspace(self.ws_bytes, dev)
+        self.replica_slots = torch.empty((R, self.N), dtype=torch.int32, device=dev)
+        self.token_dest = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
+        self.send_counts = torch.empty((R,), dtype=torch.int32, device=dev)
+        self.recv_counts = torch.empty((R,), dtype=torch.int32, device=dev)
+        self.send_offsets = torch.empty((R + 1,), dtype=torch.int32, device=dev)
+        self.token_slot = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
+        self.status = torch.empty((2,), dtype=torch.int32, device=dev)
+
+    def plan(self, global_load, local_topk, stream=None):
+        """Enqueue topoep_plan_dispatch; returns (replica_slots, token_dest,
+        send_counts, recv_counts, send_offsets, token_slot, status)."""
+        R, E = self.topo.num_ranks, self.topo.num_experts
+        _dev_i32(global_load, "global_load", (R, E))
+        if self.T > 0:
+            _dev_i32(local_topk, "local_topk", (self.T, self.k))
+        t = self.T > 0
+        rc = _lib.topoep_plan_dispatch(
+            ctypes.byref(self.topo), global_load.data_ptr(), local_topk.data_ptr() if t else None,
+            self.T, self.k, self.N, self.replica_slots.data_ptr() if self.replica_slots.numel() else None,
+            self.token_dest.data_ptr() if t else None, self.send_counts.data_ptr(),
+            self.recv_counts.data_ptr(), self.send_offsets.data_ptr(), self.token_slot.data_ptr() if t else None,
+            self.status.data_ptr(), self.ws_ptr, self.ws_bytes, _stream_ptr(stream, global_load.device))
+        if rc != OK:
+            raise TopoepError("topoep_plan_dispatch", rc)
+        return (self.replica_slots, self.token_dest, self.send_counts, self.recv_counts, self.send_offsets,
+                self.token_slot, self.status)
+
+
+class LayoutPlanner:
+    """The send-buffer layout alone (topoep_dispatch_layout) for a fixed
+    number of assignments, with preallocated outputs and workspace."""
+
+    def __init__(self, topo: Topology, T: int, k: int, device=None):
+        self.topo = topo
+        self.T, self.k = int(T), int(k)
+        dev = torch.device(device if device is not None else "cuda")
+        R = topo.num_ranks
+        self.ws_bytes = layout_workspace_bytes(topo, self.T, self.k)
+        self._ws, self.ws_ptr = _aligned_workspace(self.ws_bytes, dev)
+        self.send_offsets = torch.empty((R + 1,), dtype=torch.int32, device=dev)
+        self.token_slot = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
+        self.status = torch.zeros((1,), dtype=torch.int32, device=dev)
+
+    def layout(self, token_dest, send_counts, stream=None):
+        """Enqueue topoep_dispatch_layout; returns (send_offsets, token_slot)."""
+        R = self.topo.num_ranks
+        _dev_i32(send_counts, "send_counts", (R,))
+        t = self.T > 0
+        if t:
+            _dev_i32(token_dest, "token_dest", (self.T, self.k))
+        rc = _lib.topoep_dispatch_layout(
+            ctypes.byref(self.topo), token_dest.data_ptr() if t else None, self.T, self.k, send_counts.data_ptr(),
+            self.send_offsets.data_ptr(), self.token_slot.data_ptr() if t else None, self.status.data_ptr(),
+            self.ws_ptr, self.ws_bytes, _stream_ptr(stream, send_counts.device))
+        if rc != OK:
+            raise TopoepError("topoep_dispatch_layout", rc)
+        return self.send_offsets, self.token_slot
 
 
 def plan(topo: Topology, global_load, local_topk, replica_budget: int, stream=None, launch=None):

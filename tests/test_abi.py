@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert "topoep_plan" in names and "topoep_workspace_bytes" in names
-    assert len(names) == 6
+    assert len(names) == 10
 
 
 def test_library_exports_every_declared_symbol(tp):
@@ -154,3 +154,48 @@ def test_valid_calls_reach_the_launch(tp, solver):
     for stage in range(kernels, 3):
         assert tp._lib.topoep_plan_stage(stage, *args, ctypes.byref(launch)) == tp.EINVAL, stage
     assert tp._lib.topoep_plan_stage(4, *args, ctypes.byref(launch)) == tp.EINVAL
+
+
+def test_dispatch_workspace_and_host_checks(tp):
+    t = base(tp)
+    lw = tp.layout_workspace_bytes(t, 512, 2)
+    assert lw > 0 and lw % 256 == 0
+    assert tp.layout_workspace_bytes(t, 0, 2) > 0
+    pw = tp.workspace_bytes(t, 512, 2, 1)
+    assert tp.dispatch_workspace_bytes(t, 512, 2, 1) == pw + lw
+    out = ctypes.c_size_t(0)
+    assert tp._lib.topoep_layout_workspace_bytes(ctypes.byref(t), -1, 2, ctypes.byref(out)) == tp.EINVAL
+    assert tp._lib.topoep_layout_workspace_bytes(ctypes.byref(t), 8, 0, ctypes.byref(out)) == tp.EINVAL
+    big = base(tp, R=2048, G=8, E=2048)
+    assert tp._lib.topoep_layout_workspace_bytes(ctypes.byref(big), 8, 1, ctypes.byref(out)) == tp.ELIMIT
+    # layout: null send counts / offsets / workspace, small or misaligned workspace
+    L = tp._lib.topoep_dispatch_layout
+    assert L(ctypes.byref(t), 256, 512, 2, None, 1024, 2048, None, 4096, lw, None) == tp.EINVAL
+    assert L(ctypes.byref(t), 256, 512, 2, 512, None, 2048, None, 4096, lw, None) == tp.EINVAL
+    assert L(ctypes.byref(t), None, 512, 2, 512, 1024, 2048, None, 4096, lw, None) == tp.EINVAL
+    assert L(ctypes.byref(t), 256, 512, 2, 512, 1024, 2048, None, None, lw, None) == tp.EINVAL
+    assert L(ctypes.byref(t), 256, 512, 2, 512, 1024, 2048, None, 4096, lw - 256, None) == tp.EWORKSPACE
+    assert L(ctypes.byref(t), 256, 512, 2, 512, 1024, 2048, None, 4096 + 8, lw, None) == tp.EWORKSPACE
+    # plan + dispatch: nothing asked beyond the plan, a half-given layout, a small workspace
+    D = tp._lib.topoep_plan_dispatch
+    dw = tp.dispatch_workspace_bytes(t, 16, 2, 1)
+    assert D(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, None, None, None, 4096, 8192, dw,
+             None) == tp.EINVAL
+    assert D(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, None, 3072, None, 4096, 8192, dw,
+             None) == tp.EINVAL
+    assert D(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 2560, 3072, 3584, 4096, 8192, dw - 256,
+             None) == tp.EWORKSPACE
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="launches on placeholder pointers: only where no GPU is present")
+def test_valid_dispatch_calls_reach_the_launch(tp):
+    t = base(tp)
+    lw = tp.layout_workspace_bytes(t, 512, 2)
+    assert tp._lib.topoep_dispatch_layout(ctypes.byref(t), 256, 512, 2, 512, 1024, 2048, None, 4096, lw,
+                                          None) == tp.EHIP
+    dw = tp.dispatch_workspace_bytes(t, 16, 2, 1)
+    assert tp._lib.topoep_plan_dispatch(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 2560, 3072, 3584,
+                                        4096, 8192, dw, None) == tp.EHIP
+    # receive counts only
+    assert tp._lib.topoep_plan_dispatch(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 2560, None, None,
+                                        4096, 8192, dw, None) == tp.EHIP
