@@ -361,13 +361,72 @@ def run_bench(args):
         "roofline": roof,
         "input_generation_s": round(t_gen, 2),
     }
+    if not args.no_dispatch:
+        out["dispatch"] = bench_dispatch(torch, topoep, cfg, topo, planners, dev_inputs, args)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds, dev_inputs)
     return out
 
 
+def _graph_us(torch, enqueue, reps, per):
+    """Microseconds per unit of a HIP graph holding `enqueue()` (per units),
+    replayed reps times between events on the graph's stream."""
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        enqueue(stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(g, stream=stream):
+            enqueue(stream)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        g.replay()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            g.replay()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / (reps * per)
+
+
+def bench_dispatch(torch, topoep, cfg, topo, planners, dev_inputs, args):
+    """The dispatch side of the plan: the plan with receive counts and the
+    send-buffer layout (topoep_plan_dispatch) per layer, and the layout
+    kernel alone on each layer's destinations (its HBM roofline)."""
+    layers = len(planners)
+    dps = [topoep.DispatchPlanner(topo, cfg.T, cfg.k, cfg.N, device=dev_inputs[0][0].device)
+           for _ in range(layers)]
+
+    def plan_all(stream):
+        for d, (g, t) in zip(dps, dev_inputs):
+            d.plan(g, t, stream=stream)
+    per_layer = _graph_us(torch, plan_all, max(5, args.steps // 4), layers)
+    st = torch.stack([d.status for d in dps]).cpu().numpy()
+    if (st[:, 0] & ~topoep.ST_SELF_DIFF).any():
+        raise SystemExit("dispatch plan status bits set: %s" % np.unique(st[:, 0]))
+    lps = [topoep.LayoutPlanner(topo, cfg.T, cfg.k, device=dev_inputs[0][0].device) for _ in range(layers)]
+
+    def layout_all(stream):
+        for lp, p in zip(lps, planners):
+            lp.layout(p.token_dest, p.send_counts, stream=stream)
+    reps = max(1, args.stage_reps)
+    layout_us = _graph_us(torch, lambda s: [layout_all(s) for _ in range(reps)], 3, reps * layers)
+    n = cfg.T * cfg.k
+    nbytes = 8 * n + 4 * cfg.R + 4 * (cfg.R + 1)
+    achieved = nbytes / (layout_us * 1e-6) / 1e9
+    return {"plan_dispatch_latency_us_per_layer": per_layer,
+            "layout_kernel_avg_us": round(layout_us, 3),
+            "layout_roofline": {"bound": "hbm", "kernel": "layout_kernel", "achieved": achieved,
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                                "algorithmic_bytes_per_launch": nbytes}}
+
+
 def run_sweep(args):
-    """Histogram and reroute alone over synthetic id arrays of growing size,
+    """Histogram, reroute and send-buffer layout alone over synthetic id arrays of growing size,
     past the 256 MB Infinity Cache, with a fixed plan."""
     import torch
     from paper_2609_35481_amd import topoep
@@ -399,21 +458,26 @@ def run_sweep(args):
             torch.cuda.synchronize()
             st = int(pl.status[0].item())
             res = {}
-            for name, sid, bpa in (("hist", 0, 4), ("reroute", 2, 8)):
+            lp = topoep.LayoutPlanner(topo, T, k, device=dev)
+            runs = (("hist", lambda: pl.stage(0, gl, tk_d), 4), ("reroute", lambda: pl.stage(2, gl, tk_d), 8),
+                    ("layout", lambda: lp.layout(pl.token_dest, pl.send_counts), 8))
+            for name, fn, bpa in runs:
                 reps = 5 if n >= (1 << 26) else 20
                 a = torch.cuda.Event(enable_timing=True)
                 b = torch.cuda.Event(enable_timing=True)
-                pl.stage(sid, gl, tk_d)
+                fn()
                 a.record()
                 for _ in range(reps):
-                    pl.stage(sid, gl, tk_d)
+                    fn()
                 b.record()
                 torch.cuda.synchronize()
                 us = a.elapsed_time(b) * 1e3 / reps
                 res[name] = {"us": round(us, 2), "GB/s": round(bpa * n / us / 1e3, 1)}
+            if int(lp.status[0].item()) != 0:
+                raise SystemExit("layout status %d" % int(lp.status[0].item()))
             rows.append({"E": E, "ids": n, "status": st, **res})
             print(json.dumps(rows[-1]), flush=True)
-            del pl, tk_d, gl
+            del pl, lp, tk_d, gl
             torch.cuda.empty_cache()
     return rows
 
@@ -429,6 +493,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU baseline budget: half for one thread, a quarter for every core")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-dispatch", action="store_true", help="skip the dispatch-side measurement")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-max-log2", type=int, default=28)
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")

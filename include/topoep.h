@@ -237,23 +237,27 @@ int topoep_dispatch_layout(const topoep_topology *topo, const int32_t *token_des
                            const int32_t *send_counts, int32_t *send_offsets, int32_t *token_slot,
                            int32_t *status, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of device workspace topoep_plan_dispatch needs: the plan's
- * (default launch shape), rounded up to 256, plus the layout's. */
+/* Bytes of device workspace topoep_plan_dispatch needs (the plan's, default
+ * launch shape: the layout is computed inside the plan's kernels). */
 int topoep_dispatch_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k,
                                     int32_t replica_budget, size_t *bytes_out);
 
 /*
- * Enqueue one plan (as topoep_plan, default launch shape) and its dispatch
- * side:
+ * Enqueue one plan (as topoep_plan, default launch shape) with its dispatch
+ * side computed by the same kernels:
  *   recv_counts   device int32 out [R] or NULL: recv_counts[s] =
  *                 sum_e q[s][e][self], the assignments rank s sends to this
  *                 rank under the same plan (0 when no plan is made).
  *   send_offsets, token_slot: as topoep_dispatch_layout (both NULL to skip
  *                 the layout; recv_counts and the layout may not both be
- *                 skipped).
+ *                 skipped).  The slot count before each chunk of ids comes
+ *                 from the chunk's per-expert offsets and this rank's
+ *                 instance list (each expert's occurrences are dealt to its
+ *                 instances in occurrence order), so no second pass over
+ *                 the destinations is needed.
  * The workspace is one buffer of topoep_dispatch_workspace_bytes bytes
  * (256-byte aligned, zero-filled before its first call).  Return codes as
- * topoep_plan and topoep_dispatch_layout.
+ * topoep_plan.
  */
 int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
                          int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots,

@@ -76,7 +76,7 @@ constexpr uint32_t kIterLimit = 1u << 22;
 // ---------------------------------------------------------------- plan
 
 struct Plan {
-  int R, G, M, E, P, N, Neff, PN, I, self, MW, RW, nbits, cap1, nent_cap, QS;
+  int R, G, M, E, P, N, Neff, PN, I, self, MW, RW, nbits, rbits, cap1, nent_cap, QS;
   int cI, cX;
   int64_t S, W;
   int64_t n, chunk;
@@ -87,6 +87,8 @@ struct Plan {
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   int32_t *recv_out;   // receive counts [R], or null
+  int32_t *slot_out;   // send-buffer slot of every assignment [n], or null
+  int32_t *offs_out;   // send offsets [R + 1] (given with slot_out)
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
   uint32_t *pub, *flags, *ghist;   // one-launch plan: chunk counts, flags, histogram (E + 1 words)
@@ -160,7 +162,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
 
 // LDS layout of a chunk workgroup of the single-launch plan (nt threads).
 struct ChunkLds {
-  int wc, run, ptr, er, eend, gs, flag, words;
+  int wc, run, ptr, er, eend, gs, so, flag, words;
 };
 
 __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
@@ -172,6 +174,7 @@ __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
   l.er = o;   o += p.nent_cap;               //   instance rank
   l.eend = o; o += p.nent_cap;               //   cumulative share
   l.gs = o;   o += imax(nt, p.E);            // partial sums of the chunk's offsets
+  l.so = o;   o += p.R + 1 + (nt >> 6) + 1;  // send offsets and their scan scratch
   l.flag = o; o += 4;
   l.words = o;
   return l;
@@ -1483,6 +1486,86 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
   if (p.recv_out && !(gst & kNoPlan)) single_recv_counts(p, t);
 }
 
+// ---------------------------------------------------------------- send-buffer slots
+//
+// The send buffer groups the assignments by destination (ranks ascending,
+// row-major order inside one destination).  An assignment's slot is
+// offs[d] + (assignments to d before its tile) + (those of earlier waves of
+// the tile) + (its rank among its wave's earlier assignments to d).  The
+// count before a tile follows from the per-expert counts before it, with no
+// pass over earlier ids: expert e's occurrences are dealt to its instances
+// in occurrence order, instance j taking [end(j-1), end(j)), so
+// clamp(run[e] - end(j-1), 0, end(j) - end(j-1)) of them went to j's rank.
+
+// offs[0..R) holds the send counts: it becomes their exclusive prefix with
+// the total at offs[R] (tmp: blockDim/64 + 1 words); `first` writes it out.
+__device__ void slot_offsets(const Plan &p, int *offs, int *tmp, bool first) {
+  lds_barrier();
+  offs[p.R] = block_excl_scan(offs, p.R, tmp);
+  if (first && p.offs_out)
+    for (int r = threadIdx.x; r <= p.R; r += blockDim.x) p.offs_out[r] = offs[r];
+}
+
+// excl[r] = assignments to rank r before the tile (run[e]: occurrences of e
+// before it; ptr/er/eend: this rank's instance list).  Ends with a barrier.
+__device__ void slot_before(const Plan &p, const int *run, const int *ptr, const int *er, const int *eend,
+                            int *excl) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int r = tid; r < p.R; r += nt) excl[r] = 0;
+  lds_barrier();
+  for (int e = tid; e < p.E; e += nt) {
+    const int re = run[e], j1 = ptr[e + 1];
+    int start = 0;
+    for (int j = ptr[e]; j < j1; ++j) {
+      const int end = eend[j];
+      const int c = imin(imax(re - start, 0), end - start);
+      if (c > 0 && (unsigned)er[j] < (unsigned)p.R) atomicAdd(&excl[er[j]], c);
+      start = end;
+    }
+  }
+  lds_barrier();
+}
+
+// Slots of one tile (destinations dv in registers; index order: wave, then
+// i, then lane); wcd: blockDim/64 * R words of scratch.
+template <int IPT>
+__device__ void slot_write(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi, const int *offs,
+                           const int *excl, int *wcd) {
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6, R = p.R;
+  int *mw = wcd + wave * R;
+  for (int r = lane; r < R; r += 64) mw[r] = 0;
+  wave_sync();
+  int lr[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const bool valid = wbase + i * 64 < hi && (unsigned)dv[i] < (unsigned)R;
+    const uint64_t peers = peer_mask(dv[i], valid, p.rbits);
+    const int c = valid ? mw[dv[i]] : 0;
+    lr[i] = c + __popcll(peers & lanemask_lt());
+    wave_sync();
+    if (valid && (peers & lanemask_lt()) == 0) mw[dv[i]] = c + __popcll(peers);
+    wave_sync();
+  }
+  lds_barrier();
+  for (int r = tid; r < R; r += nt) {
+    int run = 0;
+    for (int w = 0; w < nw; ++w) {
+      const int t = wcd[w * R + r];
+      wcd[w * R + r] = run;
+      run += t;
+    }
+  }
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    if (idx < hi) {
+      const int d = dv[i];
+      p.slot_out[idx] = (unsigned)d < (unsigned)R ? offs[d] + excl[d] + mw[d] + lr[i] : -1;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- reroute
 
 template <int IPT>
@@ -1495,6 +1578,9 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   int *ptr = wc + nw * E;            // E + 1
   int *er = ptr + E + 1;             // nent_cap: instance rank
   int *eend = er + p.nent_cap;       // nent_cap: cumulative share
+  int *wcd = eend + p.nent_cap;      // nw * R: send-buffer slots: per-wave counts
+  int *excl = wcd + nw * p.R;        // R: assignments per rank before the tile
+  int *so = excl + p.R;              // R + 1 + nw + 1: send offsets, scan scratch
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   const int64_t lo = (int64_t)b * p.chunk;
@@ -1502,7 +1588,15 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   const uint32_t fin = p.ctrl[kCtrlFinal];
   if (fin & (kNoPlan | TOPOEP_ST_SYNC)) {
     for (int64_t i = lo + tid; i < hi; i += nt) p.dest_out[i] = -1;
+    if (p.slot_out)
+      for (int64_t i = lo + tid; i < hi; i += nt) p.slot_out[i] = -1;
+    if (b == 0 && p.offs_out)
+      for (int r = tid; r <= p.R; r += nt) p.offs_out[r] = 0;
     return;
+  }
+  if (p.offs_out) {
+    for (int r = tid; r < p.R; r += nt) so[r] = p.send_out[r];
+    slot_offsets(p, so, so + p.R + 1, b == 0);
   }
   for (int e = tid; e < E; e += nt) run[e] = p.offsets[(int64_t)b * E + e];
   for (int e = tid; e <= E; e += nt) {
@@ -1519,6 +1613,8 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   int *mywc = wc + wave * E;
   const int64_t tile = (int64_t)nt * IPT;
   for (int64_t base = lo; base < hi; base += tile) {
+    // run[e] counts e's occurrences before this tile
+    if (p.slot_out) slot_before(p, run, ptr, er, eend, excl);
     for (int e = lane; e < E; e += 64) mywc[e] = 0;
     wave_sync();
     const int64_t wbase = base + (int64_t)wave * 64 * IPT + lane;
@@ -1550,11 +1646,12 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
       run[e] = s;
     }
     __syncthreads();
+    int dv[IPT];
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int64_t idx = wbase + i * 64;
+      int dest = -1;
       if (idx < hi) {
-        int dest = -1;
         if ((unsigned)ev[i] < (unsigned)E) {
           const int rho = mywc[ev[i]] + lr[i];
           const int j1 = ptr[ev[i] + 1];
@@ -1567,7 +1664,9 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
         }
         p.dest_out[idx] = dest;
       }
+      dv[i] = dest;
     }
+    if (p.slot_out) slot_write<IPT>(p, dv, wbase, hi, so, excl, wcd);
     __syncthreads();
   }
 }
@@ -1823,7 +1922,7 @@ template <int IPT>
 __device__ void fused_chunk(const Plan &p, int b, int *sm) {
   const ChunkLds l = chunk_lds(p, blockDim.x);
   int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr, *er = sm + l.er, *eend = sm + l.eend;
-  int *gs = sm + l.gs, *flag = sm + l.flag;
+  int *gs = sm + l.gs, *so = sm + l.so, *flag = sm + l.flag;
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int E = p.E;
   const int64_t lo = (int64_t)b * p.chunk;
@@ -1920,22 +2019,30 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
         eend[i] = xv;
       }
     }
+    if (p.offs_out)
+      for (int r = tid; r < p.R; r += nt) so[r] = p.send_out[r];
   }
   if (!ok || (fin & (kNoPlan | TOPOEP_ST_SYNC))) {
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int64_t idx = wbase + i * 64;
-      if (idx < hi) p.dest_out[idx] = -1;
+      if (idx < hi) {
+        p.dest_out[idx] = -1;
+        if (p.slot_out) p.slot_out[idx] = -1;
+      }
     }
+    if (b == 0 && p.offs_out)
+      for (int r = tid; r <= p.R; r += nt) p.offs_out[r] = 0;
     if (!ok && tid == 0) atomicOr(reinterpret_cast<unsigned *>(p.status_out), TOPOEP_ST_SYNC);
     return;
   }
   __syncthreads();
+  int dv[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
     const int64_t idx = wbase + i * 64;
+    int dest = -1;
     if (idx < hi) {
-      int dest = -1;
       if ((unsigned)ev[i] < (unsigned)E) {
         const int rho = run[ev[i]] + wc[wave * E + ev[i]] + lr[i];
         const int j1 = ptr[ev[i] + 1];
@@ -1948,18 +2055,52 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
       }
       p.dest_out[idx] = dest;
     }
+    dv[i] = dest;
+  }
+  if (p.offs_out) {
+    // send-buffer slots (wc and gs are free once every wave has its
+    // destinations; run[e] counts e's occurrences before this chunk)
+    slot_offsets(p, so, so + p.R + 1, b == 0);
+    if (p.slot_out) {
+      slot_before(p, run, ptr, er, eend, gs);
+      slot_write<IPT>(p, dv, wbase, hi, so, gs, wc);
+    }
   }
 }
 
 // The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold
 // the ids; all are resident at once (nb <= kMaxFusedBlocks) and every wait
 // is bounded.
+typedef const __attribute__((address_space(4))) Plan KernargPlan;
+
+// The plan's fields for one role of the one-launch kernel, loaded after the
+// role's branch from an opaque pointer to the kernel arguments: otherwise
+// the compiler loads every field either role uses at the kernel's entry and
+// keeps them all live, and the solver's scalar registers spill.  (The host
+// pass only type-checks this function.)
+__device__ inline Plan role_plan(const Plan &p) {
+#if __HIP_DEVICE_COMPILE__
+  (void)p;
+  KernargPlan *k = (KernargPlan *)(__builtin_amdgcn_kernarg_segment_ptr());
+  asm volatile("" : "+s"(k));
+  return *k;
+#else
+  return p;
+#endif
+}
+
 template <int IPT>
 __global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
   extern __shared__ int64_t smem_f[];
   int *sm = reinterpret_cast<int *>(smem_f);
-  if (blockIdx.x == 0) fused_solver(p, sm);
-  else fused_chunk<IPT>(p, blockIdx.x - 1, sm);
+  (void)p;
+  if (blockIdx.x == 0) {
+    const Plan q = role_plan(p);
+    fused_solver(q, sm);
+  } else {
+    const Plan q = role_plan(p);
+    fused_chunk<IPT>(q, blockIdx.x - 1, sm);
+  }
 }
 
 // Same launch shape, empty body: the launch floor of a plan's kernel.
@@ -2007,6 +2148,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.MW = (q.M + 31) / 32;
   q.RW = (R + 31) / 32;
   q.nbits = ceil_log2(E);
+  q.rbits = ceil_log2(R);
   q.cap1 = G * q.Neff;
   q.nent_cap = E + R * q.Neff;
   q.QS = R | 1;   // odd row stride of the q columns: no LDS bank conflicts
@@ -2108,7 +2250,8 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.n_solvers = s.mode == 1 ? 1 : imin(q.M, kMaxSolveGroups);
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
-  s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap) * 4;
+  s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap +
+                   (size_t)R * (s.bt / 64 + 2) + 1 + s.bt / 64 + 1) * 4;
   s.lds_fused = 0;
   if (s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
   }
@@ -2254,7 +2397,7 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
             const int32_t *local_topk, int32_t T, int32_t k, int32_t N, int32_t *replica_slots,
             int32_t *token_dest, int32_t *send_counts, int32_t *status, void *workspace,
             size_t workspace_bytes, void *stream, const topoep_launch *launch,
-            int32_t *recv_counts = nullptr) {
+            int32_t *recv_counts = nullptr, int32_t *send_offsets = nullptr, int32_t *token_slot = nullptr) {
   Plan p;
   Shape s;
   size_t need = 0;
@@ -2273,6 +2416,8 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
   p.send_out = send_counts;
   p.status_out = status;
   p.recv_out = recv_counts;
+  p.offs_out = send_offsets;
+  p.slot_out = send_offsets ? token_slot : nullptr;   // (null when T == 0: offsets only)
   set_attrs();
   hipStream_t st = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
@@ -2354,14 +2499,7 @@ int topoep_plan(const topoep_topology *topo, const int32_t *global_load, const i
 
 int topoep_dispatch_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
                                     size_t *bytes_out) {
-  if (!bytes_out) return TOPOEP_EINVAL;
-  size_t plan_bytes = 0, layout_bytes = 0;
-  int rc = topoep_workspace_bytes_ex(topo, T, k, replica_budget, nullptr, &plan_bytes);
-  if (rc != TOPOEP_OK) return rc;
-  rc = topoep_layout_workspace_bytes(topo, T, k, &layout_bytes);
-  if (rc != TOPOEP_OK) return rc;
-  *bytes_out = align256(plan_bytes) + layout_bytes;
-  return TOPOEP_OK;
+  return topoep_workspace_bytes_ex(topo, T, k, replica_budget, nullptr, bytes_out);
 }
 
 int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
@@ -2369,22 +2507,11 @@ int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load
                          int32_t *token_dest, int32_t *send_counts, int32_t *recv_counts, int32_t *send_offsets,
                          int32_t *token_slot, int32_t *status, void *workspace, size_t workspace_bytes,
                          void *stream) {
-  size_t plan_bytes = 0, layout_bytes = 0, total = 0;
-  int rc = topoep_workspace_bytes_ex(topo, T, k, replica_budget, nullptr, &plan_bytes);
-  if (rc != TOPOEP_OK) return rc;
-  rc = topoep_dispatch_workspace_bytes(topo, T, k, replica_budget, &total);
-  if (rc != TOPOEP_OK) return rc;
   const bool layout = send_offsets != nullptr || token_slot != nullptr;
   if (layout && (!send_offsets || (T > 0 && !token_slot))) return TOPOEP_EINVAL;
   if (!recv_counts && !layout) return TOPOEP_EINVAL;
-  if (!workspace) return TOPOEP_EINVAL;
-  if (workspace_bytes < total || (reinterpret_cast<uintptr_t>(workspace) & 255)) return TOPOEP_EWORKSPACE;
-  layout_bytes = total - align256(plan_bytes);
-  rc = enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
-               status, workspace, plan_bytes, stream, nullptr, recv_counts);
-  if (rc != TOPOEP_OK || !layout) return rc;
-  return topoep_dispatch_layout(topo, token_dest, T, k, send_counts, send_offsets, token_slot, status,
-                                static_cast<char *>(workspace) + align256(plan_bytes), layout_bytes, stream);
+  return enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
+                 status, workspace, workspace_bytes, stream, nullptr, recv_counts, send_offsets, token_slot);
 }
 
 int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t *global_load,

@@ -162,7 +162,7 @@ def test_dispatch_workspace_and_host_checks(tp):
     assert lw > 0 and lw % 256 == 0
     assert tp.layout_workspace_bytes(t, 0, 2) > 0
     pw = tp.workspace_bytes(t, 512, 2, 1)
-    assert tp.dispatch_workspace_bytes(t, 512, 2, 1) == pw + lw
+    assert tp.dispatch_workspace_bytes(t, 512, 2, 1) == pw
     out = ctypes.c_size_t(0)
     assert tp._lib.topoep_layout_workspace_bytes(ctypes.byref(t), -1, 2, ctypes.byref(out)) == tp.EINVAL
     assert tp._lib.topoep_layout_workspace_bytes(ctypes.byref(t), 8, 0, ctypes.byref(out)) == tp.EINVAL

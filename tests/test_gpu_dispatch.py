@@ -112,6 +112,23 @@ def test_random_tiny(seed):
     check((t.R, t.G, t.E, s, t.cI, t.cX, t.S, t.W, t.N, omega, tk), "tiny seed %d" % seed)
 
 
+def test_many_ids_three_kernels():
+    """4 M assignments: too many for the one-launch plan, so the histogram,
+    solver and reroute kernels run, each reroute workgroup over several
+    tiles (the slot counts before each tile come from its running per-expert
+    offsets)."""
+    cfg = workload.get("dsv3")
+    rng = np.random.default_rng(17)
+    T, k = 1 << 19, 8
+    p = workload.generate.zipf_weights(cfg.E, 1.0)
+    tk = rng.choice(cfg.E, size=(T, k), p=p).astype(np.int32)
+    gl = rng.integers(0, 2000, size=(cfg.R, cfg.E)).astype(np.int32)
+    gl[0] = np.bincount(tk.ravel(), minlength=cfg.E)
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    assert topoep.plan_shape(topo, T, k, cfg.N).kernels == 3
+    check((cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W, cfg.N, gl, tk), "4M ids")
+
+
 def test_refused_plan_has_no_receive_counts():
     cfg = workload.get("tiny")
     gl, tk = workload.make_layer(cfg, 0, 0, 0)
