@@ -572,20 +572,23 @@ __device__ inline int route_self_q(const Plan &p, int d, int e, int w, const uin
 // q[s][e][self].  With full, every source's q of those instances is in
 // qcol (and reflects the refinement); otherwise the routing rule gives it
 // from omega(s, e).
+// One thread per (source, instance); acc: R words of LDS scratch.
 template <class OmegaOf>
 __device__ void write_recv_counts(const Plan &p, int i0, const int *e_of, const int *qcol, bool full,
-                                  const uint32_t *mask, const FastDiv *fdt, OmegaOf omega_of) {
+                                  const uint32_t *mask, const FastDiv *fdt, OmegaOf omega_of, int *acc) {
+  const int tid = threadIdx.x, nt = blockDim.x, R = p.R, PN = p.PN;
   const int ds = (int)fdiv((uint32_t)p.self, p.fG);
-  for (int s = threadIdx.x; s < p.R; s += blockDim.x) {
-    const int dsrc = (int)fdiv((uint32_t)s, p.fG);
-    int sum = 0;
-    for (int pos = 0; pos < p.PN; ++pos) {
-      const int i = i0 + pos, e = e_of[i];
-      if (e < 0) continue;
-      sum += full ? qcol[i * p.QS + s] : route_q(p, ds, e, omega_of(s, e), dsrc, mask, fdt);
-    }
-    p.recv_out[s] = sum;
+  for (int s = tid; s < R; s += nt) acc[s] = 0;
+  lds_barrier();
+  for (int x = tid; x < R * PN; x += nt) {
+    const int s = (int)fdiv((uint32_t)x, p.fPN), i = i0 + x - s * PN, e = e_of[i];
+    if (e < 0) continue;
+    const int q = full ? qcol[i * p.QS + s]
+                       : route_q(p, ds, e, omega_of(s, e), (int)fdiv((uint32_t)s, p.fG), mask, fdt);
+    if (q) atomicAdd(&acc[s], q);
   }
+  lds_barrier();
+  for (int s = tid; s < R; s += nt) p.recv_out[s] = acc[s];
 }
 
 // full(d): whether every source's q is needed for domain d's instances.  A
@@ -1174,7 +1177,8 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
     }
     if (p.recv_out && d == (int)fdiv((uint32_t)p.self, p.fG))
       write_recv_counts(p, (p.self - d * G) * PN, e_of, qcol, full, mask, fdt,
-                        [&](int s, int e) { return s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]; });
+                        [&](int s, int e) { return s == p.self ? hs[e] : p.gl[(int64_t)s * E + e]; },
+                        reinterpret_cast<int *>(ck));
     lds_barrier();
   }
   if (tid == 0 && (flags || !synced)) atomicOr(&p.ctrl[kCtrlStatus], flags | (synced ? 0u : TOPOEP_ST_SYNC));
@@ -1449,8 +1453,25 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
 __device__ void single_recv_counts(const Plan &p, const SingleState &t) {
   const int ds = (int)fdiv((uint32_t)p.self, p.fG), E = p.E;
   const int *om = t.om;
+  // (hs, the histogram, is no longer needed: it is the scratch)
   write_recv_counts(p, ds * p.I + (p.self - ds * p.G) * p.PN, t.e_of, t.qcol, t.dfree[ds] != 0, t.mask, t.fdt,
-                    [&](int s, int e) { return om[s * E + e]; });
+                    [&](int s, int e) { return om[s * E + e]; }, t.hs);
+}
+
+// Send offsets of the one-launch plan (exclusive prefix of the send counts
+// sendl, total at [R]) by wave 0, for the caller and for the chunks.
+__device__ void solver_send_offsets(const Plan &p, const int *sendl) {
+  if (threadIdx.x >= 64) return;
+  const int lane = threadIdx.x, R = p.R;
+  const int per = (R + 63) / 64, lo = imin(R, lane * per), hi = imin(R, lo + per);
+  int sum = 0;
+  for (int r = lo; r < hi; ++r) sum += sendl[r];
+  int run = wave_incl_scan(sum) - sum;
+  for (int r = lo; r < hi; ++r) {
+    p.offs_out[r] = run;
+    run += sendl[r];
+  }
+  if (lane == 63) p.offs_out[R] = run;
 }
 
 // The same steps with every domain's state in the LDS of one CU; each
@@ -1851,6 +1872,7 @@ __device__ void fused_solver(const Plan &p, int *sm) {
   }
   // receive counts of a plan that was made (a refused one wrote zeros)
   if (planned && p.recv_out) single_recv_counts(p, t);
+  if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
   // release: every output, the instance list and the final status before
   // the flags
   drain_then_barrier();
@@ -1907,6 +1929,64 @@ __device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
   }
   __syncthreads();
   return *flag != 0;
+}
+
+// Send-buffer slots of a chunk of the one-launch plan, with three barriers:
+// the counts per rank before the chunk (from run[e] and the instance list,
+// into excl, zeroed with the instance-list load) and each wave's ranks by
+// destination (its own row of wc, stride E, which only it read before) are
+// made together; the wave offsets per rank come from one 16-lane scan per
+// rank (lane w of a row holds wave w's count); then the slots.  offs: the
+// send offsets.
+template <int IPT>
+__device__ void chunk_slots(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi, const int *run,
+                            const int *ptr, const int *er, const int *eend, const int *offs, int *excl, int *wc) {
+  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
+  const int R = p.R, E = p.E;
+  for (int e = tid; e < E; e += nt) {
+    const int re = run[e], j1 = ptr[e + 1];
+    int start = 0;
+    for (int j = ptr[e]; j < j1; ++j) {
+      const int end = eend[j];
+      const int c = imin(imax(re - start, 0), end - start);
+      if (c > 0 && (unsigned)er[j] < (unsigned)R) atomicAdd(&excl[er[j]], c);
+      start = end;
+    }
+  }
+  int *mw = wc + wave * E;
+  wave_sync();
+  for (int r = lane; r < R; r += 64) mw[r] = 0;
+  wave_sync();
+  int lr[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const bool valid = wbase + i * 64 < hi && (unsigned)dv[i] < (unsigned)R;
+    const uint64_t peers = peer_mask(dv[i], valid, p.rbits);
+    const int c = valid ? mw[dv[i]] : 0;
+    lr[i] = c + __popcll(peers & lanemask_lt());
+    wave_sync();
+    if (valid && (peers & lanemask_lt()) == 0) mw[dv[i]] = c + __popcll(peers);
+    wave_sync();
+  }
+  lds_barrier();
+  // lane w of the row of rank r: wave w's count, scanned across the row
+  const int rows = R * 16, span = (rows + 63) & ~63;
+  for (int t = tid; t < span; t += nt) {
+    const int r = t >> 4, w = t & 15;
+    const bool in = t < rows && w < nw;
+    const int c = in ? wc[w * E + r] : 0;
+    const int incl = row16_incl_scan(c);
+    if (in) wc[w * E + r] = incl - c;
+  }
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    if (idx < hi) {
+      const int d = dv[i];
+      p.slot_out[idx] = (unsigned)d < (unsigned)R ? offs[d] + excl[d] + mw[d] + lr[i] : -1;
+    }
+  }
 }
 
 // Chunk role (workgroup 1 + b): ids [b * chunk, (b + 1) * chunk) stay in
@@ -2019,8 +2099,14 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
         eend[i] = xv;
       }
     }
-    if (p.offs_out)
-      for (int r = tid; r < p.R; r += nt) so[r] = p.send_out[r];
+    if (p.slot_out) {
+      // the send offsets (the solver wrote them) in the same round trip;
+      // the per-rank counts before this chunk start from zero
+      for (int r = tid; r < p.R; r += nt) {
+        so[r] = p.offs_out[r];
+        gs[r] = 0;
+      }
+    }
   }
   if (!ok || (fin & (kNoPlan | TOPOEP_ST_SYNC))) {
 #pragma unroll
@@ -2057,15 +2143,7 @@ __device__ void fused_chunk(const Plan &p, int b, int *sm) {
     }
     dv[i] = dest;
   }
-  if (p.offs_out) {
-    // send-buffer slots (wc and gs are free once every wave has its
-    // destinations; run[e] counts e's occurrences before this chunk)
-    slot_offsets(p, so, so + p.R + 1, b == 0);
-    if (p.slot_out) {
-      slot_before(p, run, ptr, er, eend, gs);
-      slot_write<IPT>(p, dv, wbase, hi, so, gs, wc);
-    }
-  }
+  if (p.slot_out) chunk_slots<IPT>(p, dv, wbase, hi, run, ptr, er, eend, so, gs, wc);
 }
 
 // The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold

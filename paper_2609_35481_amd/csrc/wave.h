@@ -94,6 +94,15 @@ __device__ inline int wave_incl_scan(int x) {
   return x;
 }
 
+// Inclusive prefix sum inside each row of 16 lanes.
+__device__ inline int row16_incl_scan(int x) {
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+  x += (int)__builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+  return x;
+}
+
 __device__ inline int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
 __device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t b1, uint64_t b2,
