@@ -452,8 +452,12 @@ def run_sweep(args):
             gl = torch.randint(0, 1000, (R, E), dtype=torch.int32, device=dev)
             gl[0] = hist
             topo = topoep.topology(R, G, E, 0, 1, 8, 4096, 9 << 20)
-            # the three-kernel path, so the histogram and reroute kernels run alone
-            pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_SINGLE))
+            # the three-kernel path, so the histogram and reroute kernels run
+            # alone (the per-domain solver where one workgroup's LDS is too small)
+            try:
+                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_SINGLE))
+            except topoep.TopoepError:
+                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_PER_DOMAIN))
             pl.plan(gl, tk_d)
             torch.cuda.synchronize()
             st = int(pl.status[0].item())

@@ -13,8 +13,9 @@
 //     over up to 64 predecessors at a time: wave 0 waits for their flags in
 //     parallel and stops at the nearest one whose inclusive prefix is
 //     published (flag 2), the whole workgroup sums their counts per
-//     destination, and the workgroup publishes its own inclusive prefix
-//     (flag 2).  Workgroup 0 publishes its counts as its inclusive prefix;
+//     destination, and (when the grid is longer than one window plus
+//     workgroup 0) the workgroup publishes its own inclusive prefix (flag
+//     2).  Workgroup 0 publishes its counts as its inclusive prefix;
 //   - slot = send_offsets[dest] + (earlier workgroups) + (earlier waves) +
 //     (rank in the wave).
 // The waits are bounded and only on lower workgroup indices, which are
@@ -54,9 +55,9 @@ struct Layout {
 
 // LDS words: per-wave counts (then offsets) [nw][R], the workgroup's counts
 // [R], the exclusive prefix over earlier workgroups [R], send offsets
-// [R + 1], scan scratch and broadcast words.
+// [R + 1] and broadcast words.
 struct LayoutLds {
-  int wc, agg, excl, offs, tmp, misc, words;
+  int wc, agg, excl, offs, misc, words;
 };
 
 __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
@@ -66,7 +67,6 @@ __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
   l.agg = o; o += R;
   l.excl = o; o += R;
   l.offs = o; o += R + 1;
-  l.tmp = o; o += nt / 64 + 1;
   l.misc = o; o += 8;
   l.words = o;
   return l;
@@ -79,10 +79,13 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
   const int b = blockIdx.x;
   const LayoutLds l = layout_lds(R, nt);
   int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs;
-  int *tmp = lsm + l.tmp, *misc = lsm + l.misc;
+  int *misc = lsm + l.misc;
   const int64_t lo = (int64_t)b * L.chunk;
   const int64_t hi = lo + L.chunk < L.n ? lo + L.chunk : L.n;
   const int64_t wbase = lo + (int64_t)wave * 64 * IPT + lane;
+  // workgroups whose look-back window reaches workgroup 0 never need the
+  // inclusive prefix of another one
+  const bool publish_incl = L.nb > kLayoutWindow + 1;
 
   int dv[IPT], lr[IPT];
 #pragma unroll
@@ -90,19 +93,16 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     const int64_t idx = wbase + i * 64;
     dv[i] = idx < hi ? L.dest[idx] : -1;
   }
-  // send offsets (exclusive prefix of the plan's send counts)
-  for (int r = tid; r < R; r += nt) offs[r] = L.send[r];
-  for (int r = lane; r < R; r += 64) wc[wave * R + r] = 0;
-  for (int r = tid; r < R; r += nt) excl[r] = 0;
+  for (int r = tid; r < R; r += nt) {
+    offs[r] = L.send[r];
+    excl[r] = 0;
+  }
   if (tid < 8) misc[tid] = 0;
-  lds_barrier();
-  offs[R] = block_excl_scan(offs, R, tmp);
-  if (b == 0 && L.offs_out)
-    for (int r = tid; r <= R; r += nt) L.offs_out[r] = offs[r];
-
   // rank of each assignment among the wave's earlier ones with the same
-  // destination (index order: i, then lane)
+  // destination (index order: i, then lane); each wave owns its row of wc
   int *mywc = wc + wave * R;
+  for (int r = lane; r < R; r += 64) mywc[r] = 0;
+  wave_sync();
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
     const bool valid = (unsigned)dv[i] < (unsigned)R;
@@ -114,21 +114,41 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     wave_sync();
   }
   lds_barrier();
-  // per destination: offsets of the waves, the workgroup's counts
-  for (int r = tid; r < R; r += nt) {
-    int sum = 0;
-    for (int w = 0; w < nw; ++w) {
-      const int c = wc[w * R + r];
-      wc[w * R + r] = sum;
-      sum += c;
+  // per destination: offsets of the waves (one 16-lane scan per rank, lane w
+  // holding wave w's count) and the workgroup's count (the row's total)
+  {
+    const int rows = R * 16, span = (rows + 63) & ~63;
+    for (int t = tid; t < span; t += nt) {
+      const int r = t >> 4, w = t & 15;
+      const bool in = t < rows && w < nw;
+      const int c = in ? wc[w * R + r] : 0;
+      const int incl = row16_incl_scan(c);
+      if (in) wc[w * R + r] = incl - c;
+      if (t < rows && w == 15) {
+        agg[r] = incl;
+        L.agg[(int64_t)b * R + r] = (uint32_t)incl;
+        if (b == 0) L.incl[r] = (uint32_t)incl;
+      }
     }
-    agg[r] = sum;
-    L.agg[(int64_t)b * R + r] = (uint32_t)sum;
-    if (b == 0) L.incl[r] = (uint32_t)sum;
+  }
+  // send offsets (exclusive prefix of the send counts) by wave 0
+  if (wave == 0) {
+    const int per = (R + 63) / 64, a0 = imin(R, lane * per), a1 = imin(R, a0 + per);
+    int sum = 0;
+    for (int r = a0; r < a1; ++r) sum += offs[r];
+    int run = wave_incl_scan(sum) - sum;
+    for (int r = a0; r < a1; ++r) {
+      const int c = offs[r];
+      offs[r] = run;
+      run += c;
+    }
+    if (lane == 63) offs[R] = run;
   }
   drain_then_barrier();
   if (tid == 0)
     __hip_atomic_store(L.flags + b, b == 0 ? 2u : 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (b == 0 && L.offs_out)
+    for (int r = tid; r <= R; r += nt) L.offs_out[r] = offs[r];
 
   // look-back over the workgroups before b
   bool ok = true;
@@ -180,11 +200,20 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     if (found) break;
     jhi = stop - 1;
   }
-  if (b > 0) {
+  if (b > 0 && publish_incl) {
     for (int r = tid; r < R; r += nt) L.incl[(int64_t)b * R + r] = (uint32_t)(excl[r] + agg[r]);
     drain_then_barrier();
     if (tid == 0)
       __hip_atomic_store(L.flags + b, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int64_t idx = wbase + i * 64;
+    if (idx < hi) {
+      const int d = dv[i];
+      const bool valid = ok && (unsigned)d < (unsigned)R;
+      L.slot_out[idx] = valid ? offs[d] + excl[d] + wc[wave * R + d] + lr[i] : -1;
+    }
   }
   // this workgroup has read every flag it needs: the last one to get here
   // clears them all for the next call
@@ -198,16 +227,6 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     for (int j = tid; j < L.nb; j += nt)
       __hip_atomic_store(L.flags + j, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (tid == 0) __hip_atomic_store(L.ctrl, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-
-#pragma unroll
-  for (int i = 0; i < IPT; ++i) {
-    const int64_t idx = wbase + i * 64;
-    if (idx < hi) {
-      const int d = dv[i];
-      const bool valid = ok && (unsigned)d < (unsigned)R;
-      L.slot_out[idx] = valid ? offs[d] + excl[d] + wc[wave * R + d] + lr[i] : -1;
-    }
   }
 }
 
