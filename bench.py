@@ -363,6 +363,8 @@ def run_bench(args):
     }
     if not args.no_dispatch:
         out["dispatch"] = bench_dispatch(torch, topoep, cfg, topo, planners, dev_inputs, args)
+    if not args.no_gather:
+        out["replica_gather"] = bench_gather(torch, topoep, cfg, topo, planners)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds, dev_inputs)
     return out
@@ -391,6 +393,46 @@ def _graph_us(torch, enqueue, reps, per):
         b.record(stream)
     torch.cuda.synchronize()
     return a.elapsed_time(b) * 1e3 / (reps * per)
+
+
+def bench_gather(torch, topoep, cfg, topo, planners, reps=20):
+    """Replica-slot parameter gather after the first layer's plan: rank 0's
+    slots receive their experts' bf16 parameters (||W_e|| bytes each) from a
+    buffer holding every expert's; against a plain device copy of the same
+    bytes."""
+    dev = planners[0].replica_slots.device
+    slots = planners[0].replica_slots
+    n_copied = int((slots[0] >= 0).sum().item())
+    elems = cfg.W // 2
+    params = torch.empty((cfg.E, elems), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((cfg.N, elems), dtype=torch.bfloat16, device=dev)
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    topoep.gather_replicas(topo, slots, params, out)
+    a.record()
+    for _ in range(reps):
+        topoep.gather_replicas(topo, slots, params, out)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1e3 / reps
+    moved = 2 * n_copied * cfg.W
+    src = params[:max(n_copied, 1)].view(-1)
+    dst = out[:max(n_copied, 1)].view(-1)
+    dst.copy_(src)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    copy_us = a.elapsed_time(b) * 1e3 / reps
+    del params, out
+    torch.cuda.empty_cache()
+    achieved = moved / (us * 1e-6) / 1e9
+    return {"slots_copied": n_copied, "bytes_per_expert": cfg.W, "gather_us": round(us, 2),
+            "device_copy_us": round(copy_us, 2),
+            "roofline": {"bound": "hbm", "kernel": "gather_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": moved},
+            "device_copy_GBps": moved / (copy_us * 1e-6) / 1e9}
 
 
 def bench_dispatch(torch, topoep, cfg, topo, planners, dev_inputs, args):
@@ -498,6 +540,7 @@ def main():
                     help="CPU baseline budget: half for one thread, a quarter for every core")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dispatch", action="store_true", help="skip the dispatch-side measurement")
+    ap.add_argument("--no-gather", action="store_true", help="skip the replica-slot gather measurement")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-max-log2", type=int, default=28)
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")

@@ -265,6 +265,34 @@ int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load
                          int32_t *send_offsets, int32_t *token_slot, int32_t *status, void *workspace,
                          size_t workspace_bytes, void *stream);
 
+/*
+ * Replica-slot parameter gather (Section 3.2): once the plan names the
+ * expert of each of this rank's replica slots, the slot receives a copy of
+ * that expert's parameters.  On one GPU the parameters of every expert sit
+ * in one buffer and the gather is a device copy in slot order (one kernel,
+ * HBM-bound).
+ *
+ *   topo           R, E and self_rank are read.
+ *   replica_budget N_slot (the plan's).
+ *   replica_slots  device int32 [R, N_slot]: a plan's replica slots; row
+ *                  self_rank is used, -1 = empty (left untouched).
+ *   prev_slots     device int32 [N_slot] or NULL: the experts the slots held
+ *                  before; a slot whose expert is unchanged is not copied.
+ *   expert_params  device [E, bytes_per_expert] (any element type), 16-byte
+ *                  aligned.
+ *   bytes_per_expert  ||W_e|| in bytes, a multiple of 16 (0 copies nothing).
+ *   slot_params    device out [N_slot, bytes_per_expert], 16-byte aligned;
+ *                  slot j receives expert_params[replica_slots[self][j]].
+ *
+ * Host checks: TOPOEP_EINVAL for null pointers, R <= 0, E <= 0, self_rank
+ * outside [0, R), N_slot < 0, a size that is not a multiple of 16 or a
+ * misaligned buffer; TOPOEP_ELIMIT for N_slot > 65535; TOPOEP_EHIP when the
+ * launch fails.  Slots holding an id outside [0, E) are left untouched.
+ */
+int topoep_gather_replicas(const topoep_topology *topo, int32_t replica_budget, const int32_t *replica_slots,
+                           const int32_t *prev_slots, const void *expert_params, int64_t bytes_per_expert,
+                           void *slot_params, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -167,6 +167,23 @@ def layout_ref(R: int, token_dest, send_counts):
     return offs, slot
 
 
+def gather_ref(replica_slots, self_rank: int, expert_params, slot_params, prev_slots=None):
+    """Replica-slot parameter gather (Section 3.2), its plain definition:
+    slot j of rank self receives the parameters of expert
+    replica_slots[self, j]; an empty slot (-1, or any id outside [0, E)) and,
+    with prev_slots, a slot whose expert is unchanged keep their contents.
+    Returns a new array; the inputs are not modified."""
+    out = np.array(slot_params, copy=True)
+    E = expert_params.shape[0]
+    for j, e in enumerate(np.asarray(replica_slots)[self_rank]):
+        if not 0 <= e < E:
+            continue
+        if prev_slots is not None and prev_slots[j] == e:
+            continue
+        out[j] = expert_params[e]
+    return out
+
+
 def plan_cfg(cfg, global_load, local_topk, self_rank: int = 0, **kw):
     """Convenience: oracle plan for a ``workload.Config``."""
     topo = topology(cfg.R, cfg.G, cfg.E, self_rank, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)

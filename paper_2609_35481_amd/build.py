@@ -6,7 +6,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", "topoep.hip"), os.path.join(HERE, "csrc", "layout.hip")]
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("topoep.hip", "layout.hip", "gather.hip")]
 SRC = SRCS[0]
 LIB = os.path.join(HERE, "libtopoep.so")
 INCLUDE = os.path.join(ROOT, "include")

@@ -111,10 +111,13 @@ _lib.topoep_plan_dispatch.restype = ctypes.c_int
 _lib.topoep_plan_dispatch.argtypes = [ctypes.POINTER(Topology), _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp,
                                       _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
 
+_lib.topoep_gather_replicas.restype = ctypes.c_int
+_lib.topoep_gather_replicas.argtypes = [ctypes.POINTER(Topology), _i32, _vp, _vp, _vp, ctypes.c_int64, _vp, _vp]
+
 EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
            "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape",
            "topoep_layout_workspace_bytes", "topoep_dispatch_layout",
-           "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch")
+           "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch", "topoep_gather_replicas")
 
 
 def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
@@ -312,6 +315,33 @@ class LayoutPlanner:
         if rc != OK:
             raise TopoepError("topoep_dispatch_layout", rc)
         return self.send_offsets, self.token_slot
+
+
+def gather_replicas(topo: Topology, replica_slots, expert_params, slot_params, prev_slots=None, stream=None):
+    """Enqueue topoep_gather_replicas: slot j of rank topo.self_rank receives
+    expert_params[replica_slots[self, j]] (empty or unchanged slots are not
+    written).  expert_params [E, ...] and slot_params [N, ...] are CUDA
+    tensors of one dtype and one per-expert shape."""
+    R, E = topo.num_ranks, topo.num_experts
+    _dev_i32(replica_slots, "replica_slots")
+    if replica_slots.dim() != 2 or replica_slots.shape[0] != R:
+        raise ValueError("replica_slots must be [R, N]")
+    N = int(replica_slots.shape[1])
+    if not (expert_params.is_cuda and slot_params.is_cuda) or expert_params.dtype != slot_params.dtype:
+        raise TypeError("expert_params and slot_params must be CUDA tensors of one dtype")
+    if not (expert_params.is_contiguous() and slot_params.is_contiguous()):
+        raise ValueError("expert_params and slot_params must be contiguous")
+    if expert_params.shape[0] != E or slot_params.shape[0] != N or expert_params.shape[1:] != slot_params.shape[1:]:
+        raise ValueError("expert_params must be [E, ...] and slot_params [N, ...] with the same per-expert shape")
+    per = expert_params[0].numel() * expert_params.element_size() if E else 0
+    if prev_slots is not None:
+        _dev_i32(prev_slots, "prev_slots", (N,))
+    rc = _lib.topoep_gather_replicas(
+        ctypes.byref(topo), N, replica_slots.data_ptr(), prev_slots.data_ptr() if prev_slots is not None else None,
+        expert_params.data_ptr(), per, slot_params.data_ptr(), _stream_ptr(stream, replica_slots.device))
+    if rc != OK:
+        raise TopoepError("topoep_gather_replicas", rc)
+    return slot_params
 
 
 def plan(topo: Topology, global_load, local_topk, replica_budget: int, stream=None, launch=None):

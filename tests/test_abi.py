@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert "topoep_plan" in names and "topoep_workspace_bytes" in names
-    assert len(names) == 10
+    assert len(names) == 11
 
 
 def test_library_exports_every_declared_symbol(tp):
@@ -199,3 +199,20 @@ def test_valid_dispatch_calls_reach_the_launch(tp):
     # receive counts only
     assert tp._lib.topoep_plan_dispatch(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 2560, None, None,
                                         4096, 8192, dw, None) == tp.EHIP
+
+
+def test_gather_host_checks(tp):
+    t = base(tp)
+    G = tp._lib.topoep_gather_replicas
+    assert G(None, 1, 256, None, 512, 64, 1024, None) == tp.EINVAL
+    assert G(ctypes.byref(t), -1, 256, None, 512, 64, 1024, None) == tp.EINVAL
+    assert G(ctypes.byref(t), 1, None, None, 512, 64, 1024, None) == tp.EINVAL
+    assert G(ctypes.byref(t), 1, 256, None, None, 64, 1024, None) == tp.EINVAL
+    assert G(ctypes.byref(t), 1, 256, None, 512, 64, None, None) == tp.EINVAL
+    assert G(ctypes.byref(t), 1, 256, None, 512, 60, 1024, None) == tp.EINVAL     # not a multiple of 16
+    assert G(ctypes.byref(t), 1, 256, None, 520, 64, 1024, None) == tp.EINVAL     # misaligned
+    assert G(ctypes.byref(base(tp, self_rank=9)), 1, 256, None, 512, 64, 1024, None) == tp.EINVAL
+    assert G(ctypes.byref(t), 1 << 17, 256, None, 512, 64, 1024, None) == tp.ELIMIT
+    # nothing to copy: no launch, OK even on placeholder pointers
+    assert G(ctypes.byref(t), 0, None, None, None, 64, None, None) == tp.OK
+    assert G(ctypes.byref(t), 2, 256, None, 512, 0, 1024, None) == tp.OK

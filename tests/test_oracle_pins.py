@@ -349,3 +349,25 @@ def test_receive_counts_without_a_plan():
     out = run(t, om, topks[0], 0)
     assert out["status"] & oracle.ST_NEG_LOAD
     assert (out["recv_counts"] == 0).all()
+
+
+# ---------------------------------------------------------------- replica-slot gather
+
+def test_gather_matches_fancy_indexing_and_keeps_other_slots():
+    """The gather against numpy fancy indexing, on parameters whose every
+    row encodes its expert id, with empty slots and unchanged slots."""
+    rng = np.random.default_rng(4)
+    R, E, N, W = 6, 12, 3, 40
+    params = (np.arange(E, dtype=np.int64)[:, None] * 1000 + np.arange(W)).astype(np.int32)
+    slots = rng.integers(-1, E, size=(R, N)).astype(np.int32)
+    slots[2] = [5, -1, 11]
+    before = rng.integers(-9, 0, size=(N, W)).astype(np.int32)
+    out = oracle.gather_ref(slots, 2, params, before)
+    assert (out[0] == params[5]).all() and (out[2] == params[11]).all()
+    assert (out[1] == before[1]).all()              # empty slot untouched
+    assert (out[0] // 1000 == 5).all()
+    filled = slots[2] >= 0
+    assert (out[filled] == params[slots[2][filled]]).all()
+    # a slot whose expert is unchanged is not copied
+    out2 = oracle.gather_ref(slots, 2, params, before, prev_slots=np.array([5, 7, 3], np.int32))
+    assert (out2[0] == before[0]).all() and (out2[2] == params[11]).all()
