@@ -396,37 +396,47 @@ def _graph_us(torch, enqueue, reps, per):
 
 
 def bench_gather(torch, topoep, cfg, topo, planners, reps=20):
-    """Replica-slot parameter gather after the first layer's plan: rank 0's
-    slots receive their experts' bf16 parameters (||W_e|| bytes each) from a
-    buffer holding every expert's; against a plain device copy of the same
-    bytes."""
+    """Replica-slot parameter gather: rank 0's slots (as many as the first
+    layer's plan fills) receive bf16 experts of ||W_e|| bytes from a buffer
+    holding every expert's parameters.  Each repetition gathers a different
+    set of experts, so the sources are never resident in the 256 MB
+    Infinity Cache; a plain device copy of the same bytes from the same
+    rotating sources is timed beside it."""
     dev = planners[0].replica_slots.device
-    slots = planners[0].replica_slots
-    n_copied = int((slots[0] >= 0).sum().item())
+    n_copied = int((planners[0].replica_slots[0] >= 0).sum().item())
+    if n_copied == 0:
+        return {"slots_copied": 0}
     elems = cfg.W // 2
     params = torch.empty((cfg.E, elems), dtype=torch.bfloat16, device=dev)
     out = torch.empty((cfg.N, elems), dtype=torch.bfloat16, device=dev)
+    sets = []
+    for r in range(reps):
+        sl = torch.full((cfg.R, cfg.N), -1, dtype=torch.int32)
+        sl[0, :n_copied] = torch.tensor([(r * n_copied + j) % cfg.E for j in range(n_copied)], dtype=torch.int32)
+        sets.append(sl.to(dev))
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
-    topoep.gather_replicas(topo, slots, params, out)
+    topoep.gather_replicas(topo, sets[-1], params, out)
     a.record()
-    for _ in range(reps):
-        topoep.gather_replicas(topo, slots, params, out)
+    for sl in sets:
+        topoep.gather_replicas(topo, sl, params, out)
     b.record()
     torch.cuda.synchronize()
     us = a.elapsed_time(b) * 1e3 / reps
-    moved = 2 * n_copied * cfg.W
-    src = params[:max(n_copied, 1)].view(-1)
-    dst = out[:max(n_copied, 1)].view(-1)
-    dst.copy_(src)
     a.record()
-    for _ in range(reps):
-        dst.copy_(src)
+    for r in range(reps):
+        e0 = (r * n_copied) % cfg.E
+        if e0 + n_copied <= cfg.E:
+            out[:n_copied].copy_(params[e0:e0 + n_copied])
+        else:
+            for j in range(n_copied):
+                out[j].copy_(params[(e0 + j) % cfg.E])
     b.record()
     torch.cuda.synchronize()
     copy_us = a.elapsed_time(b) * 1e3 / reps
     del params, out
     torch.cuda.empty_cache()
+    moved = 2 * n_copied * cfg.W
     achieved = moved / (us * 1e-6) / 1e9
     return {"slots_copied": n_copied, "bytes_per_expert": cfg.W, "gather_us": round(us, 2),
             "device_copy_us": round(copy_us, 2),
