@@ -4,10 +4,15 @@
  * Follows the paper's Section 4 step by step, in its notation:
  *   O0  histogram of local_topk -> row self of Omega   (Section 3.1, Eq. 3)
  *   O1  domain demand D                                 (Section 4.1, Eq. 4)
- *   O2  inter-node placement with b = 2 D S - W         (Section 4.3, Eq. 9)
+ *   O2  inter-node placement with b = 2 D S - W_e       (Section 4.3, Eq. 9)
  *   O3  routing construction q, U, L                    (Section 4.3)
  *   O4  intra-node refinement, delta of Eq. 10          (Section 4.3)
  *   O5  send counts and per-assignment destinations     (Section 4.2, q)
+ *
+ * The cost c(s, r) is the two-level one of the topology (0, cost_intra,
+ * cost_inter) or, in topoep_plan_ref_general, any symmetric nonnegative
+ * matrix with a zero diagonal (the full model of Section 4.1), and ||W_e||
+ * one size for every expert or one per expert.
  *
  * Where the paper leaves a choice open, the readings below are used; each is
  * repeated at the step it concerns.
@@ -44,13 +49,21 @@
 typedef struct {
   int R, G, M, E, P, N, self;
   int64_t cI, cX, S, W;
+  const int32_t *C;    /* general cost matrix [R][R], or NULL (two-level) */
+  const int64_t *We;   /* ||W_e|| per expert, or NULL (W for every expert) */
 } model;
 
-/* Communication cost per byte c(s, r) of the two-level model. */
+/* Communication cost per byte c(s, r) (Section 4.1): the given symmetric
+ * matrix, or the two-level model (0 on the diagonal, cI inside a domain, cX
+ * across). */
 static int64_t cost(const model *m, int s, int r) {
+  if (m->C) return m->C[(size_t)s * m->R + r];
   if (s == r) return 0;
   return (s / m->G == r / m->G) ? m->cI : m->cX;
 }
+
+/* Parameter size of expert e, ||W_e||. */
+static int64_t wexp(const model *m, int e) { return m->We ? m->We[e] : m->W; }
 
 static int dom(const model *m, int r) { return r / m->G; }
 static int main_rank(const model *m, int e) { return e / m->P; }
@@ -106,6 +119,16 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
                        int32_t replica_budget, int32_t *replica_slots,
                        int32_t *token_dest, int32_t *send_counts,
                        int32_t *recv_counts, int32_t *status, ref_debug *dbg) {
+  return topoep_plan_ref_general(topo, NULL, NULL, global_load, local_topk, T, k, replica_budget,
+                                 replica_slots, token_dest, send_counts, recv_counts, status, dbg);
+}
+
+int topoep_plan_ref_general(const ref_topology *topo, const int32_t *cost_matrix,
+                            const int64_t *expert_bytes, const int32_t *global_load,
+                            const int32_t *local_topk, int32_t T, int32_t k,
+                            int32_t replica_budget, int32_t *replica_slots,
+                            int32_t *token_dest, int32_t *send_counts,
+                            int32_t *recv_counts, int32_t *status, ref_debug *dbg) {
   if (!topo || !global_load || !replica_slots || !send_counts || !status) return REF_EINVAL;
   if (T < 0 || k < 1 || replica_budget < 0) return REF_EINVAL;
   if (T > 0 && (!local_topk || !token_dest)) return REF_EINVAL;
@@ -126,6 +149,8 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
   m.cX = topo->cost_inter;
   m.S = topo->tok_bytes;
   m.W = topo->expert_bytes;
+  m.C = cost_matrix;
+  m.We = expert_bytes;
   const int R = m.R, G = m.G, M = m.M, E = m.E, N = m.N;
   const int64_t n_assign = (int64_t)T * k;
 
@@ -171,22 +196,42 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
   for (size_t i = 0; i < (size_t)R * E; ++i)
     if (global_load[i] < 0) st |= REF_ST_NEG_LOAD;
 
+  /* A general cost matrix must be a cost: symmetric, nonnegative, zero on
+   * the diagonal (Section 4.1); expert sizes nonnegative. */
+  int64_t cmax = m.cI > m.cX ? m.cI : m.cX, wmax = m.W;
+  if (m.C) {
+    cmax = 0;
+    for (int s = 0; s < R; ++s)
+      for (int r = 0; r < R; ++r) {
+        int32_t c = m.C[(size_t)s * R + r];
+        if (c < 0 || c != m.C[(size_t)r * R + s] || (s == r && c != 0)) st |= REF_ST_COST;
+        if (c > cmax) cmax = c;
+      }
+  }
+  if (m.We) {
+    wmax = 0;
+    for (int e = 0; e < E; ++e) {
+      if (m.We[e] < 0) st |= REF_ST_COST;
+      if (m.We[e] > wmax) wmax = m.We[e];
+    }
+  }
+
   /* Exact-arithmetic range: counts are int32 and cost terms int64.  The
-   * total load must fit int32 and 4 S total max(c,1) + max(c,1) W < 2^62
-   * bounds every benefit b and every cost change of a move. */
+   * total load must fit int32 and 4 S total max(c,1) + max(c,1) max(W) <
+   * 2^62 bounds every benefit b and every cost change of a move. */
   {
     int64_t total = 0;
     for (size_t i = 0; i < (size_t)R * E; ++i)
       if (omega[i] > 0) total += omega[i];
-    int64_t cm = m.cI > m.cX ? m.cI : m.cX;
+    int64_t cm = cmax;
     if (cm < 1) cm = 1;
     unsigned __int128 bound = (unsigned __int128)4 * (unsigned __int128)m.S *
                                   (unsigned __int128)total * (unsigned __int128)cm +
-                              (unsigned __int128)cm * (unsigned __int128)m.W;
+                              (unsigned __int128)cm * (unsigned __int128)(wmax > 0 ? wmax : 0);
     if (total > INT32_MAX || bound >= ((unsigned __int128)1 << 62)) st |= REF_ST_RANGE;
   }
 
-  if (st & (REF_ST_BAD_ID | REF_ST_NEG_LOAD | REF_ST_RANGE)) {
+  if (st & (REF_ST_BAD_ID | REF_ST_NEG_LOAD | REF_ST_RANGE | REF_ST_COST)) {
     for (int i = 0; i < R * N; ++i) replica_slots[i] = -1;
     for (int r = 0; r < R; ++r) send_counts[r] = 0;
     if (recv_counts)
@@ -221,7 +266,7 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
     int nc = 0;
     for (int e = 0; e < E; ++e) {
       if (dom(&m, main_rank(&m, e)) == d) continue;
-      int64_t b = 2 * D[(size_t)d * E + e] * m.S - m.W;
+      int64_t b = 2 * D[(size_t)d * E + e] * m.S - wexp(&m, e);
       if (b > 0) {
         cand[nc].e = e;
         cand[nc].b = b;
@@ -311,7 +356,7 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
             remaining -= take;
             dtok += take * order[i].diff;
           }
-          int64_t dcost = 2 * m.S * dtok + (hosts ? 0 : cost(&m, main_rank(&m, e), rt) * m.W);
+          int64_t dcost = 2 * m.S * dtok + (hosts ? 0 : cost(&m, main_rank(&m, e), rt) * wexp(&m, e));
           cand_key key = {-delta, L[rt], dcost, e, rt};
           if (!have || key_less(&key, &best)) {
             have = 1;

@@ -65,6 +65,9 @@ typedef struct {
 #define REF_ST_NEG_LOAD 2u    /* a negative entry in global_load                  */
 #define REF_ST_SELF_DIFF 4u   /* global_load[self] differs from the histogram     */
 #define REF_ST_RANGE 8u       /* loads or costs exceed the exact integer range    */
+#define REF_ST_COST 64u       /* a general cost matrix is not symmetric, has a    */
+                              /* nonzero diagonal or a negative entry, or an      */
+                              /* expert size is negative                          */
 
 /*
  * All pointers are host pointers, row-major.  Outputs: replica_slots[R*N]
@@ -89,6 +92,17 @@ int topoep_plan_ref_ex(const ref_topology *topo, const int32_t *global_load,
                        int32_t replica_budget, int32_t *replica_slots,
                        int32_t *token_dest, int32_t *send_counts,
                        int32_t *recv_counts, int32_t *status, ref_debug *dbg);
+
+/* The full model of Section 4.1: cost_matrix [R*R] (c(s,r), row-major) or
+ * NULL for the topology's two-level cost; expert_bytes [E] (||W_e||) or
+ * NULL for topo->expert_bytes for every expert.  An invalid matrix or a
+ * negative size sets REF_ST_COST and no plan is made. */
+int topoep_plan_ref_general(const ref_topology *topo, const int32_t *cost_matrix,
+                            const int64_t *expert_bytes, const int32_t *global_load,
+                            const int32_t *local_topk, int32_t T, int32_t k,
+                            int32_t replica_budget, int32_t *replica_slots,
+                            int32_t *token_dest, int32_t *send_counts,
+                            int32_t *recv_counts, int32_t *status, ref_debug *dbg);
 
 /* Dispatch layout of the rerouted assignments: send_offsets[R + 1] is the
  * exclusive prefix of send_counts; token_slot[n] = send_offsets[dest] + the

@@ -23,6 +23,8 @@ class Topo:
     S: int
     W: int
     N: int
+    C: object = None      # general cost matrix [R, R] (the full model of Sec. 4.1), or None
+    Wvec: object = None   # ||W_e|| per expert [E], or None (W for every expert)
 
     @property
     def M(self):
@@ -38,7 +40,12 @@ class Topo:
     def main(self, e):
         return e // self.P
 
+    def w(self, e):
+        return int(self.Wvec[e]) if self.Wvec is not None else self.W
+
     def cost_matrix(self):
+        if self.C is not None:
+            return np.asarray(self.C, np.int64)
         r = np.arange(self.R)
         same = (r[:, None] // self.G) == (r[None, :] // self.G)
         C = np.where(same, self.cI, self.cX).astype(np.int64)
@@ -68,7 +75,7 @@ def check_constraints(t: Topo, omega, x, q, D=None):
     for e in range(t.E):
         for r in range(t.R):
             if x[e, r] and t.dom(r) != t.dom(t.main(e)):
-                assert t.W < 2 * int(D[t.dom(r), e]) * t.S, "C4 violated"
+                assert t.w(e) < 2 * int(D[t.dom(r), e]) * t.S, "C4 violated"
     # C5 fixed main placement
     assert x[np.arange(t.E), np.arange(t.E) // t.P].all(), "C5 violated"
 
@@ -95,7 +102,7 @@ def objective(t: Topo, x, q, t_ffn=0):
         me = t.main(e)
         for r in range(t.R):
             if r != me and x[e, r]:
-                T_rep += int(C[me, r]) * t.W
+                T_rep += int(C[me, r]) * t.w(e)
     return T_comp + T_tok + T_rep
 
 
@@ -123,7 +130,7 @@ def brute_force_opt_no_compute(t: Topo, omega):
         ok = True
         for i, (e, r) in enumerate(pairs):
             if mask >> i & 1:
-                if t.dom(r) != t.dom(t.main(e)) and not (t.W < 2 * int(D[t.dom(r), e]) * t.S):
+                if t.dom(r) != t.dom(t.main(e)) and not (t.w(e) < 2 * int(D[t.dom(r), e]) * t.S):
                     ok = False
                     break
                 x[e, r] = True
@@ -134,7 +141,7 @@ def brute_force_opt_no_compute(t: Topo, omega):
             for e in range(t.E):
                 if omega[s, e]:
                     tok += int(omega[s, e]) * int(C[s, x[e]].min())
-        rep = sum(int(C[t.main(e), r]) * t.W for e in range(t.E) for r in range(t.R)
+        rep = sum(int(C[t.main(e), r]) * t.w(e) for e in range(t.E) for r in range(t.R)
                   if r != t.main(e) and x[e, r])
         val = 2 * t.S * tok + rep
         if best is None or val < best:
@@ -149,7 +156,7 @@ def stage1_best_benefit(t: Topo, D, d):
     for e in range(t.E):
         if t.dom(t.main(e)) == d:
             continue
-        b = 2 * int(D[d, e]) * t.S - t.W
+        b = 2 * int(D[d, e]) * t.S - t.w(e)
         if b > 0:
             bs.append(b)
     cap = t.G * t.N
@@ -206,7 +213,7 @@ def enumerate_candidates(t: Topo, x, q, used, d, brute_split=True):
                 continue
             avail = [int(q[s, e, rb]) for s in range(t.R)]
             diff = [int(C[s, rt] - C[s, rb]) for s in range(t.R)]
-            rep = 0 if hosts else int(C[t.main(e), rt]) * t.W
+            rep = 0 if hosts else int(C[t.main(e), rt]) * t.w(e)
             if brute_split:
                 best = None
                 order = sorted(range(t.R), key=lambda s: (diff[s], s))

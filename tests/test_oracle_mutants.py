@@ -17,7 +17,7 @@ SRC = os.path.join(ROOT, "oracle", "topoep_oracle.c")
 
 MUTANTS = [
     ("benefit without the factor 2",
-     "int64_t b = 2 * D[(size_t)d * E + e] * m.S - m.W;", "int64_t b = D[(size_t)d * E + e] * m.S - m.W;"),
+     "int64_t b = 2 * D[(size_t)d * E + e] * m.S - wexp(&m, e);", "int64_t b = D[(size_t)d * E + e] * m.S - wexp(&m, e);"),
     ("benefit test not strict", "if (b > 0) {", "if (b >= 0) {"),
     ("candidates in ascending benefit",
      "if (a->b != b->b) return a->b > b->b ? -1 : 1;", "if (a->b != b->b) return a->b < b->b ? -1 : 1;"),
@@ -40,13 +40,24 @@ MUTANTS = [
      "if (a->diff != b->diff) return a->diff < b->diff ? -1 : 1;",
      "if (a->diff != b->diff) return a->diff > b->diff ? -1 : 1;"),
     ("replica transfer cost dropped",
-     "(hosts ? 0 : cost(&m, main_rank(&m, e), rt) * m.W)", "0"),
+     "(hosts ? 0 : cost(&m, main_rank(&m, e), rt) * wexp(&m, e))", "0"),
     ("token cost change with the wrong sign", "int64_t dcost = 2 * m.S * dtok +", "int64_t dcost = -2 * m.S * dtok +"),
     ("rerouting off by one", "if (rho < prefix + c) {", "if (rho <= prefix + c) {"),
     ("send counts read the wrong index",
      "for (int e = 0; e < E; ++e) sc += Q(m.self, e, r);", "for (int e = 0; e < E; ++e) sc += Q(r, e, m.self);"),
     ("histogram not used as row self", "omega[(size_t)m.self * E + e] = hist[e];", "(void)0;"),
     ("full slots still accept replicas", "if (!hosts && used[rt] >= N) continue;", "if (!hosts && used[rt] > N) continue;"),
+    ("one expert size for every expert",
+     "static int64_t wexp(const model *m, int e) { return m->We ? m->We[e] : m->W; }",
+     "static int64_t wexp(const model *m, int e) { (void)e; return m->W; }"),
+    ("replica cost from the target's own expert size",
+     "(hosts ? 0 : cost(&m, main_rank(&m, e), rt) * wexp(&m, e))",
+     "(hosts ? 0 : cost(&m, main_rank(&m, e), rt) * wexp(&m, rt % m.E))"),
+    ("general cost read as the two-level one",
+     "  if (m->C) return m->C[(size_t)s * m->R + r];\n", ""),
+    ("asymmetric matrix accepted",
+     "if (c < 0 || c != m.C[(size_t)r * R + s] || (s == r && c != 0)) st |= REF_ST_COST;",
+     "if (c < 0 || (s == r && c != 0)) st |= REF_ST_COST;"),
 ]
 
 
@@ -64,10 +75,13 @@ def _battery():
               edges.test_self_row_mismatch_is_informational]
     for s in pins.SEEDS[:30]:
         checks += [lambda s=s: pins.test_histogram_and_demand(s),
-                   lambda s=s: pins.test_stage1_placement(s),
+                   lambda s=s: pins.test_stage1_placement(s, False),
+                   lambda s=s: pins.test_stage1_placement(s, True),
                    lambda s=s: pins.test_routing_construction(s),
-                   lambda s=s: pins.test_refinement_steps(s),
+                   lambda s=s: pins.test_refinement_steps(s, False),
+                   lambda s=s: pins.test_refinement_steps(s, True),
                    lambda s=s: pins.test_rerouting_and_cross_rank(s)]
+    checks += [pins.test_invalid_cost_model_makes_no_plan]
     for s in range(20):
         checks += [lambda s=s: pins.test_one_gpu_per_node_reaches_the_optimum(s)]
     for c in checks:

@@ -17,8 +17,10 @@ from planmodel import (Topo, best_candidate, brute_force_opt_no_compute, check_c
                        objective, stage1_best_benefit)
 
 
-def random_instance(seed, R=None, G=None, P=None, N=None, k=None, big=False):
-    """A tiny instance whose every rank's top-k array is simulated."""
+def random_instance(seed, R=None, G=None, P=None, N=None, k=None, big=False, general=False):
+    """A tiny instance whose every rank's top-k array is simulated; with
+    general, a random symmetric cost matrix (zero diagonal) and a random
+    size per expert (the full model of Section 4.1)."""
     rng = np.random.default_rng(seed)
     if G is None:
         G = int(rng.choice([1, 2, 3, 4]))
@@ -45,12 +47,16 @@ def random_instance(seed, R=None, G=None, P=None, N=None, k=None, big=False):
     Dmax = max(1, int(domain_demand(Topo(R, G, E, cI, cX, S, 0, N), omega).max()))
     W = int(rng.integers(0, 2 * S * Dmax + 2))
     t = Topo(R, G, E, cI, cX, S, W, N)
+    if general:
+        C = np.triu(rng.integers(0, 9, size=(R, R)), 1)
+        t.C = (C + C.T).astype(np.int32)
+        t.Wvec = rng.integers(0, 2 * S * Dmax + 2, size=E).astype(np.int64)
     return t, omega, topks
 
 
 def run(t, omega, topk, self_rank, **kw):
     topo = oracle.topology(t.R, t.G, t.E, self_rank, t.cI, t.cX, t.S, t.W)
-    return oracle.plan_ref(topo, omega, topk, t.N, **kw)
+    return oracle.plan_ref(topo, omega, topk, t.N, cost_matrix=t.C, expert_bytes=t.Wvec, **kw)
 
 
 SEEDS = list(range(60))
@@ -68,11 +74,12 @@ def test_histogram_and_demand(seed):
     assert (D.sum(axis=0) == omega.sum(axis=0)).all()
 
 
+@pytest.mark.parametrize("general", [False, True])
 @pytest.mark.parametrize("seed", SEEDS)
-def test_stage1_placement(seed):
+def test_stage1_placement(seed, general):
     """Inter-node placement (Eq. 9): greedy sum of b is the subset optimum, the
     ranks follow 'least occupied rank with a free slot', C3-C5 hold."""
-    t, omega, topks = random_instance(seed, N=int(np.random.default_rng(seed).integers(0, 3)))
+    t, omega, topks = random_instance(seed, N=int(np.random.default_rng(seed).integers(0, 3)), general=general)
     out = run(t, omega, topks[0], 0, debug=True, move_cap=1000)
     x1 = out["x_stage1"].astype(bool)
     D = domain_demand(t, omega)
@@ -86,13 +93,13 @@ def test_stage1_placement(seed):
         for e in chosen:
             assert reps[e, list(ranks)].sum() == 1
             assert t.dom(t.main(e)) != d
-            assert 2 * int(D[d, e]) * t.S - t.W > 0
-        total_b = sum(2 * int(D[d, e]) * t.S - t.W for e in chosen)
+            assert 2 * int(D[d, e]) * t.S - t.w(e) > 0
+        total_b = sum(2 * int(D[d, e]) * t.S - t.w(e) for e in chosen)
         assert total_b == stage1_best_benefit(t, D, d)
         # closed form of 'fewest used slots, ties to the lowest rank': the i-th
         # chosen candidate in (b desc, e asc) order lands on rank dG + i mod G,
         # slot i div G
-        order = sorted(chosen, key=lambda e: (-(2 * int(D[d, e]) * t.S - t.W), e))
+        order = sorted(chosen, key=lambda e: (-(2 * int(D[d, e]) * t.S - t.w(e)), e))
         for i, e in enumerate(order):
             r = d * t.G + i % t.G
             assert reps[e, r]
@@ -123,14 +130,15 @@ def test_routing_construction(seed):
     assert (loads(q) == out["load_routed"]).all()
 
 
+@pytest.mark.parametrize("general", [False, True])
 @pytest.mark.parametrize("seed", SEEDS)
-def test_refinement_steps(seed):
+def test_refinement_steps(seed, general):
     """Replay every committed move of the intra-node refinement (Eq. 10)
     against an independent enumerator: the chosen candidate is the key
     minimum, its split is a minimum-cost split, its cost change equals the
     change of Eqs. 6-7, and the invariants of Section 4.3 hold."""
     rng = np.random.default_rng(1000 + seed)
-    t, omega, topks = random_instance(1000 + seed, N=int(rng.integers(1, 4)), big=True)
+    t, omega, topks = random_instance(1000 + seed, N=int(rng.integers(1, 4)), big=True, general=general)
     out = run(t, omega, topks[0], 0, debug=True, move_cap=10000)
     assert out["n_moves"] <= 10000
     x = out["x_stage1"].astype(bool).copy()
@@ -371,3 +379,50 @@ def test_gather_matches_fancy_indexing_and_keeps_other_slots():
     # a slot whose expert is unchanged is not copied
     out2 = oracle.gather_ref(slots, 2, params, before, prev_slots=np.array([5, 7, 3], np.int32))
     assert (out2[0] == before[0]).all() and (out2[2] == params[11]).all()
+
+
+# ---------------------------------------------------------------- general cost model
+
+@pytest.mark.parametrize("seed", range(30))
+def test_general_model_with_two_level_costs_is_the_two_level_plan(seed):
+    """The two-level matrix and one size for every expert, given explicitly,
+    give exactly the plan of the two-level parameters."""
+    t, omega, topks = random_instance(3300 + seed, big=True)
+    s = seed % t.R
+    a = run(t, omega, topks[s], s)
+    t.C = t.cost_matrix().astype(np.int32)
+    t.Wvec = np.full(t.E, t.W, np.int64)
+    b = run(t, omega, topks[s], s)
+    for key in ("replica_slots", "token_dest", "send_counts", "recv_counts"):
+        assert (a[key] == b[key]).all(), key
+    assert (a["status"], a["move_count"]) == (b["status"], b["move_count"])
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_general_model_conservation_and_receive_counts(seed):
+    """C1-C5 on the final plan and every rank's receive counts against every
+    sender's own plan, under a general cost matrix and per-expert sizes."""
+    t, omega, topks = random_instance(3400 + seed, big=True, general=True)
+    outs = [run(t, omega, topks[s], s, debug=True) for s in range(t.R)]
+    for r in range(t.R):
+        assert outs[r]["status"] == 0
+        assert (outs[r]["replica_slots"] == outs[0]["replica_slots"]).all()
+        for s in range(t.R):
+            assert outs[r]["recv_counts"][s] == outs[s]["send_counts"][r]
+    check_constraints(t, omega, outs[0]["x_final"], outs[0]["q_final"])
+
+
+def test_invalid_cost_model_makes_no_plan():
+    t, omega, topks = random_instance(77, big=True, general=True)
+    good = t.C.copy()
+    bad_cases = []
+    c = good.copy(); c[0, 1] += 1; bad_cases.append(("asymmetric", c, t.Wvec))
+    c = good.copy(); c[1, 1] = 2; bad_cases.append(("diagonal", c, t.Wvec))
+    c = good.copy(); c[0, 1] = c[1, 0] = -1; bad_cases.append(("negative", c, t.Wvec))
+    w = t.Wvec.copy(); w[3] = -5; bad_cases.append(("negative size", good, w))
+    for what, C, W in bad_cases:
+        t.C, t.Wvec = C, W
+        out = run(t, omega, topks[0], 0)
+        assert out["status"] & oracle.ST_COST, what
+        assert (out["replica_slots"] == -1).all() and (out["send_counts"] == 0).all(), what
+        assert (out["token_dest"] == -1).all() and (out["recv_counts"] == 0).all(), what
