@@ -109,7 +109,10 @@ typedef struct topoep_shape {
                                  /* integer cost terms would not be exact            */
 #define TOPOEP_ST_SYNC 16u       /* a bounded in-kernel wait gave up (outputs wrong) */
 #define TOPOEP_ST_ITER 32u       /* refinement hit its iteration bound               */
-/* With BAD_ID, NEG_LOAD or RANGE no plan is made: replica_slots = -1,
+#define TOPOEP_ST_COST 64u       /* (topoep_plan_costs) the cost matrix is not        */
+                                 /* symmetric, nonnegative and zero on its diagonal, */
+                                 /* or an expert size is negative                    */
+/* With BAD_ID, NEG_LOAD, RANGE or COST no plan is made: replica_slots = -1,
  * send_counts = 0, token_dest = -1, status[1] = 0. */
 
 /*
@@ -292,6 +295,41 @@ int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load
 int topoep_gather_replicas(const topoep_topology *topo, int32_t replica_budget, const int32_t *replica_slots,
                            const int32_t *prev_slots, const void *expert_params, int64_t bytes_per_expert,
                            void *slot_params, void *stream);
+
+/*
+ * The full model of Section 4.1: a general symmetric cost matrix C and one
+ * parameter size per expert, in place of the topology's two-level cost
+ * (cost_intra, cost_inter) and single expert_bytes.  Both enter the
+ * stage-1 benefit b = 2 D S_tok - ||W_e|| (Eq. 9), the refinement's cost
+ * change and the order in which a move takes assignments from the sources
+ * (ascending c(s,rt) - c(s,rb), then s), and the exact-range bound (the
+ * largest entry of C and the largest size).  Domains stay G consecutive
+ * ranks.  Such plans run the three-kernel shape with the per-domain solver.
+ */
+typedef struct topoep_costs {
+  const int32_t *cost;          /* device int32 [R, R] c(s, r) row-major, or NULL:     */
+                                /* the topology's two-level cost                       */
+  const int64_t *expert_bytes;  /* device int64 [E] ||W_e||, or NULL: the topology's   */
+                                /* expert_bytes for every expert                       */
+} topoep_costs;
+
+/* Bytes of device workspace topoep_plan_costs needs (TOPOEP_ELIMIT when a
+ * domain's state with the cost tables cannot fit in LDS). */
+int topoep_costs_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
+                                 size_t *bytes_out);
+
+/*
+ * topoep_plan under the full cost model (costs may be NULL, or either of
+ * its pointers, for the topology's values).  The matrix is checked on the
+ * device: an asymmetric matrix, a nonzero diagonal or a negative entry, or
+ * a negative size, sets TOPOEP_ST_COST and no plan is made.  Other
+ * arguments, outputs and return codes as topoep_plan; the workspace is
+ * topoep_costs_workspace_bytes bytes.
+ */
+int topoep_plan_costs(const topoep_topology *topo, const topoep_costs *costs, const int32_t *global_load,
+                      const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
+                      int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts, int32_t *status,
+                      void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -62,7 +62,7 @@ constexpr int kCtrlArrive = 8;
 constexpr uint32_t kVerdictSame = 1;
 constexpr uint32_t kVerdictRedo = 2;
 
-constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE;
+constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE | TOPOEP_ST_COST;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kMaxSolveGroups = 128;    // co-resident by a wide margin (256 CUs)
 constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
@@ -87,6 +87,9 @@ struct Plan {
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   int32_t *recv_out;   // receive counts [R], or null
+  const int32_t *Cm;   // general cost matrix [R, R] (with general), else null
+  const int64_t *We;   // ||W_e|| per expert [E] (with general), else null
+  int general;         // the full model of Section 4.1 (per-domain solver only)
   int32_t *slot_out;   // send-buffer slot of every assignment [n], or null
   int32_t *offs_out;   // send offsets [R + 1] (given with slot_out)
   uint32_t *ctrl;
@@ -101,7 +104,14 @@ __host__ __device__ inline int hist_scratch_words(const Plan &p) { return imax(p
 
 // LDS layout of the one-workgroup-per-domain solver, in int32 words.
 struct DomainLds {
-  int ck, fdt, hs, rows, mask, slots, used, L, e_of, U, misc, qcol, words;
+  int ck, fdt, hs, rows, mask, slots, used, L, e_of, U, misc, qcol, ord, ccol, wx, words;
+};
+
+// The general cost model's per-domain tables in LDS (see domain_lds).
+struct GenCost {
+  const uint16_t *ord;
+  const int *ccol;
+  const int64_t *wx;
 };
 
 __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
@@ -121,6 +131,13 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
   l.misc = o;  o += 64;
   l.qcol = o;                                // q[s][e][r] of the domain's instances
   o += imax(p.I * p.QS, imax(2 * p.E + 2 + p.E * p.RW + 64, hist_scratch_words(p)));
+  // general cost model: per (busiest, target) pair of the domain's ranks the
+  // sources in (c(s,rt) - c(s,rb), s) order (16-bit), the costs to the
+  // domain's ranks, ||W_e||
+  l.ord = o;   o += p.general ? (p.G * p.G * p.R + 1) / 2 : 0;
+  l.ccol = o;  o += p.general ? p.G * p.R : 0;
+  o = (o + 1) & ~1;
+  l.wx = o;    o += p.general ? 2 * p.E : 0;
   l.words = o;
   return l;
 }
@@ -423,17 +440,21 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch) {
 
 // Exact-range check: the total load fits int32 and 4 S total c + c W < 2^62
 // (c = max(c_intra, c_inter, 1)), so every benefit and cost change is exact.
-__device__ inline bool out_of_range(const Plan &p, uint64_t total) {
+__device__ inline bool out_of_range_cw(const Plan &p, uint64_t total, uint64_t cmax, uint64_t wmax) {
   const uint64_t lim = 1ull << 62;
-  const uint64_t cm = (uint64_t)imax(imax(p.cI, p.cX), 1);
+  const uint64_t cm = cmax > 1 ? cmax : 1;
   if (total > 0x7FFFFFFFull) return true;
   // 4 S total cm and cm W with overflow checks (every factor is nonnegative)
   uint64_t tok = 0, rep = 0;
   if (__builtin_mul_overflow((uint64_t)p.S, 4ull * total, &tok)) return true;
   if (__builtin_mul_overflow(tok, cm, &tok)) return true;
-  if (__builtin_mul_overflow((uint64_t)p.W, cm, &rep)) return true;
+  if (__builtin_mul_overflow(wmax, cm, &rep)) return true;
   if (tok >= lim || rep >= lim) return true;
   return tok + rep >= lim;
+}
+
+__device__ inline bool out_of_range(const Plan &p, uint64_t total) {
+  return out_of_range_cw(p, total, (uint64_t)imax(p.cI, p.cX), (uint64_t)p.W);
 }
 
 // Grid barrier of the per-domain solver workgroups: all of them are
@@ -682,9 +703,13 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // delta >= 1.  Returns the number of moves committed (at once 0 when no rank
 // of the domain has a free slot).  With prepared, em already holds the masks
 // and the wave sums the rank loads Lr itself; otherwise Lr is given and em is
-// scratch filled here.
+// scratch filled here.  With General (the full model of Section 4.1) the
+// moved assignments come from the sources in the precomputed (c(s,rt) -
+// c(s,rb), s) order of gc, and the cost change uses the cost matrix and
+// ||W_e||.
+template <bool General = false>
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
-                                  int *Lr, uint64_t *em, uint32_t *flags, bool prepared) {
+                                  int *Lr, uint64_t *em, uint32_t *flags, bool prepared, GenCost gc = GenCost{}) {
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return 0;
@@ -769,14 +794,30 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
       const int rt = r0 + rtj;
       const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
       int64_t dcost = 0;
-      if (p.cI > 0) {
-        const int qrt = qcol[a * QS + rt], qrb = qcol[a * QS + rb];
-        const int m_rt = imin(delta, qrt);
-        const int rest = delta - m_rt;
-        const int m_rb = rest - imin(rest, u - qrt - qrb);
-        dcost = tokc * (int64_t)(m_rb - m_rt);
+      if constexpr (General) {
+        // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
+        const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
+        const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
+        int rest = delta;
+        int64_t dt = 0;
+        for (int k = 0; k < R && rest > 0; ++k) {
+          const int s = o[k];
+          const int take = imin(rest, qcol[a * QS + s]);
+          dt += (int64_t)take * (ct[s] - cb[s]);
+          rest -= take;
+        }
+        dcost = 2 * p.S * dt;
+        if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
+      } else {
+        if (p.cI > 0) {
+          const int qrt = qcol[a * QS + rt], qrb = qcol[a * QS + rb];
+          const int m_rt = imin(delta, qrt);
+          const int rest = delta - m_rt;
+          const int m_rb = rest - imin(rest, u - qrt - qrb);
+          dcost = tokc * (int64_t)(m_rb - m_rt);
+        }
+        if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
       }
-      if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
       const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
       const uint64_t c2 = (uint64_t)dcost ^ (1ull << 63);
       const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)rt;
@@ -822,29 +863,49 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     int *qa = qcol + a * QS;
     int *qb = qcol + a2 * QS;
     int rest = delta;
-    if (p.cI > 0) {
-      const int m_rt = imin(rest, qa[rt]);
-      wave_sync();
-      if (lane == 0 && m_rt) {
-        qa[rt] -= m_rt;
-        qb[rt] += m_rt;
+    if constexpr (General) {
+      // the sources in the pair's order, 64 at a time
+      const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
+      for (int k0 = 0; k0 < R && rest > 0; k0 += 64) {
+        const int k = k0 + lane;
+        const int s = k < R ? o[k] : 0;
+        const int av = k < R ? qa[s] : 0;
+        const int incl = wave_incl_scan(av);
+        const int excl = incl - av;
+        int m = rest - excl;
+        m = m < 0 ? 0 : (m > av ? av : m);
+        if (m) {
+          qa[s] -= m;
+          qb[s] += m;
+        }
+        const int total = readlane_i32(incl, 63);
+        rest -= total < rest ? total : rest;
       }
-      rest -= m_rt;
-    }
-    for (int s0 = 0; s0 < R && rest > 0; s0 += 64) {
-      const int s = s0 + lane;
-      int av = 0;
-      if (s < R && (p.cI == 0 || (s != rt && s != rb))) av = qa[s];
-      const int incl = wave_incl_scan(av);
-      const int excl = incl - av;
-      int m = rest - excl;
-      m = m < 0 ? 0 : (m > av ? av : m);
-      if (m) {
-        qa[s] -= m;
-        qb[s] += m;
+    } else {
+      if (p.cI > 0) {
+        const int m_rt = imin(rest, qa[rt]);
+        wave_sync();
+        if (lane == 0 && m_rt) {
+          qa[rt] -= m_rt;
+          qb[rt] += m_rt;
+        }
+        rest -= m_rt;
       }
-      const int total = readlane_i32(incl, 63);
-      rest -= total < rest ? total : rest;
+      for (int s0 = 0; s0 < R && rest > 0; s0 += 64) {
+        const int s = s0 + lane;
+        int av = 0;
+        if (s < R && (p.cI == 0 || (s != rt && s != rb))) av = qa[s];
+        const int incl = wave_incl_scan(av);
+        const int excl = incl - av;
+        int m = rest - excl;
+        m = m < 0 ? 0 : (m > av ? av : m);
+        if (m) {
+          qa[s] -= m;
+          qb[s] += m;
+        }
+        const int total = readlane_i32(incl, 63);
+        rest -= total < rest ? total : rest;
+      }
     }
     wave_sync();
     if (lane == 0) {
@@ -884,6 +945,21 @@ __device__ inline void rank_candidates(int c, int nc, int cap, const uint64_t *k
   }
   for (; c2 < nc; ++c2) rank += keys[c2] < kc;
   if (rank < cap) out[rank] = (int)(uint32_t)kc;
+}
+
+// Rank of candidate c by (benefit b descending, expert ascending) among nc
+// candidates with benefits bs[] and experts es[] (the general model, where
+// ||W_e|| differs per expert so b does not follow D); the first cap ranks
+// name the domain's stage-1 replicas.
+__device__ inline void rank_candidates_b(int c, int nc, int cap, const uint64_t *bs, const int *es, int *out) {
+  const uint64_t bc = bs[c];
+  const int ec = es[c];
+  int rank = 0;
+  for (int c2 = 0; c2 < nc; ++c2) {
+    const uint64_t b2 = bs[c2];
+    rank += b2 > bc || (b2 == bc && es[c2] < ec);
+  }
+  if (rank < cap) out[rank] = ec;
 }
 
 // Stage 1 (Eq. 9) candidates of domain d, by one wave: the experts whose
@@ -994,6 +1070,83 @@ __device__ void scan_rows(const Plan &p, int r0, int r1, const int *rows, const 
   }
 }
 
+// ---------------------------------------------------------------- general cost model
+
+// The full model of Section 4.1 on the device: whether the cost matrix is a
+// cost (symmetric, nonnegative, zero diagonal) and every size nonnegative,
+// and the largest entry and size for the exact-range bound.  misc[16..23]
+// are scratch; returns the COST bit or 0 (the same on every thread).
+__device__ uint32_t general_check(const Plan &p, int *misc, uint64_t *cmax, uint64_t *wmax) {
+  const int tid = threadIdx.x, nt = blockDim.x, R = p.R;
+  if (tid < 8) misc[16 + tid] = 0;
+  lds_barrier();
+  bool bad = false;
+  uint32_t cm = 0;
+  uint64_t wm = 0;
+  if (p.Cm) {
+    for (int i = tid; i < R * R; i += nt) {
+      const int s = i / R, r = i - s * R;
+      const int c = p.Cm[i];
+      bad |= c < 0 || (s == r && c != 0) || c != p.Cm[(int64_t)r * R + s];
+      if (c > 0 && (uint32_t)c > cm) cm = (uint32_t)c;
+    }
+  } else {
+    cm = (uint32_t)imax(p.cI, p.cX);
+  }
+  if (p.We) {
+    for (int e = tid; e < p.E; e += nt) {
+      const int64_t w = p.We[e];
+      bad |= w < 0;
+      if (w > 0 && (uint64_t)w > wm) wm = (uint64_t)w;
+    }
+  } else {
+    wm = (uint64_t)p.W;
+  }
+  if (bad) misc[16] = 1;
+  atomicMax(reinterpret_cast<unsigned *>(&misc[17]), cm);
+  atomicMax(reinterpret_cast<unsigned long long *>(misc + 18), (unsigned long long)wm);
+  lds_barrier();
+  *cmax = (uint32_t)misc[17];
+  *wmax = *reinterpret_cast<const unsigned long long *>(misc + 18);
+  const uint32_t st = misc[16] ? TOPOEP_ST_COST : 0u;
+  lds_barrier();
+  return st;
+}
+
+// Cost tables of domain d for its refinement: ccol[j][s] = c(s, dG + j),
+// ||W_e|| and, per ordered pair (jb, jt) of the domain's ranks, the sources
+// in ascending (c(s,rt) - c(s,rb), s) order.
+__device__ GenCost general_tables(const Plan &p, int d, int *sm, const DomainLds &lay) {
+  const int tid = threadIdx.x, nt = blockDim.x, R = p.R, G = p.G;
+  uint16_t *ord = reinterpret_cast<uint16_t *>(sm + lay.ord);
+  int *ccol = sm + lay.ccol;
+  int64_t *wx = reinterpret_cast<int64_t *>(sm + lay.wx);
+  for (int i = tid; i < G * R; i += nt) {
+    const int j = i / R, s = i - j * R, r = d * G + j;
+    ccol[i] = p.Cm ? p.Cm[(int64_t)s * R + r] : (s == r ? 0 : (s / G == r / G ? p.cI : p.cX));
+  }
+  for (int e = tid; e < p.E; e += nt) wx[e] = p.We ? p.We[e] : p.W;
+  lds_barrier();
+  for (int x = tid; x < G * G * R; x += nt) {
+    const int pair = x / R, s = x - pair * R, jb = pair / G, jt = pair - jb * G;
+    if (jb == jt) continue;
+    const int *cb = ccol + jb * R, *ct = ccol + jt * R;
+    const int ds = ct[s] - cb[s];
+    int rank = 0;
+    for (int s2 = 0; s2 < R; ++s2) {
+      const int d2 = ct[s2] - cb[s2];
+      rank += d2 < ds || (d2 == ds && s2 < s);
+    }
+    ord[pair * R + rank] = (uint16_t)s;
+  }
+  lds_barrier();
+  GenCost gc;
+  gc.ord = ord;
+  gc.ccol = ccol;
+  gc.wx = wx;
+  return gc;
+}
+
 // ---------------------------------------------------------------- solver: one workgroup per domain
 
 __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
@@ -1023,6 +1176,11 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
 
   if (tid < 16) misc[tid] = 0;
   build_divisors(M, fdt);
+  uint64_t cmax = (uint64_t)imax(p.cI, p.cX), wmax = (uint64_t)p.W;
+  if (p.general) {
+    const uint32_t cst = general_check(p, misc, &cmax, &wmax);
+    if (tid == 0 && cst) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), cst);
+  }
   // ---- row self of Omega: the histogram of local_topk
   hist_from_partials(p, hs, qcol);
   if (wg == 0)
@@ -1043,14 +1201,25 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
         const int s = d * G + j;
         D += s == p.self ? hs[e] : rows[j * E + e];
       }
-      if ((int64_t)2 * D * p.S > p.W) {
+      const int64_t we = p.general && p.We ? p.We[e] : p.W;
+      if ((int64_t)2 * D * p.S > we) {
         const int pos = atomicAdd(&misc[1], 1);
-        ck[pos] = cand_key(D, e);
+        if (p.general) {
+          // sizes differ per expert: rank by the benefit itself (qcol is
+          // free until the routing and holds the experts)
+          ck[pos] = (uint64_t)((int64_t)2 * D * p.S - we);
+          qcol[pos] = e;
+        } else {
+          ck[pos] = cand_key(D, e);
+        }
       }
     }
     lds_barrier();
     const int nc = misc[1];
-    for (int c = tid; c < nc; c += nt) rank_candidates(c, nc, cap, ck, p.repl1 + (int64_t)d * cap);
+    for (int c = tid; c < nc; c += nt) {
+      if (p.general) rank_candidates_b(c, nc, cap, ck, qcol, p.repl1 + (int64_t)d * cap);
+      else rank_candidates(c, nc, cap, ck, p.repl1 + (int64_t)d * cap);
+    }
     for (int i = imin(nc, cap) + tid; i < cap; i += nt) p.repl1[(int64_t)d * cap + i] = -1;
     lds_barrier();
   }
@@ -1065,7 +1234,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
   uint32_t gst = __hip_atomic_load(&p.ctrl[kCtrlStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint64_t total = __hip_atomic_load(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal),
                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (out_of_range(p, total)) gst |= TOPOEP_ST_RANGE;
+  if (out_of_range_cw(p, total, cmax, wmax)) gst |= TOPOEP_ST_RANGE;
   if (!synced) gst |= TOPOEP_ST_SYNC;
   const bool noplan = (gst & kNoPlan) != 0 || !synced;
 
@@ -1156,7 +1325,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
       Lr[j] = l;
     }
     lds_barrier();
-    if (tid < 64) {
+    if (p.general && full) {
+      const GenCost gc = general_tables(p, d, sm, lay);
+      if (tid < 64) {
+        const uint32_t mv = refine_domain<true>(p, d, e_of, U, qcol, slots, used, Lr, ck, &flags, false, gc);
+        if (tid == 0 && mv) atomicAdd(&p.ctrl[kCtrlMoves], mv);
+      }
+    } else if (tid < 64) {
       const uint32_t mv = refine_domain(p, d, e_of, U, qcol, slots, used, Lr, ck, &flags, false);
       if (tid == 0 && mv) atomicAdd(&p.ctrl[kCtrlMoves], mv);
     }
@@ -2204,7 +2379,7 @@ int ceil_log2(int v) {
 // Validate the arguments and fill the plan's sizes, launch shape and
 // workspace layout (pointers are offsets when ws == nullptr).
 int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoep_launch *lc, Plan *p,
-          Shape *sh, size_t *ws_bytes, char *ws) {
+          Shape *sh, size_t *ws_bytes, char *ws, bool general = false) {
   if (!t) return TOPOEP_EINVAL;
   const int R = t->num_ranks, G = t->ranks_per_node, E = t->num_experts;
   if (R <= 0 || G <= 0 || E <= 0 || R % G != 0 || E % R != 0) return TOPOEP_EINVAL;
@@ -2237,6 +2412,8 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.n = (int64_t)T * k;
   q.spin_limit = kSpinLimit;
   q.iter_limit = kIterLimit;
+  q.general = general ? 1 : 0;
+  if (general && R > 65535) return TOPOEP_ELIMIT;
   if ((int64_t)q.M * q.I * q.QS >= (1 << 30) || (int64_t)R * E >= (1 << 30)) return TOPOEP_ELIMIT;
   q.fE = make_fastdiv((uint32_t)E);
   q.fG = make_fastdiv((uint32_t)G);
@@ -2286,7 +2463,8 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     const int64_t fused_words = single_words > chunk_words ? single_words : chunk_words;
     const bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
     if (solver == 3 && !fused_ok) return TOPOEP_ELIMIT;
-    if (fused_ok && (solver == 3 || solver == 0)) {
+    if (general && solver == 3) return TOPOEP_EINVAL;   // the general model runs the per-domain solver
+    if (fused_ok && !general && (solver == 3 || solver == 0)) {
       s.mode = 3;
       s.ipt = ipt;
       s.st = st;
@@ -2313,7 +2491,11 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   if (nb > (1 << 24)) return TOPOEP_ELIMIT;
   q.nb = (int)nb;
   q.n_helpers = (E + kOffsetExperts - 1) / kOffsetExperts;
-  if (solver == 1) {
+  if (general) {
+    if (solver == 1) return TOPOEP_EINVAL;
+    if (!multi_fits) return TOPOEP_ELIMIT;
+    s.mode = 2;
+  } else if (solver == 1) {
     if (!single_fits) return TOPOEP_ELIMIT;
     s.mode = 1;
   } else if (solver == 2) {
@@ -2475,18 +2657,22 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
             const int32_t *local_topk, int32_t T, int32_t k, int32_t N, int32_t *replica_slots,
             int32_t *token_dest, int32_t *send_counts, int32_t *status, void *workspace,
             size_t workspace_bytes, void *stream, const topoep_launch *launch,
-            int32_t *recv_counts = nullptr, int32_t *send_offsets = nullptr, int32_t *token_slot = nullptr) {
+            int32_t *recv_counts = nullptr, int32_t *send_offsets = nullptr, int32_t *token_slot = nullptr,
+            const topoep_costs *costs = nullptr) {
   Plan p;
   Shape s;
   size_t need = 0;
-  int rc = setup(topo, T, k, N, launch, &p, &s, &need, nullptr);
+  const bool general = costs != nullptr;
+  int rc = setup(topo, T, k, N, launch, &p, &s, &need, nullptr, general);
   if (rc != TOPOEP_OK) return rc;
   if (!global_load || !send_counts || !status || !workspace) return TOPOEP_EINVAL;
   if ((int64_t)topo->num_ranks * N > 0 && !replica_slots) return TOPOEP_EINVAL;
   if (T > 0 && (!local_topk || !token_dest)) return TOPOEP_EINVAL;
   if (workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return TOPOEP_EWORKSPACE;
-  rc = setup(topo, T, k, N, launch, &p, &s, &need, static_cast<char *>(workspace));
+  rc = setup(topo, T, k, N, launch, &p, &s, &need, static_cast<char *>(workspace), general);
   if (rc != TOPOEP_OK) return rc;
+  p.Cm = general ? costs->cost : nullptr;
+  p.We = general ? costs->expert_bytes : nullptr;
   p.gl = global_load;
   p.topk = local_topk;
   p.slots_out = replica_slots;
@@ -2590,6 +2776,27 @@ int topoep_plan_dispatch(const topoep_topology *topo, const int32_t *global_load
   if (!recv_counts && !layout) return TOPOEP_EINVAL;
   return enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
                  status, workspace, workspace_bytes, stream, nullptr, recv_counts, send_offsets, token_slot);
+}
+
+int topoep_costs_workspace_bytes(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
+                                 size_t *bytes_out) {
+  if (!bytes_out) return TOPOEP_EINVAL;
+  Plan p;
+  Shape s;
+  size_t need = 0;
+  const int rc = setup(topo, T, k, replica_budget, nullptr, &p, &s, &need, nullptr, true);
+  if (rc == TOPOEP_OK) *bytes_out = need;
+  return rc;
+}
+
+int topoep_plan_costs(const topoep_topology *topo, const topoep_costs *costs, const int32_t *global_load,
+                      const int32_t *local_topk, int32_t T, int32_t k, int32_t replica_budget,
+                      int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts, int32_t *status,
+                      void *workspace, size_t workspace_bytes, void *stream) {
+  const topoep_costs none = {nullptr, nullptr};
+  return enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
+                 status, workspace, workspace_bytes, stream, nullptr, nullptr, nullptr, nullptr,
+                 costs ? costs : &none);
 }
 
 int topoep_plan_stage(int32_t stage, const topoep_topology *topo, const int32_t *global_load,

@@ -26,6 +26,7 @@ ST_SELF_DIFF = 4
 ST_RANGE = 8
 ST_SYNC = 16
 ST_ITER = 32
+ST_COST = 64
 
 STAGE_HIST = 0
 STAGE_SOLVE = 1
@@ -65,6 +66,12 @@ class Shape(ctypes.Structure):
         return {"kernels": n, "solver": self.solver, "items_per_thread": self.items_per_thread,
                 "chunk_blocks": self.chunk_blocks, "grid": list(self.grid)[:n],
                 "block": list(self.block)[:n], "lds_bytes": list(self.lds_bytes)[:n]}
+
+
+class Costs(ctypes.Structure):
+    """topoep_costs: a general cost matrix [R, R] int32 and per-expert sizes
+    [E] int64 (device pointers; 0 = the topology's two-level values)."""
+    _fields_ = [("cost", ctypes.c_void_p), ("expert_bytes", ctypes.c_void_p)]
 
 
 class TopoepError(RuntimeError):
@@ -111,13 +118,20 @@ _lib.topoep_plan_dispatch.restype = ctypes.c_int
 _lib.topoep_plan_dispatch.argtypes = [ctypes.POINTER(Topology), _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp,
                                       _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
 
+_lib.topoep_costs_workspace_bytes.restype = ctypes.c_int
+_lib.topoep_costs_workspace_bytes.argtypes = [ctypes.POINTER(Topology), _i32, _i32, _i32,
+                                              ctypes.POINTER(ctypes.c_size_t)]
+_lib.topoep_plan_costs.restype = ctypes.c_int
+_lib.topoep_plan_costs.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(Costs), _vp, _vp, _i32, _i32, _i32,
+                                   _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
 _lib.topoep_gather_replicas.restype = ctypes.c_int
 _lib.topoep_gather_replicas.argtypes = [ctypes.POINTER(Topology), _i32, _vp, _vp, _vp, ctypes.c_int64, _vp, _vp]
 
 EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
            "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape",
            "topoep_layout_workspace_bytes", "topoep_dispatch_layout",
-           "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch", "topoep_gather_replicas")
+           "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch", "topoep_gather_replicas",
+           "topoep_costs_workspace_bytes", "topoep_plan_costs")
 
 
 def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
@@ -245,6 +259,58 @@ class Planner:
     def workspace_view(self) -> torch.Tensor:
         off = self.ws_ptr - self._ws.data_ptr()
         return self._ws[off:off + self.ws_bytes]
+
+
+def costs_workspace_bytes(topo: Topology, T: int, k: int, replica_budget: int) -> int:
+    out = ctypes.c_size_t(0)
+    rc = _lib.topoep_costs_workspace_bytes(ctypes.byref(topo), T, k, replica_budget, ctypes.byref(out))
+    if rc != OK:
+        raise TopoepError("topoep_costs_workspace_bytes", rc)
+    return out.value
+
+
+class CostPlanner:
+    """Plans under the full cost model of Section 4.1 (topoep_plan_costs): a
+    general cost matrix (CUDA int32 [R, R]) and/or per-expert sizes (CUDA
+    int64 [E]); None keeps the topology's value."""
+
+    def __init__(self, topo: Topology, T: int, k: int, replica_budget: int, cost=None, expert_bytes=None,
+                 device=None):
+        self.topo = topo
+        self.T, self.k, self.N = int(T), int(k), int(replica_budget)
+        dev = torch.device(device if device is not None else "cuda")
+        R, E = topo.num_ranks, topo.num_experts
+        if cost is not None:
+            _dev_i32(cost, "cost", (R, R))
+        if expert_bytes is not None:
+            if expert_bytes.dtype != torch.int64 or not expert_bytes.is_cuda or tuple(expert_bytes.shape) != (E,):
+                raise TypeError("expert_bytes must be a CUDA int64 tensor of shape [E]")
+        self.cost, self.expert_bytes = cost, expert_bytes
+        self.costs = Costs(cost.data_ptr() if cost is not None else None,
+                           expert_bytes.data_ptr() if expert_bytes is not None else None)
+        self.ws_bytes = costs_workspace_bytes(topo, self.T, self.k, self.N)
+        self._ws, self.ws_ptr = _aligned_workspace(self.ws_bytes, dev)
+        self.replica_slots = torch.empty((R, self.N), dtype=torch.int32, device=dev)
+        self.token_dest = torch.empty((self.T, self.k), dtype=torch.int32, device=dev)
+        self.send_counts = torch.empty((R,), dtype=torch.int32, device=dev)
+        self.status = torch.empty((2,), dtype=torch.int32, device=dev)
+
+    def plan(self, global_load, local_topk, stream=None):
+        """Enqueue topoep_plan_costs; returns (replica_slots, token_dest, send_counts, status)."""
+        R, E = self.topo.num_ranks, self.topo.num_experts
+        _dev_i32(global_load, "global_load", (R, E))
+        t = self.T > 0
+        if t:
+            _dev_i32(local_topk, "local_topk", (self.T, self.k))
+        rc = _lib.topoep_plan_costs(
+            ctypes.byref(self.topo), ctypes.byref(self.costs), global_load.data_ptr(),
+            local_topk.data_ptr() if t else None, self.T, self.k, self.N,
+            self.replica_slots.data_ptr() if self.replica_slots.numel() else None,
+            self.token_dest.data_ptr() if t else None, self.send_counts.data_ptr(), self.status.data_ptr(),
+            self.ws_ptr, self.ws_bytes, _stream_ptr(stream, global_load.device))
+        if rc != OK:
+            raise TopoepError("topoep_plan_costs", rc)
+        return self.replica_slots, self.token_dest, self.send_counts, self.status
 
 
 class DispatchPlanner:

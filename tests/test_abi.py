@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert "topoep_plan" in names and "topoep_workspace_bytes" in names
-    assert len(names) == 11
+    assert len(names) == 13
 
 
 def test_library_exports_every_declared_symbol(tp):
@@ -216,3 +216,27 @@ def test_gather_host_checks(tp):
     # nothing to copy: no launch, OK even on placeholder pointers
     assert G(ctypes.byref(t), 0, None, None, None, 64, None, None) == tp.OK
     assert G(ctypes.byref(t), 2, 256, None, 512, 0, 1024, None) == tp.OK
+
+
+def test_costs_workspace_and_shape(tp):
+    t = base(tp)
+    n = tp.costs_workspace_bytes(t, 512, 2, 1)
+    assert n > 0 and n % 256 == 0
+    out = ctypes.c_size_t(0)
+    # a domain too large for one workgroup's LDS with the cost tables
+    big = base(tp, R=256, G=64, E=256 * 60)
+    assert tp._lib.topoep_costs_workspace_bytes(ctypes.byref(big), 16, 1, 4, ctypes.byref(out)) == tp.ELIMIT
+    assert tp._lib.topoep_costs_workspace_bytes(ctypes.byref(t), -1, 1, 1, ctypes.byref(out)) == tp.EINVAL
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="launches on placeholder pointers: only where no GPU is present")
+def test_valid_costs_call_reaches_the_launch(tp):
+    t = base(tp)
+    ws = tp.costs_workspace_bytes(t, 16, 2, 1)
+    c = tp.Costs(4096, 8192)
+    assert tp._lib.topoep_plan_costs(ctypes.byref(t), ctypes.byref(c), 256, 256, 16, 2, 1, 512, 1024, 2048,
+                                     2560, 8192 * 2, ws, None) == tp.EHIP
+    assert tp._lib.topoep_plan_costs(ctypes.byref(t), None, 256, 256, 16, 2, 1, 512, 1024, 2048,
+                                     2560, 8192 * 2, ws, None) == tp.EHIP
+    assert tp._lib.topoep_plan_costs(ctypes.byref(t), ctypes.byref(c), None, 256, 16, 2, 1, 512, 1024, 2048,
+                                     2560, 8192 * 2, ws, None) == tp.EINVAL
