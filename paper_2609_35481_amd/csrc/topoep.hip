@@ -98,6 +98,26 @@ struct Plan {
 };
 
 
+// The solvers hold more uniform values (sizes, divisors, LDS offsets,
+// pointers) than the scalar register file takes; the spilled ones come back
+// lane by lane (v_readlane) all over the solver.  A value passed through
+// vgpr() is kept in a vector register instead (LDS addresses and the
+// divisions' multiplies take vector operands anyway).
+__device__ inline int vgpr(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// The plan with its divisors in vector registers (see vgpr).
+__device__ inline Plan solver_plan(Plan q) {
+  FastDiv *fds[] = {&q.fE, &q.fG, &q.fGP, &q.fP, &q.fI, &q.fPN, &q.fCap, &q.fG1, &q.fN, &q.fMI};
+  for (FastDiv *f : fds) {
+    f->m = (uint32_t)vgpr((int)f->m);
+    f->sh = (uint32_t)vgpr((int)f->sh);
+  }
+  return q;
+}
+
 // Scratch words of the histogram reduction (hist_from_partials, load_fast)
 // for up to 1024 threads: max(E, 4 * threads).
 __host__ __device__ inline int hist_scratch_words(const Plan &p) { return imax(p.E, 4 * 1024); }
@@ -1149,14 +1169,18 @@ __device__ GenCost general_tables(const Plan &p, int d, int *sm, const DomainLds
 
 // ---------------------------------------------------------------- solver: one workgroup per domain
 
-__global__ __launch_bounds__(1024) void solve_kernel(Plan p) {
+__global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   extern __shared__ int64_t smem_s[];
   int *sm = reinterpret_cast<int *>(smem_s);
-  if ((int)blockIdx.x >= p.n_solvers) {
-    block_offsets(p, blockIdx.x - p.n_solvers, sm);
+  if ((int)blockIdx.x >= p0.n_solvers) {
+    block_offsets(p0, blockIdx.x - p0.n_solvers, sm);
     return;
   }
-  const DomainLds lay = domain_lds(p);
+  const Plan p = solver_plan(p0);
+  DomainLds lay = domain_lds(p);
+  int *offs[] = {&lay.ck, &lay.fdt, &lay.hs, &lay.rows, &lay.mask, &lay.slots, &lay.used, &lay.L,
+                 &lay.e_of, &lay.U, &lay.misc, &lay.qcol, &lay.ord, &lay.ccol, &lay.wx};
+  for (int *o : offs) *o = vgpr(*o);
   uint64_t *ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
   FastDiv *fdt = reinterpret_cast<FastDiv *>(sm + lay.fdt);
   int *hs = sm + lay.hs;
@@ -1433,7 +1457,26 @@ struct SingleState {
 };
 
 __device__ inline SingleState single_state(const Plan &p, int *sm) {
-  const SingleLds lay = single_lds(p);
+  SingleLds lay = single_lds(p);
+  lay.ck = vgpr(lay.ck);
+  lay.em = vgpr(lay.em);
+  lay.fdt = vgpr(lay.fdt);
+  lay.hs = vgpr(lay.hs);
+  lay.cnt = vgpr(lay.cnt);
+  lay.dfree = vgpr(lay.dfree);
+  lay.mask = vgpr(lay.mask);
+  lay.bm = vgpr(lay.bm);
+  lay.sendl = vgpr(lay.sendl);
+  lay.wt = vgpr(lay.wt);
+  lay.repl = vgpr(lay.repl);
+  lay.slots = vgpr(lay.slots);
+  lay.used = vgpr(lay.used);
+  lay.L = vgpr(lay.L);
+  lay.e_of = vgpr(lay.e_of);
+  lay.U = vgpr(lay.U);
+  lay.misc = vgpr(lay.misc);
+  lay.om = vgpr(lay.om);
+  lay.qcol = vgpr(lay.qcol);
   SingleState t;
   t.ck = reinterpret_cast<uint64_t *>(sm + lay.ck);
   t.em = reinterpret_cast<uint64_t *>(sm + lay.em);
@@ -1653,13 +1696,14 @@ __device__ void solver_send_offsets(const Plan &p, const int *sendl) {
 // domain's refinement runs on its own wave.  Used when Omega and all q
 // columns fit in LDS.  Workgroups beyond the first compute the histogram
 // blocks' offsets for the reroute.
-__global__ __launch_bounds__(1024) void solve_single_kernel(Plan p) {
+__global__ __launch_bounds__(1024) void solve_single_kernel(Plan p0) {
   extern __shared__ int64_t smem_1[];
   int *sm = reinterpret_cast<int *>(smem_1);
   if (blockIdx.x > 0) {
-    block_offsets(p, blockIdx.x - 1, sm);
+    block_offsets(p0, blockIdx.x - 1, sm);
     return;
   }
+  const Plan p = solver_plan(p0);
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E, R = p.R;
   single_init(p, t);
@@ -2348,7 +2392,7 @@ __global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
   int *sm = reinterpret_cast<int *>(smem_f);
   (void)p;
   if (blockIdx.x == 0) {
-    const Plan q = role_plan(p);
+    const Plan q = solver_plan(role_plan(p));
     fused_solver(q, sm);
   } else {
     const Plan q = role_plan(p);
