@@ -759,19 +759,26 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     }
   }
   wave_sync();
-  const int ncand = PN * (G - 1);
-  // the lane's first two candidates (instance position ai on rb, target index jj)
-  int ai0 = 0, jj0 = 0, ai1 = 0, jj1 = 0;
-  if (lane < ncand) {
-    ai0 = (int)fdiv((uint32_t)lane, p.fG1);
-    jj0 = lane - ai0 * (G - 1);
-  }
-  if (lane + 64 < ncand) {
-    ai1 = (int)fdiv((uint32_t)(lane + 64), p.fG1);
-    jj1 = lane + 64 - ai1 * (G - 1);
-  }
+  // One lane per instance of rb.  Among the targets an instance may move to
+  // (the domain's other ranks with L[rt] <= L[rb] - 2 that host its expert
+  // or have a free slot) delta = min(u, (L[rb] - L[rt]) / 2) only grows as
+  // L[rt] falls, so the instance's best keys all sit at its lightest
+  // targets: the lane scores just those (usually one rank) instead of all
+  // G - 1, and the wave keeps the overall minimum of the same key.
+  const int rounds = (PN + 63) >> 6;
+  // with at most 16 ranks the reductions over ranks stay in the first row
+  // of 16 lanes
+  const bool rank_row = G <= 16;
+  auto min_u32 = [&](uint32_t v) { return rows_min_u32(v, rank_row); };
   const int64_t tokc = 2 * p.S * (int64_t)p.cI;   // cost change per moved assignment and unit of (m_rb - m_rt)
   const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
+  // lane j < G keeps rank j's load and used slots in registers (and the
+  // LDS copies current for the other lanes' reads)
+  int lj = 0, uj = 0;
+  if (lane < G) {
+    lj = Lr[lane];
+    uj = used[lane];
+  }
   uint32_t it = 0;
   for (;; ++it) {
     if (it >= p.iter_limit) {
@@ -779,73 +786,104 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
       break;
     }
     // busiest rank, lowest index on ties
-    uint64_t bkey = 0;
-    if (lane < G) bkey = ((uint64_t)(uint32_t)Lr[lane] << 32) | (uint32_t)(0xFFFFFFFFu - lane);
-    bkey = wave_max_u64(bkey);
-    const int rbj = (int)(0xFFFFFFFFu - (uint32_t)bkey);
-    const int Lrb = (int)(bkey >> 32);
+    const int Lrb = (int)~min_u32(lane < G ? ~(uint32_t)lj : ~0u);
+    const int rbj = __ffsll((long long)__ballot(lane < G && lj == Lrb)) - 1;
     const int rb = r0 + rbj;
-    uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull;
-    int best_a = 0;
-    for (int c = lane, round = 0; c - lane < ncand; c += 64, ++round) {
-      if (c >= ncand) continue;
-      int ai, jj;
-      if (round == 0) {
-        ai = ai0;
-        jj = jj0;
-      } else if (round == 1) {
-        ai = ai1;
-        jj = jj1;
-      } else {
-        ai = (int)fdiv((uint32_t)c, p.fG1);
-        jj = c - ai * (G - 1);
-      }
-      const int rtj = jj < rbj ? jj : jj + 1;
+    // receivers: delta >= 1 needs L[rt] <= L[rb] - 2; those with a free slot
+    // take any expert, and the lightest of them form one level (lf, tf)
+    const bool low = lane < G && lane != rbj && (int64_t)Lrb - lj >= 2;
+    const uint64_t lowm = __ballot(low);
+    if (lowm == 0) break;
+    const bool fr = low && uj < Neff;
+    uint32_t lf = ~0u;
+    uint64_t tf = 0;
+    if (__ballot(fr)) {
+      lf = min_u32(fr ? (uint32_t)lj : ~0u);
+      tf = __ballot(fr && (uint32_t)lj == lf);
+    }
+    // the first rank of the free level: its q is read with the instance's
+    // own words (it is usually the one target scored)
+    const int jf = tf ? __ffsll((long long)tf) - 1 : 0;
+    uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull, best_hm = 0;
+    int best_a = 0, best_u = 0, best_q = 0;
+    for (int rd = 0; rd < rounds; ++rd) {
+      const int ai = lane + rd * 64;
+      if (ai >= PN) continue;
       const int a = rbj * PN + ai;
+      const int *qa = qcol + a * QS;
+      const bool two_level = !General && p.cI > 0;
       const int e = e_of[a];
       const int u = U[a];
-      const int Lrt = Lr[rtj];
-      const int urt = used[rtj];
+      const int qrb = two_level ? qa[rb] : 0;
+      const int qf = two_level ? qa[r0 + jf] : 0;
       if (e < 0 || u <= 0) continue;
-      const int64_t gap = (int64_t)Lrb - Lrt;
-      if (gap < 2) continue;
-      const bool hosts = (em[e] >> rtj) & 1ull;
-      if (!hosts && urt >= Neff) continue;
-      const int rt = r0 + rtj;
-      const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
-      int64_t dcost = 0;
-      if constexpr (General) {
-        // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
-        const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
-        const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
-        int rest = delta;
-        int64_t dt = 0;
-        for (int k = 0; k < R && rest > 0; ++k) {
-          const int s = o[k];
-          const int take = imin(rest, qcol[a * QS + s]);
-          dt += (int64_t)take * (ct[s] - cb[s]);
-          rest -= take;
+      const uint64_t hmf = em[e];
+      // the lightest receivers already hosting e (no slot needed)
+      uint32_t lh = ~0u;
+      uint64_t th = 0;
+      for (uint64_t h = hmf & lowm; h; h &= h - 1) {
+        const int j = __ffsll((long long)h) - 1;
+        const uint32_t L = (uint32_t)Lr[j];
+        if (L < lh) {
+          lh = L;
+          th = 0;
         }
-        dcost = 2 * p.S * dt;
-        if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
-      } else {
-        if (p.cI > 0) {
-          const int qrt = qcol[a * QS + rt], qrb = qcol[a * QS + rb];
-          const int m_rt = imin(delta, qrt);
-          const int rest = delta - m_rt;
-          const int m_rb = rest - imin(rest, u - qrt - qrb);
-          dcost = tokc * (int64_t)(m_rb - m_rt);
-        }
-        if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+        if (L == lh) th |= 1ull << j;
       }
-      const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
-      const uint64_t c2 = (uint64_t)dcost ^ (1ull << 63);
-      const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)rt;
+      const uint32_t lm = lf < lh ? lf : lh;
+      if (lm == ~0u) continue;
+      const uint64_t tset = (lf == lm ? tf : 0) | (lh == lm ? th : 0);
+      const int delta = imin(u, (Lrb - (int)lm) >> 1);
+      // lowest (cost change, rt) among the lightest receivers
+      int64_t bc = INT64_MAX;
+      int bj = 0, bq = 0;
+      for (uint64_t t = tset; t; t &= t - 1) {
+        const int rtj = __ffsll((long long)t) - 1;
+        const bool hosts = (hmf >> rtj) & 1ull;
+        const int rt = r0 + rtj;
+        int64_t dcost = 0;
+        int qrt = 0;
+        if constexpr (General) {
+          // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
+          const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
+          const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
+          int rest = delta;
+          int64_t dt = 0;
+          for (int k = 0; k < R && rest > 0; ++k) {
+            const int s2 = o[k];
+            const int take = imin(rest, qa[s2]);
+            dt += (int64_t)take * (ct[s2] - cb[s2]);
+            rest -= take;
+          }
+          dcost = 2 * p.S * dt;
+          if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
+        } else {
+          if (p.cI > 0) {
+            qrt = rtj == jf ? qf : qa[rt];
+            const int m_rt = imin(delta, qrt);
+            const int rest = delta - m_rt;
+            const int m_rb = rest - imin(rest, u - qrt - qrb);
+            dcost = tokc * (int64_t)(m_rb - m_rt);
+          }
+          if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+        }
+        if (dcost < bc) {
+          bc = dcost;
+          bj = rtj;
+          bq = qrt;
+        }
+      }
+      const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm;
+      const uint64_t c2 = (uint64_t)bc ^ (1ull << 63);
+      const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj);
       if (lex_less(c1, c2, c3, k1, k2, k3)) {
         k1 = c1;
         k2 = c2;
         k3 = c3;
         best_a = a;
+        best_u = u;
+        best_hm = hmf;
+        best_q = bq;
       }
     }
     const uint64_t m1 = wave_min_u64(k1);
@@ -860,29 +898,37 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
       }
     }
     const int wl = __ffsll((long long)win) - 1;
-    const int delta = 0x7FFFFFFF - (int)(readlane64(k1, wl) >> 32);
+    const uint64_t kw1 = readlane64(k1, wl);
+    const int delta = 0x7FFFFFFF - (int)(kw1 >> 32);
+    const int Lrt = (int)(uint32_t)kw1;
     const uint64_t kw = readlane64(k3, wl);
     const int e = (int)(kw >> 32);
     const int rt = (int)(uint32_t)kw;
     const int rtj = rt - r0;
     const int a = readlane_i32(best_a, wl);
-    int a2 = instance_of(p, d, rtj, e, slots, used);
-    wave_sync();
-    if (a2 < 0) {
-      // new replica in the first free slot of rt
-      const int t = used[rtj];
-      a2 = rtj * PN + P + t;
-      if (lane == 0) {
-        slots[rtj * Neff + t] = e;
-        used[rtj] = t + 1;
-        e_of[a2] = e;
-        em[e] |= 1ull << rtj;
+    const int ua = readlane_i32(best_u, wl);
+    const int qrt = readlane_i32(best_q, wl);
+    const bool hosts = (readlane64(best_hm, wl) >> rtj) & 1ull;
+    // rt's instance of e: its main expert, the replica slot holding it, or a
+    // new replica in rt's first free slot
+    int a2 = -1;
+    bool fresh = false;
+    if (!hosts) {
+      a2 = rtj * PN + P + readlane_i32(uj, rtj);
+      fresh = true;
+    } else if ((int)fdiv((uint32_t)e, p.fP) == rt) {
+      a2 = rtj * PN + (e - rt * P);
+    } else {
+      const int ut = readlane_i32(uj, rtj);
+      for (int t0 = 0; t0 < ut && a2 < 0; t0 += 64) {
+        const uint64_t hit = __ballot(t0 + lane < ut && slots[rtj * Neff + t0 + lane] == e);
+        if (hit) a2 = rtj * PN + P + t0 + __ffsll((long long)hit) - 1;
       }
     }
-    wave_sync();
     int *qa = qcol + a * QS;
     int *qb = qcol + a2 * QS;
     int rest = delta;
+    int m_rt = 0;
     if constexpr (General) {
       // the sources in the pair's order, 64 at a time
       const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
@@ -895,20 +941,17 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
         int m = rest - excl;
         m = m < 0 ? 0 : (m > av ? av : m);
         if (m) {
-          qa[s] -= m;
-          qb[s] += m;
+          qa[s] = av - m;
+          atomicAdd(&qb[s], m);
         }
         const int total = readlane_i32(incl, 63);
         rest -= total < rest ? total : rest;
       }
     } else {
+      // rt's own assignments first, then the other sources ascending (rb's
+      // own are taken last, below)
       if (p.cI > 0) {
-        const int m_rt = imin(rest, qa[rt]);
-        wave_sync();
-        if (lane == 0 && m_rt) {
-          qa[rt] -= m_rt;
-          qb[rt] += m_rt;
-        }
+        m_rt = imin(rest, qrt);
         rest -= m_rt;
       }
       for (int s0 = 0; s0 < R && rest > 0; s0 += 64) {
@@ -920,23 +963,39 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
         int m = rest - excl;
         m = m < 0 ? 0 : (m > av ? av : m);
         if (m) {
-          qa[s] -= m;
-          qb[s] += m;
+          qa[s] = av - m;
+          atomicAdd(&qb[s], m);
         }
         const int total = readlane_i32(incl, 63);
         rest -= total < rest ? total : rest;
       }
     }
-    wave_sync();
+    // (the sources above exclude rt and rb, so these words are disjoint
+    // from the lanes' updates; LDS atomics without return need no wait)
     if (lane == 0) {
-      if (rest > 0) {   // the rest comes from rb itself (two-level cost, taken last)
-        qa[rb] -= rest;
-        qb[rb] += rest;
+      if (fresh) {
+        slots[rtj * Neff + (a2 - rtj * PN - P)] = e;
+        used[rtj] = a2 - rtj * PN - P + 1;
+        e_of[a2] = e;
+        atomicOr(reinterpret_cast<unsigned long long *>(&em[e]), 1ull << rtj);
       }
-      U[a] -= delta;
-      U[a2] += delta;
-      Lr[rbj] -= delta;
-      Lr[rtj] += delta;
+      if (m_rt) {
+        atomicSub(&qa[rt], m_rt);
+        atomicAdd(&qb[rt], m_rt);
+      }
+      if (rest > 0) {   // the rest comes from rb itself (two-level cost, taken last)
+        atomicSub(&qa[rb], rest);
+        atomicAdd(&qb[rb], rest);
+      }
+      U[a] = ua - delta;
+      atomicAdd(&U[a2], delta);
+      Lr[rbj] = Lrb - delta;
+      Lr[rtj] = Lrt + delta;
+    }
+    if (lane == rbj) lj = Lrb - delta;
+    if (lane == rtj) {
+      lj = Lrt + delta;
+      uj += fresh ? 1 : 0;
     }
     wave_sync();
   }

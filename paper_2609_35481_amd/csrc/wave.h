@@ -75,6 +75,41 @@ __device__ inline uint64_t wave_min_u64(uint64_t v) {
 
 __device__ inline uint64_t wave_max_u64(uint64_t v) { return ~wave_min_u64(~v); }
 
+__device__ inline uint32_t wave_min_u32(uint32_t v) {
+  uint32_t o;
+  o = dpp_mov<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov<0x121>(v); v = o < v ? o : v;
+  uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0), b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+  uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32), d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+  a = b < a ? b : a;
+  c = d < c ? d : c;
+  return c < a ? c : a;
+}
+
+__device__ inline uint32_t wave_max_u32(uint32_t v) { return ~wave_min_u32(~v); }
+
+// Minimum with the candidates known to sit in lanes 0..15 when rows1 (the
+// other rows are then ignored): one readlane instead of four.
+__device__ inline uint32_t rows_min_u32(uint32_t v, bool rows1) {
+  uint32_t o;
+  o = dpp_mov<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov<0x121>(v); v = o < v ? o : v;
+  uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+  if (!rows1) {
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    a = b < a ? b : a;
+    a = c < a ? c : a;
+    a = d < a ? d : a;
+  }
+  return a;
+}
+
 __device__ inline uint64_t wave_sum_u64(uint64_t v) {
   v += dpp_mov64<0x128>(v);
   v += dpp_mov64<0x124>(v);

@@ -161,6 +161,49 @@ def test_config_larger_budget(name, N):
     both(*cfg_args(cfg, 0, gl, tk, N=N), what="%s N=%d" % (name, N))
 
 
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("R,E,N", [(8, 640, 2), (8, 512, 6), (16, 640, 4), (8, 64, 1), (4, 320, 3)])
+def test_many_instances_per_rank(R, E, N, solver):
+    """The solver-scaling rows: up to 80 main experts per rank (more than one
+    wavefront of instances on the busiest rank) and tens of refinement moves
+    per layer."""
+    cfg = workload.Config("scale", 6, R=R, G=min(R, 8), E=E, k=8, T=4096, N=N, c_intra=1, c_inter=8,
+                          S=2048 * 2, W=3 * 2048 * 768 * 2, layers=1, microbatches=1, zipf_s=1.0)
+    gl, tk = workload.make_layer(cfg, 0, 0, 0)
+    both(*cfg_args(cfg, 0, gl, np.ascontiguousarray(tk)), launch=SOLVERS[solver],
+         what="R=%d E=%d N=%d %s" % (R, E, N, solver))
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_refinement_equal_loads(seed):
+    """Receivers tied on load: every token count a multiple of a large unit,
+    so many ranks share one load level and the cost change and rank order
+    break the ties."""
+    rng = np.random.default_rng(9500 + seed)
+    G = int(rng.choice([4, 8]))
+    M = int(rng.choice([1, 2]))
+    R, P = G * M, int(rng.choice([1, 2, 3]))
+    E = R * P
+    k = int(rng.integers(1, min(E, 3) + 1))
+    N = int(rng.integers(2, 6))
+    hot = rng.choice(E, size=max(1, E // 4), replace=False)
+    pop = np.full(E, 1.0)
+    pop[hot] = 8.0
+    pop /= pop.sum()
+    T = int(rng.integers(16, 64)) * 4
+    topks = [np.stack([rng.choice(E, size=k, replace=False, p=pop) for _ in range(T)]).astype(np.int32)
+             for _ in range(R)]
+    omega = np.stack([np.bincount(x.ravel(), minlength=E) for x in topks]).astype(np.int32)
+    omega = (omega // 4) * 4
+    s = int(rng.integers(R))
+    tk = topks[s]
+    omega[s] = np.bincount(tk.ravel(), minlength=E)
+    cI = int(rng.integers(0, 2))
+    both(R, G, E, s, cI, cI + int(rng.integers(0, 6)), int(rng.integers(1, 9)), int(rng.integers(1, 200)), N,
+         omega, tk, launch=SOLVERS[["single", "perdomain", "fused"][seed % 3]],
+         what="equal loads seed %d" % seed)
+
+
 @pytest.mark.parametrize("name", ["tiny", "qwen3"])
 def test_every_self_rank_agrees(name):
     """Every rank derives the same replica slots; send counts add up to the
