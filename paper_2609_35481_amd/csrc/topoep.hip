@@ -537,8 +537,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
       const bool inr = idx < hi;
       const bool valid = inr && (unsigned)ev[i] < (unsigned)p.E;
       bad |= (inr && !valid) ? 1 : 0;
-      const uint64_t peers = peer_mask(ev[i], valid, p.nbits);
-      if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&h[ev[i]], __popcll(peers));
+      if (valid) atomicAdd(&h[ev[i]], 1);
     }
   }
   bad = __syncthreads_or(bad);
