@@ -65,7 +65,8 @@ constexpr uint32_t kVerdictRedo = 2;
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE | TOPOEP_ST_COST;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
 constexpr int kMaxSolveGroups = 128;    // co-resident by a wide margin (256 CUs)
-constexpr int kTargetBlocks = 1024;     // histogram/reroute blocks to aim for
+constexpr int kMinBlocks = 2048;        // histogram/reroute blocks to aim for, at least
+constexpr int kMaxBlocks = 8192;        // and at most
 constexpr int kOffsetExperts = 64;      // experts per offset workgroup
 constexpr int kFusedBlocks = 64;        // chunk workgroups the single-launch plan aims for
 constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs)
@@ -2585,8 +2586,12 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   if (s.mode != 3) {
   const int64_t tile = (int64_t)s.bt * s.ipt;
   const int64_t tiles = (q.n + tile - 1) / tile;
-  int64_t tpb = lc && lc->tiles_per_block > 0 ? lc->tiles_per_block
-                                              : (tiles + kTargetBlocks - 1) / kTargetBlocks;
+  // about 16 K ids per block, 2048..8192 blocks: every CU keeps eight
+  // 256-thread blocks resident with work to spare, while the solver's
+  // per-block offset scan (nb words per expert) stays short
+  const int64_t want = q.n / 16384;
+  const int64_t target = want < kMinBlocks ? kMinBlocks : (want > kMaxBlocks ? kMaxBlocks : want);
+  int64_t tpb = lc && lc->tiles_per_block > 0 ? lc->tiles_per_block : (tiles + target - 1) / target;
   if (tpb < 1) tpb = 1;
   q.chunk = tpb * tile;
   const int64_t nb = q.n > 0 ? (q.n + q.chunk - 1) / q.chunk : 1;
