@@ -4,11 +4,14 @@
 // assignments form one contiguous run that an all-to-all dispatch sends as
 // is (the per-destination counts the dispatch consumes, Section 4.3).
 //
-// One pass over token_dest, one launch:
-//   - each workgroup holds a contiguous chunk of assignments in registers
-//     and ranks them among equal destinations inside each wave (ballots
-//     over the destination bits give each lane its peers), then scans the
-//     per-wave counts across waves in LDS;
+// One launch; one pass over token_dest for a chunk of one tile per
+// workgroup, two passes for longer chunks (at most 256 workgroups):
+//   - a one-tile workgroup holds its assignments in registers and ranks
+//     them among equal destinations inside each wave (ballots over the
+//     destination bits give each lane its peers), then scans the per-wave
+//     counts across waves in LDS; a longer chunk only counts its
+//     destinations here (LDS atomics) and ranks tile by tile after the
+//     look-back, reading the assignments again;
 //   - it publishes its per-destination counts (flag 1), then looks back
 //     over up to 64 predecessors at a time: wave 0 waits for their flags in
 //     parallel and stops at the nearest one whose inclusive prefix is
@@ -16,8 +19,8 @@
 //     destination, and (when the grid is longer than one window plus
 //     workgroup 0) the workgroup publishes its own inclusive prefix (flag
 //     2).  Workgroup 0 publishes its counts as its inclusive prefix;
-//   - slot = send_offsets[dest] + (earlier workgroups) + (earlier waves) +
-//     (rank in the wave).
+//   - slot = send_offsets[dest] + (earlier workgroups) + (earlier tiles of
+//     the chunk) + (earlier waves) + (rank in the wave).
 // The waits are bounded and only on lower workgroup indices, which are
 // dispatched first.  The last workgroup to finish its look-back (a ticket)
 // clears every flag, so the workspace is zero again for the next call.
@@ -35,6 +38,7 @@ using namespace topoep_dev;
 constexpr int kLayoutThreads = 1024;
 constexpr int kLayoutMaxRanks = 1024;   // per-wave counts of 16 waves fit 64 KB of LDS
 constexpr int kLayoutWindow = 64;       // predecessors examined per look-back step
+constexpr int kLayoutBlocks = 256;      // workgroups at most (longer chunks take several tiles)
 constexpr uint32_t kLayoutSpin = 1u << 24;
 constexpr int kLayoutCtrlBytes = 256;
 
@@ -55,9 +59,10 @@ struct Layout {
 
 // LDS words: per-wave counts (then offsets) [nw][R], the workgroup's counts
 // [R], the exclusive prefix over earlier workgroups [R], send offsets
-// [R + 1] and broadcast words.
+// [R + 1], the running slot base of a multi-tile chunk [R] and broadcast
+// words.
 struct LayoutLds {
-  int wc, agg, excl, offs, misc, words;
+  int wc, agg, excl, offs, run, misc, words;
 };
 
 __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
@@ -67,9 +72,44 @@ __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
   l.agg = o; o += R;
   l.excl = o; o += R;
   l.offs = o; o += R + 1;
+  l.run = o; o += R;
   l.misc = o; o += 8;
   l.words = o;
   return l;
+}
+
+// Rank of each of the wave's IPT x 64 assignments among the wave's earlier
+// ones with the same destination (index order: i, then lane) into lr, and
+// the wave's count of every destination into its row of wc.
+template <int IPT>
+__device__ inline void rank_wave(int R, int nbits, const int (&dv)[IPT], int (&lr)[IPT], int *mywc) {
+  const int lane = lane_id();
+  for (int r = lane; r < R; r += 64) mywc[r] = 0;
+  wave_sync();
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const bool valid = (unsigned)dv[i] < (unsigned)R;
+    const uint64_t peers = peer_mask(dv[i], valid, nbits);
+    const int c = valid ? mywc[dv[i]] : 0;
+    lr[i] = c + __popcll(peers & lanemask_lt());
+    wave_sync();
+    if (valid && (peers & lanemask_lt()) == 0) mywc[dv[i]] = c + __popcll(peers);
+    wave_sync();
+  }
+}
+
+// Per destination: the waves' counts in wc become their offsets (one 16-lane
+// scan per rank, lane w holding wave w's count) and tot[r] the row's total.
+__device__ inline void scan_waves(int R, int nw, int *wc, int *tot) {
+  const int rows = R * 16, span = (rows + 63) & ~63;
+  for (int t = threadIdx.x; t < span; t += blockDim.x) {
+    const int r = t >> 4, w = t & 15;
+    const bool in = t < rows && w < nw;
+    const int c = in ? wc[w * R + r] : 0;
+    const int incl = row16_incl_scan(c);
+    if (in) wc[w * R + r] = incl - c;
+    if (t < rows && w == 15) tot[r] = incl;
+  }
 }
 
 template <int IPT>
@@ -78,71 +118,69 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
   const int R = L.R, tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   const LayoutLds l = layout_lds(R, nt);
-  int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs;
+  int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs, *run = lsm + l.run;
   int *misc = lsm + l.misc;
   const int64_t lo = (int64_t)b * L.chunk;
   const int64_t hi = lo + L.chunk < L.n ? lo + L.chunk : L.n;
-  const int64_t wbase = lo + (int64_t)wave * 64 * IPT + lane;
+  const int64_t tile = (int64_t)nt * IPT;
+  // a chunk of one tile keeps its ids and ranks in registers across the
+  // look-back; a longer chunk counts its tiles first (pass 1) and ranks them
+  // after the look-back (pass 2), reading the ids twice
+  const bool multi = L.chunk > tile;
+  const int64_t wofs = (int64_t)wave * 64 * IPT + lane;
   // workgroups whose look-back window reaches workgroup 0 never need the
   // inclusive prefix of another one
   const bool publish_incl = L.nb > kLayoutWindow + 1;
+  int *mywc = wc + wave * R;
 
   int dv[IPT], lr[IPT];
-#pragma unroll
-  for (int i = 0; i < IPT; ++i) {
-    const int64_t idx = wbase + i * 64;
-    dv[i] = idx < hi ? L.dest[idx] : -1;
-  }
   for (int r = tid; r < R; r += nt) {
     offs[r] = L.send[r];
     excl[r] = 0;
   }
   if (tid < 8) misc[tid] = 0;
-  // rank of each assignment among the wave's earlier ones with the same
-  // destination (index order: i, then lane); each wave owns its row of wc
-  int *mywc = wc + wave * R;
-  for (int r = lane; r < R; r += 64) mywc[r] = 0;
-  wave_sync();
+  if (!multi) {
 #pragma unroll
-  for (int i = 0; i < IPT; ++i) {
-    const bool valid = (unsigned)dv[i] < (unsigned)R;
-    const uint64_t peers = peer_mask(dv[i], valid, L.nbits);
-    const int c = valid ? mywc[dv[i]] : 0;
-    lr[i] = c + __popcll(peers & lanemask_lt());
+    for (int i = 0; i < IPT; ++i) {
+      const int64_t idx = lo + wofs + i * 64;
+      dv[i] = idx < hi ? L.dest[idx] : -1;
+    }
+    rank_wave<IPT>(R, L.nbits, dv, lr, mywc);
+  } else {
+    // pass 1: the chunk's count of every destination, one LDS atomic per
+    // assignment into the wave's own row
+    for (int r = lane; r < R; r += 64) mywc[r] = 0;
     wave_sync();
-    if (valid && (peers & lanemask_lt()) == 0) mywc[dv[i]] = c + __popcll(peers);
-    wave_sync();
+    for (int64_t base = lo; base < hi; base += tile) {
+#pragma unroll
+      for (int i = 0; i < IPT; ++i) {
+        const int64_t idx = base + wofs + i * 64;
+        dv[i] = idx < hi ? L.dest[idx] : -1;
+      }
+#pragma unroll
+      for (int i = 0; i < IPT; ++i)
+        if ((unsigned)dv[i] < (unsigned)R) atomicAdd(&mywc[dv[i]], 1);
+    }
   }
   lds_barrier();
-  // per destination: offsets of the waves (one 16-lane scan per rank, lane w
-  // holding wave w's count) and the workgroup's count (the row's total)
-  {
-    const int rows = R * 16, span = (rows + 63) & ~63;
-    for (int t = tid; t < span; t += nt) {
-      const int r = t >> 4, w = t & 15;
-      const bool in = t < rows && w < nw;
-      const int c = in ? wc[w * R + r] : 0;
-      const int incl = row16_incl_scan(c);
-      if (in) wc[w * R + r] = incl - c;
-      if (t < rows && w == 15) {
-        agg[r] = incl;
-        L.agg[(int64_t)b * R + r] = (uint32_t)incl;
-        if (b == 0) L.incl[r] = (uint32_t)incl;
-      }
-    }
+  scan_waves(R, nw, wc, agg);
+  lds_barrier();
+  for (int r = tid; r < R; r += nt) {
+    L.agg[(int64_t)b * R + r] = (uint32_t)agg[r];
+    if (b == 0) L.incl[r] = (uint32_t)agg[r];
   }
   // send offsets (exclusive prefix of the send counts) by wave 0
   if (wave == 0) {
     const int per = (R + 63) / 64, a0 = imin(R, lane * per), a1 = imin(R, a0 + per);
     int sum = 0;
     for (int r = a0; r < a1; ++r) sum += offs[r];
-    int run = wave_incl_scan(sum) - sum;
+    int acc = wave_incl_scan(sum) - sum;
     for (int r = a0; r < a1; ++r) {
       const int c = offs[r];
-      offs[r] = run;
-      run += c;
+      offs[r] = acc;
+      acc += c;
     }
-    if (lane == 63) offs[R] = run;
+    if (lane == 63) offs[R] = acc;
   }
   drain_then_barrier();
   if (tid == 0)
@@ -206,13 +244,41 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     if (tid == 0)
       __hip_atomic_store(L.flags + b, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   }
+  if (!multi) {
 #pragma unroll
-  for (int i = 0; i < IPT; ++i) {
-    const int64_t idx = wbase + i * 64;
-    if (idx < hi) {
-      const int d = dv[i];
-      const bool valid = ok && (unsigned)d < (unsigned)R;
-      L.slot_out[idx] = valid ? offs[d] + excl[d] + wc[wave * R + d] + lr[i] : -1;
+    for (int i = 0; i < IPT; ++i) {
+      const int64_t idx = lo + wofs + i * 64;
+      if (idx < hi) {
+        const int d = dv[i];
+        const bool valid = ok && (unsigned)d < (unsigned)R;
+        L.slot_out[idx] = valid ? offs[d] + excl[d] + mywc[d] + lr[i] : -1;
+      }
+    }
+  } else {
+    // pass 2: tile by tile, slot = base of the destination before the tile
+    // + offset of the wave + rank in the wave
+    for (int r = tid; r < R; r += nt) run[r] = offs[r] + excl[r];
+    for (int64_t base = lo; base < hi; base += tile) {
+#pragma unroll
+      for (int i = 0; i < IPT; ++i) {
+        const int64_t idx = base + wofs + i * 64;
+        dv[i] = idx < hi ? L.dest[idx] : -1;
+      }
+      rank_wave<IPT>(R, L.nbits, dv, lr, mywc);
+      lds_barrier();
+      scan_waves(R, nw, wc, agg);
+      lds_barrier();
+#pragma unroll
+      for (int i = 0; i < IPT; ++i) {
+        const int64_t idx = base + wofs + i * 64;
+        if (idx < hi) {
+          const int d = dv[i];
+          const bool valid = ok && (unsigned)d < (unsigned)R;
+          L.slot_out[idx] = valid ? run[d] + mywc[d] + lr[i] : -1;
+        }
+      }
+      lds_barrier();
+      for (int r = tid; r < R; r += nt) run[r] += agg[r];
     }
   }
   // this workgroup has read every flag it needs: the last one to get here
@@ -254,12 +320,14 @@ int layout_setup(const topoep_topology *t, int32_t T, int32_t k, Layout *out, La
   L.R = R;
   L.nbits = ceil_log2(R);
   L.n = (int64_t)T * k;
-  // ids per thread: the fewest that keep the grid at most 4096 workgroups
-  int ipt = 1;
-  while (ipt < 8 && L.n > (int64_t)kLayoutThreads * ipt * 4096) ipt *= 2;
-  if (L.n <= (int64_t)kLayoutThreads * 16) ipt = 1;
-  else if (ipt < 4) ipt = 4;
-  L.chunk = (int64_t)kLayoutThreads * ipt;
+  // ids per thread, then whole tiles per workgroup so that the grid stays
+  // within kLayoutBlocks workgroups, half that up to 2^21 ids (the look-back
+  // chain grows with the grid; on MI355X these bounds measured fastest)
+  const int ipt = L.n <= (int64_t)kLayoutThreads * 16 ? 1 : (L.n <= (int64_t)1 << 20 ? 4 : 8);
+  const int64_t tile = (int64_t)kLayoutThreads * ipt;
+  const int64_t tiles = L.n > 0 ? (L.n + tile - 1) / tile : 1;
+  const int64_t max_blocks = L.n <= ((int64_t)1 << 21) ? kLayoutBlocks / 2 : kLayoutBlocks;
+  L.chunk = tile * ((tiles + max_blocks - 1) / max_blocks);
   const int64_t nb = L.n > 0 ? (L.n + L.chunk - 1) / L.chunk : 1;
   if (nb > (1 << 20)) return TOPOEP_ELIMIT;
   L.nb = (int)nb;

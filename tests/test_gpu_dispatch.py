@@ -178,6 +178,8 @@ def layout_case(R, n, rng, k=8, invalid=0.0, skew=None):
     (1024, 200000, 0.01, 0.8),      # the most ranks
     (64, (1 << 20) + 24, 0.0, 1.2),   # 256 workgroups: look-back across windows
     (7, 8 * 3, 0.0, None),          # smaller than one wave
+    (32, 5000000, 0.01, 1.0),       # 2 tiles per workgroup: counts first, ranks after the look-back
+    (256, (1 << 24) + 8 * 13, 0.0, 1.4),   # 5 tiles per workgroup, ragged last tile
 ])
 def test_layout_alone(R, n, invalid, skew):
     say("layout R=%d n=%d" % (R, n))
