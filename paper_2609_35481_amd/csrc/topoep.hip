@@ -2065,7 +2065,7 @@ __device__ void collect_counts(const Plan &p, int *hs, int *misc) {
 // histogram with row self of Omega, that plan stands (equal rows, so Omega'
 // = Omega) or is made again from Omega' on fresh state; then every chunk's
 // flag 2.
-__device__ void fused_solver(const Plan &p, int *sm) {
+__device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
   if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
@@ -2217,8 +2217,9 @@ __device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
 // rank (lane w of a row holds wave w's count); then the slots.  offs: the
 // send offsets.
 template <int IPT>
-__device__ void chunk_slots(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi, const int *run,
-                            const int *ptr, const int *er, const int *eend, const int *offs, int *excl, int *wc) {
+__device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi,
+                                            const int *run, const int *ptr, const int *er, const int *eend,
+                                            const int *offs, int *excl, int *wc) {
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int R = p.R, E = p.E;
   for (int e = tid; e < E; e += nt) {
@@ -2277,7 +2278,7 @@ __device__ void chunk_slots(const Plan &p, const int (&dv)[IPT], int64_t wbase, 
 // instance from this rank's instance list.  A bounded wait that gives up
 // writes -1 and SYNC.
 template <int IPT>
-__device__ void fused_chunk(const Plan &p, int b, int *sm) {
+__device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   const ChunkLds l = chunk_lds(p, blockDim.x);
   int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr, *er = sm + l.er, *eend = sm + l.eend;
   int *gs = sm + l.gs, *so = sm + l.so, *flag = sm + l.flag;
@@ -2531,7 +2532,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
 
   Shape s;
   const int ipt_req = lc ? lc->items_per_thread : 0;
-  s.ipt = ipt_req ? ipt_req : 4;
+  s.ipt = ipt_req ? ipt_req : (q.n >= ((int64_t)1 << 24) ? 8 : 4);   // 8 ids per thread measured ~3 % faster from 2^24 on
   s.bt = lc && lc->block_threads ? lc->block_threads : 256;
   s.st = lc && lc->solve_threads ? lc->solve_threads : 0;
   const int solver = lc ? lc->solver : 0;
