@@ -151,7 +151,7 @@ __host__ __device__ inline DomainLds domain_lds(const Plan &p) {
   o = (o + 3) & ~3;
   l.misc = o;  o += 64;
   l.qcol = o;                                // q[s][e][r] of the domain's instances
-  o += imax(p.I * p.QS, imax(2 * p.E + 2 + p.E * p.RW + 64, hist_scratch_words(p)));
+  o += imax(p.I * p.QS, imax(p.E + 2 + p.E * p.RW + 64 + p.nent_cap, hist_scratch_words(p)));
   // general cost model: per (busiest, target) pair of the domain's ranks the
   // sources in (c(s,rt) - c(s,rb), s) order (16-bit), the costs to the
   // domain's ranks, ||W_e||
@@ -1264,8 +1264,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     const uint32_t cst = general_check(p, misc, &cmax, &wmax);
     if (tid == 0 && cst) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), cst);
   }
-  // ---- row self of Omega: the histogram of local_topk
-  hist_from_partials(p, hs, qcol);
+  // ---- row self of Omega: the histogram of local_topk, in full on the
+  // workgroup of the domain holding self (its stage 1 and receive counts
+  // read every expert); the others sum it later for their own instances'
+  // experts only
+  const int dself = (int)fdiv((uint32_t)p.self, p.fG);
+  const bool has_self = dself < M && dself % nwg == wg;
+  if (has_self) hist_from_partials(p, hs, qcol);
   if (wg == 0)
     for (int b = tid; b < p.nb; b += nt)
       if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
@@ -1354,10 +1359,18 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     }
     // stage-1 slots of the domain's ranks: candidate i sits on local rank
     // i mod G, slot i / G; the chosen ones are a prefix of the list
-    if (tid == 0) {
-      int nsel = 0;
-      while (nsel < cap && (unsigned)p.repl1[(int64_t)d * cap + nsel] < (unsigned)E) ++nsel;
-      misc[3] = nsel;
+    if (tid < 64) {
+      // the chosen ones: the prefix before the first empty entry
+      int nsel = cap;
+      for (int c0 = 0; c0 < cap; c0 += 64) {
+        const int c = c0 + tid;
+        const uint64_t m = __ballot(c < cap && (unsigned)p.repl1[(int64_t)d * cap + c] >= (unsigned)E);
+        if (m) {
+          nsel = c0 + __ffsll((long long)m) - 1;
+          break;
+        }
+      }
+      if (tid == 0) misc[3] = nsel;
     }
     lds_barrier();
     const int nsel = misc[3];
@@ -1374,8 +1387,31 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       else e = (pos - P) < used[j] ? slots[j * Neff + pos - P] : -1;
       e_of[a] = e;
       U[a] = 0;
+      if (!has_self && e >= 0) hs[e] = 0;
     }
     lds_barrier();
+    if (!has_self) {
+      // hs[e] of the domain's instances (distinct experts), the blocks'
+      // partial counts split over thread groups
+      const int groups = imax(1, nt / I);
+      const int per = (p.nb + groups - 1) / groups;
+      for (int t = tid; t < groups * I; t += nt) {
+        const int g = (int)fdiv((uint32_t)t, p.fI), a = t - g * I;
+        const int e = e_of[a];
+        if (e < 0) continue;
+        const int b0 = g * per, b1 = imin(p.nb, b0 + per);
+        int sum = 0;
+        for (int b = b0; b < b1; b += 8) {
+          int v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
+#pragma unroll
+          for (int u = 0; u < 8; ++u) sum += v[u];
+        }
+        if (sum) atomicAdd(&hs[e], sum);
+      }
+      lds_barrier();
+    }
     // whether the domain can refine at all (a rank with a free slot); if not,
     // only the q[self] column is needed, else the columns omega[s][e] of the
     // domain's instances, then q in place
@@ -1451,7 +1487,8 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   if (!misc[4]) return;
   int *cnt = qcol;                                            // E + 1
   uint32_t *bm = reinterpret_cast<uint32_t *>(qcol + E + 2);  // E * RW
-  int *tmp = qcol + E + 2 + E * p.RW;                         // scan scratch
+  int *tmp = qcol + E + 2 + E * p.RW;                         // scan scratch (64)
+  int *cv = tmp + 64;                                         // nent_cap: shares, then their prefix
   for (int e = tid; e <= E; e += nt) cnt[e] = 0;
   for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
   __syncthreads();
@@ -1478,17 +1515,20 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       pos += __popc(row[r >> 5] & ((1u << (r & 31)) - 1u));
       const int j = cnt[e] + pos;
       p.csr_r[j] = r;
-      p.csr_end[j] = q;
+      cv[j] = q;
     }
   }
   __syncthreads();
+  // cumulative shares per expert, in LDS, then out
   for (int e = tid; e < E; e += nt) {
     int run = 0;
     for (int j = cnt[e]; j < cnt[e + 1]; ++j) {
-      run += p.csr_end[j];
-      p.csr_end[j] = run;
+      run += cv[j];
+      cv[j] = run;
     }
   }
+  __syncthreads();
+  for (int j = tid; j < cnt[E]; j += nt) p.csr_end[j] = cv[j];
   __syncthreads();
   if (tid == 0) {
     uint32_t fin = __hip_atomic_load(&p.ctrl[kCtrlStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
