@@ -1358,13 +1358,17 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       continue;
     }
     // stage-1 slots of the domain's ranks: candidate i sits on local rank
-    // i mod G, slot i / G; the chosen ones are a prefix of the list
+    // i mod G, slot i / G; the chosen ones are a prefix of the list (read
+    // once into rows, free after stage 1: cap = G Neff <= G E words)
+    int *sel = rows;
+    for (int c = tid; c < cap; c += nt) sel[c] = p.repl1[(int64_t)d * cap + c];
+    lds_barrier();
     if (tid < 64) {
       // the chosen ones: the prefix before the first empty entry
       int nsel = cap;
       for (int c0 = 0; c0 < cap; c0 += 64) {
         const int c = c0 + tid;
-        const uint64_t m = __ballot(c < cap && (unsigned)p.repl1[(int64_t)d * cap + c] >= (unsigned)E);
+        const uint64_t m = __ballot(c < cap && (unsigned)sel[c] >= (unsigned)E);
         if (m) {
           nsel = c0 + __ffsll((long long)m) - 1;
           break;
@@ -1377,7 +1381,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     for (int j = tid; j < G; j += nt) {
       const int u = nsel > j ? (int)fdiv((uint32_t)(nsel - j + G - 1), p.fG) : 0;
       used[j] = u;
-      for (int t = 0; t < Neff; ++t) slots[j * Neff + t] = t < u ? p.repl1[(int64_t)d * cap + t * G + j] : -1;
+      for (int t = 0; t < Neff; ++t) slots[j * Neff + t] = t < u ? sel[t * G + j] : -1;
     }
     lds_barrier();
     for (int a = tid; a < I; a += nt) {
