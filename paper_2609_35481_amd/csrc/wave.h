@@ -59,8 +59,8 @@ __device__ inline uint64_t readlane64(uint64_t v, int l) {
          (uint32_t)__builtin_amdgcn_readlane((int)v, l);
 }
 
-// Wave-wide minimum / maximum / sum, the same value in every lane: rotations
-// by 8, 4, 2, 1 inside each row of 16 lanes, then the four row results.
+// Wave-wide minimum / sum, the same value in every lane: rotations by 8, 4,
+// 2, 1 inside each row of 16 lanes, then the four row results.
 __device__ inline uint64_t wave_min_u64(uint64_t v) {
   uint64_t o;
   o = dpp_mov64<0x128>(v); v = o < v ? o : v;
@@ -73,25 +73,8 @@ __device__ inline uint64_t wave_min_u64(uint64_t v) {
   return c < a ? c : a;
 }
 
-__device__ inline uint64_t wave_max_u64(uint64_t v) { return ~wave_min_u64(~v); }
-
-__device__ inline uint32_t wave_min_u32(uint32_t v) {
-  uint32_t o;
-  o = dpp_mov<0x128>(v); v = o < v ? o : v;
-  o = dpp_mov<0x124>(v); v = o < v ? o : v;
-  o = dpp_mov<0x122>(v); v = o < v ? o : v;
-  o = dpp_mov<0x121>(v); v = o < v ? o : v;
-  uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0), b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
-  uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32), d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
-  a = b < a ? b : a;
-  c = d < c ? d : c;
-  return c < a ? c : a;
-}
-
-__device__ inline uint32_t wave_max_u32(uint32_t v) { return ~wave_min_u32(~v); }
-
-// Minimum with the candidates known to sit in lanes 0..15 when rows1 (the
-// other rows are then ignored): one readlane instead of four.
+// 32-bit minimum, with the candidates known to sit in lanes 0..15 when
+// rows1 (the other rows are then ignored): one readlane instead of four.
 __device__ inline uint32_t rows_min_u32(uint32_t v, bool rows1) {
   uint32_t o;
   o = dpp_mov<0x128>(v); v = o < v ? o : v;
@@ -145,26 +128,6 @@ __device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t 
   if (a1 != b1) return a1 < b1;
   if (a2 != b2) return a2 < b2;
   return a3 < b3;
-}
-
-// Lexicographic minimum of (k1, k2, k3) over the wave, in every lane: one
-// wave minimum per key, the later ones only when the earlier key ties.
-__device__ inline void wave_argmin3(uint64_t &k1, uint64_t &k2, uint64_t &k3) {
-  const uint64_t m1 = wave_min_u64(k1);
-  uint64_t tie = __ballot(k1 == m1);
-  if (__popcll(tie) == 1) {
-    const int l = __ffsll((long long)tie) - 1;
-    k1 = m1;
-    k2 = readlane64(k2, l);
-    k3 = readlane64(k3, l);
-    return;
-  }
-  const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
-  tie = __ballot(k1 == m1 && k2 == m2);
-  const uint64_t m3 = wave_min_u64((k1 == m1 && k2 == m2) ? k3 : ~0ull);
-  k1 = m1;
-  k2 = m2;
-  k3 = m3;
 }
 
 // Exclusive scan of a[0..n) in place by the whole workgroup; returns the total.
