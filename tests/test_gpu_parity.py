@@ -174,6 +174,33 @@ def test_many_instances_per_rank(R, E, N, solver):
          what="R=%d E=%d N=%d %s" % (R, E, N, solver))
 
 
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("G,M,P,N", [(16, 1, 2, 3), (32, 2, 1, 4), (64, 1, 1, 2), (24, 2, 3, 4), (32, 4, 2, 4), (64, 2, 1, 2)])
+def test_large_nodes(G, M, P, N, solver):
+    """Nodes of 16 to 64 ranks: rank reductions over the whole wavefront,
+    hosting masks of up to 64 ranks, long refinement."""
+    rng = np.random.default_rng(9700 + G * 10 + M * 3 + N)
+    R = G * M
+    E = R * P
+    k = 4
+    pop = rng.dirichlet(np.full(E, 0.3))
+    topks = [np.stack([rng.choice(E, size=k, replace=False, p=pop) for _ in range(int(rng.integers(100, 300)))])
+             .astype(np.int32) for _ in range(R)]
+    omega = np.stack([np.bincount(x.ravel(), minlength=E) for x in topks]).astype(np.int32)
+    s = int(rng.integers(R))
+    ref = ref_plan(R, G, E, s, 1, 8, 64, 1000, N, omega, topks[s])
+    assert ref["move_count"] > 0
+    try:
+        topoep.Planner(topoep.topology(R, G, E, s, 1, 8, 64, 1000), topks[s].shape[0], k, N, device=DEV,
+                       launch=SOLVERS[solver])
+    except topoep.TopoepError as ex:
+        if ex.rc != topoep.ELIMIT:
+            raise
+        pytest.skip("the %s solver's state does not fit one workgroup's LDS here" % solver)
+    both(R, G, E, s, 1, 8, 64, 1000, N, omega, topks[s], launch=SOLVERS[solver],
+         what="G=%d M=%d P=%d N=%d %s" % (G, M, P, N, solver))
+
+
 @pytest.mark.parametrize("seed", range(30))
 def test_refinement_equal_loads(seed):
     """Receivers tied on load: every token count a multiple of a large unit,
