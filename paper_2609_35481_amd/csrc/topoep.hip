@@ -2193,15 +2193,16 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   } else {
     single_plan(p, t, TOPOEP_ST_SYNC, true);
   }
-  // receive counts of a plan that was made (a refused one wrote zeros)
-  if (planned && p.recv_out) single_recv_counts(p, t);
   if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
-  // release: every output, the instance list and the final status before
-  // the flags
+  // release: every output the chunks read (the instance list, the final
+  // status, the send offsets) before the flags
   drain_then_barrier();
   if (tid < 64)
     for (int b = tid; b < p.nb; b += 64)
       __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  // receive counts of a plan that was made (a refused one wrote zeros):
+  // for the caller only, so they are summed while the chunks route
+  if (planned && p.recv_out) single_recv_counts(p, t);
 }
 
 // The last chunk to arrive (every count is written): flag 1 of every chunk,
