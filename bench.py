@@ -20,7 +20,8 @@ thread, then every core, then the host-planning path of Eq. 1: copy the
 inputs to the host, plan there, copy the outputs back).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config dsv3]
-       python bench.py --sweep    (histogram/reroute bandwidth sweep)
+       python bench.py --sweep    (histogram/reroute/layout bandwidth sweep; with
+                                   --pmc-pass it ends with the counter calibration copy)
 """
 from __future__ import annotations
 
@@ -510,9 +511,9 @@ def run_sweep(args):
 
     dev = torch.device("cuda:0")
     rows = []
-    for E in (128, 512):
+    for E in [int(x) for x in args.sweep_experts.split(",")]:
         R, G = 32, 8
-        for lg in range(16, args.sweep_max_log2 + 1, 2):
+        for lg in range(args.sweep_min_log2, args.sweep_max_log2 + 1, 2):
             n = 1 << lg
             k = 8
             T = n // k
@@ -560,6 +561,13 @@ def run_sweep(args):
             print(json.dumps(rows[-1]), flush=True)
             del pl, lp, tk_d, gl
             torch.cuda.empty_cache()
+    if args.pmc_pass:
+        # counter calibration in the same run: a plain device copy of 256 MiB
+        src = torch.ones(64 << 20, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
     return rows
 
 
@@ -577,7 +585,9 @@ def main():
     ap.add_argument("--no-dispatch", action="store_true", help="skip the dispatch-side measurement")
     ap.add_argument("--no-gather", action="store_true", help="skip the replica-slot gather measurement")
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-min-log2", type=int, default=16)
     ap.add_argument("--sweep-max-log2", type=int, default=28)
+    ap.add_argument("--sweep-experts", default="128,512")
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")
     ap.add_argument("--solver", type=int, default=0,
                     help="0 auto, 1 one solver workgroup, 2 one per domain, 3 one launch")
