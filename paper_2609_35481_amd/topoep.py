@@ -202,6 +202,14 @@ def _dev_i32(t, name, shape=None):
     return t
 
 
+def _same_device(dev, **tensors):
+    """Every given tensor (None skipped) lives where the outputs and the
+    workspace do."""
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise ValueError("%s is on %s, the planner's memory on %s" % (name, t.device, dev))
+
+
 class Planner:
     """Holds the output tensors and workspace of one (topology, T, k, N)
     problem so repeated plans allocate nothing (and can be graph-captured)."""
@@ -230,6 +238,7 @@ class Planner:
         _dev_i32(global_load, "global_load", (R, E))
         if self.T > 0:
             _dev_i32(local_topk, "local_topk", (self.T, self.k))
+        _same_device(self._ws.device, global_load=global_load, local_topk=local_topk if self.T > 0 else None)
         if stream is None:
             stream = torch.cuda.current_stream(global_load.device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
@@ -302,6 +311,8 @@ class CostPlanner:
         t = self.T > 0
         if t:
             _dev_i32(local_topk, "local_topk", (self.T, self.k))
+        _same_device(self._ws.device, global_load=global_load, local_topk=local_topk if t else None,
+                     cost=self.cost, expert_bytes=self.expert_bytes)
         rc = _lib.topoep_plan_costs(
             ctypes.byref(self.topo), ctypes.byref(self.costs), global_load.data_ptr(),
             local_topk.data_ptr() if t else None, self.T, self.k, self.N,
@@ -340,6 +351,7 @@ class DispatchPlanner:
         if self.T > 0:
             _dev_i32(local_topk, "local_topk", (self.T, self.k))
         t = self.T > 0
+        _same_device(self._ws.device, global_load=global_load, local_topk=local_topk if t else None)
         rc = _lib.topoep_plan_dispatch(
             ctypes.byref(self.topo), global_load.data_ptr(), local_topk.data_ptr() if t else None,
             self.T, self.k, self.N, self.replica_slots.data_ptr() if self.replica_slots.numel() else None,
@@ -374,6 +386,7 @@ class LayoutPlanner:
         t = self.T > 0
         if t:
             _dev_i32(token_dest, "token_dest", (self.T, self.k))
+        _same_device(self._ws.device, send_counts=send_counts, token_dest=token_dest if t else None)
         rc = _lib.topoep_dispatch_layout(
             ctypes.byref(self.topo), token_dest.data_ptr() if t else None, self.T, self.k, send_counts.data_ptr(),
             self.send_offsets.data_ptr(), self.token_slot.data_ptr() if t else None, self.status.data_ptr(),
