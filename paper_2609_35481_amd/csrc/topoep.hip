@@ -54,6 +54,7 @@ constexpr int kCtrlStatus = 2;   // status bits accumulated during the plan
 constexpr int kCtrlFinal = 3;    // final status of the plan (read by reroute)
 constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
 constexpr int kCtrlMoves = 6;    // refinement moves of the per-domain solver
+constexpr int kCtrlHelpers = 7;  // offset helpers that have published their experts' totals
 // one-launch plan: chunks whose counts are written, then the last chunk's
 // verdict on top: nb + kVerdictSame when the histogram equals row self of
 // Omega and no id is bad (the counts are cleared), nb + kVerdictRedo
@@ -95,6 +96,7 @@ struct Plan {
   int32_t *offs_out;   // send offsets [R + 1] (given with slot_out)
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
+  int32_t *htot;   // three-kernel plan: each expert's count over the histogram blocks [E]
   uint32_t *pub, *flags, *ghist;   // one-launch plan: chunk counts, flags, histogram (E + 1 words)
 };
 
@@ -421,7 +423,9 @@ __device__ void load_fast(const Plan &p, int *om, int *hs, int *scratch, int *mi
 }
 
 // Exclusive per-expert offset of every histogram block, for the reroute
-// (offset workgroup h of n_helpers handles kOffsetExperts experts at a time).
+// (offset workgroup h of n_helpers handles kOffsetExperts experts at a time),
+// and each expert's count over all blocks (htot, the histogram of
+// local_topk), announced by one increment of the helpers' counter.
 __device__ void block_offsets(const Plan &p, int h, int *scratch) {
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, E = p.E, nb = p.nb;
   const int el = tid & 63, g = tid >> 6;
@@ -443,6 +447,7 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch) {
     __syncthreads();
     int base = 0;
     for (int g2 = 0; g2 < g; ++g2) base += scratch[g2 * 64 + el];
+    if (g == nw - 1 && e < E) p.htot[e] = base + run;   // the expert's count over every block
     if (e < E) {
       for (int b = b0; b < b1; b += 8) {
         int v[8];
@@ -456,6 +461,37 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch) {
       }
     }
     __syncthreads();
+  }
+  // publish: every total written before the count of finished helpers
+  drain_then_barrier();
+  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlHelpers], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The histogram of local_topk (row self of Omega) for the per-domain
+// solver: the offset helpers' totals once all of them have published (a
+// bounded wait; the helpers run beside the solver workgroups), else the sum
+// of the blocks' counts made here.  flag: one LDS word.
+__device__ void row_self(const Plan &p, int *hs, int *scratch, int *flag) {
+  if (threadIdx.x == 0) {
+    uint32_t it = 0;
+    int ok = 1;
+    while (__hip_atomic_load(&p.ctrl[kCtrlHelpers], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
+           (uint32_t)p.n_helpers) {
+      if (++it > p.spin_limit) {
+        ok = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    *flag = ok;
+  }
+  __syncthreads();
+  if (*flag) {
+    for (int e = threadIdx.x; e < p.E; e += blockDim.x) hs[e] = p.htot[e];
+    lds_barrier();
+  } else {
+    hist_from_partials(p, hs, scratch);
   }
 }
 
@@ -516,6 +552,7 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
     p.ctrl[kCtrlStatus] = 0;
     p.ctrl[kCtrlFinal] = 0;
     p.ctrl[kCtrlMoves] = 0;
+    p.ctrl[kCtrlHelpers] = 0;
     *reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal) = 0ull;
   }
   for (int e = tid; e < p.E; e += nt) h[e] = 0;
@@ -1265,13 +1302,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     const uint32_t cst = general_check(p, misc, &cmax, &wmax);
     if (tid == 0 && cst) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), cst);
   }
-  // ---- row self of Omega: the histogram of local_topk, in full on the
-  // workgroup of the domain holding self (its stage 1 and receive counts
-  // read every expert); the others sum it later for their own instances'
-  // experts only
+  // ---- row self of Omega: the histogram of local_topk, from the offset
+  // helpers; the workgroup of the domain holding self needs it for its
+  // stage 1, the others only after the grid barrier (by then the helpers
+  // are done)
   const int dself = (int)fdiv((uint32_t)p.self, p.fG);
   const bool has_self = dself < M && dself % nwg == wg;
-  if (has_self) hist_from_partials(p, hs, qcol);
+  if (has_self) row_self(p, hs, qcol, &misc[10]);
   if (wg == 0)
     for (int b = tid; b < p.nb; b += nt)
       if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
@@ -1326,6 +1363,8 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   if (out_of_range_cw(p, total, cmax, wmax)) gst |= TOPOEP_ST_RANGE;
   if (!synced) gst |= TOPOEP_ST_SYNC;
   const bool noplan = (gst & kNoPlan) != 0 || !synced;
+
+  if (!has_self && !noplan) row_self(p, hs, qcol, &misc[10]);
 
   // ---- domains hosting each expert: the main's domain plus stage-1 replicas
   if (!noplan) {
@@ -1392,31 +1431,8 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       else e = (pos - P) < used[j] ? slots[j * Neff + pos - P] : -1;
       e_of[a] = e;
       U[a] = 0;
-      if (!has_self && e >= 0) hs[e] = 0;
     }
     lds_barrier();
-    if (!has_self) {
-      // hs[e] of the domain's instances (distinct experts), the blocks'
-      // partial counts split over thread groups
-      const int groups = imax(1, nt / I);
-      const int per = (p.nb + groups - 1) / groups;
-      for (int t = tid; t < groups * I; t += nt) {
-        const int g = (int)fdiv((uint32_t)t, p.fI), a = t - g * I;
-        const int e = e_of[a];
-        if (e < 0) continue;
-        const int b0 = g * per, b1 = imin(p.nb, b0 + per);
-        int sum = 0;
-        for (int b = b0; b < b1; b += 8) {
-          int v[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
-#pragma unroll
-          for (int u = 0; u < 8; ++u) sum += v[u];
-        }
-        if (sum) atomicAdd(&hs[e], sum);
-      }
-      lds_barrier();
-    }
     // whether the domain can refine at all (a rank with a free slot); if not,
     // only the q[self] column is needed, else the columns omega[s][e] of the
     // domain's instances, then q in place
@@ -2698,6 +2714,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   const size_t o_cr = take((size_t)q.nent_cap * 4);
   const size_t o_ce = take((size_t)q.nent_cap * 4);
   const bool one = s.mode == 3;
+  const size_t o_ht = take(one ? 0 : (size_t)E * 4);
   const size_t o_pub = take(one ? (size_t)q.nb * E * 4 : 0);
   const size_t o_flg = take(one ? (size_t)q.nb * kFlagStride * 4 : 0);
   const size_t o_gh = take(one ? (size_t)(E + 1) * 4 : 0);
@@ -2713,6 +2730,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     q.csr_ptr = reinterpret_cast<int32_t *>(ws + o_cptr);
     q.csr_r = reinterpret_cast<int32_t *>(ws + o_cr);
     q.csr_end = reinterpret_cast<int32_t *>(ws + o_ce);
+    q.htot = one ? nullptr : reinterpret_cast<int32_t *>(ws + o_ht);
     q.pub = one ? reinterpret_cast<uint32_t *>(ws + o_pub) : nullptr;
     q.flags = one ? reinterpret_cast<uint32_t *>(ws + o_flg) : nullptr;
     q.ghist = one ? reinterpret_cast<uint32_t *>(ws + o_gh) : nullptr;
