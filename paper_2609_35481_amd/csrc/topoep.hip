@@ -1304,11 +1304,10 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   }
   // ---- row self of Omega: the histogram of local_topk, from the offset
   // helpers; the workgroup of the domain holding self needs it for its
-  // stage 1, the others only after the grid barrier (by then the helpers
-  // are done)
+  // stage 1 (it waits once its rows of Omega are loaded), the others only
+  // after the grid barrier (by then the helpers are done)
   const int dself = (int)fdiv((uint32_t)p.self, p.fG);
   const bool has_self = dself < M && dself % nwg == wg;
-  if (has_self) row_self(p, hs, qcol, &misc[10]);
   if (wg == 0)
     for (int b = tid; b < p.nb; b += nt)
       if (p.blk_err[b]) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
@@ -1316,6 +1315,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   // ---- inter-node placement (Eq. 9), each domain independently
   for (int d = wg; d < M; d += nwg) {
     copy_to_lds(rows, p.gl + (int64_t)d * G * E, G * E);
+    if (d == dself) row_self(p, hs, qcol, &misc[10]);
     if (tid == 0) misc[1] = 0;
     lds_barrier();
     scan_rows(p, d * G, (d + 1) * G, rows, hs, misc);
