@@ -73,6 +73,7 @@ constexpr int kFusedBlocks = 64;        // chunk workgroups the single-launch pl
 constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs)
 constexpr int kFlagStride = 32;         // words between ready flags (one 128-byte line each)
 constexpr uint32_t kSpinLimit = 1u << 24;
+constexpr uint32_t kHelperSpin = 1u << 12;   // polls of the offset helpers' counter before summing alone
 constexpr uint32_t kIterLimit = 1u << 22;
 
 // ---------------------------------------------------------------- plan
@@ -468,16 +469,18 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch) {
 }
 
 // The histogram of local_topk (row self of Omega) for the per-domain
-// solver: the offset helpers' totals once all of them have published (a
-// bounded wait; the helpers run beside the solver workgroups), else the sum
-// of the blocks' counts made here.  flag: one LDS word.
+// solver: the offset helpers' totals once all of them have published, else
+// the sum of the blocks' counts made here.  The helpers normally finish in
+// a few microseconds beside the solver workgroups; the wait is bounded by
+// kHelperSpin polls (~0.2 ms), not by the hang guard, so a dispatch whose
+// helpers start late costs little.  flag: one LDS word.
 __device__ void row_self(const Plan &p, int *hs, int *scratch, int *flag) {
   if (threadIdx.x == 0) {
     uint32_t it = 0;
     int ok = 1;
     while (__hip_atomic_load(&p.ctrl[kCtrlHelpers], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <
            (uint32_t)p.n_helpers) {
-      if (++it > p.spin_limit) {
+      if (++it > kHelperSpin) {
         ok = 0;
         break;
       }
