@@ -74,6 +74,7 @@ constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs
 constexpr int kFlagStride = 32;         // words between ready flags (one 128-byte line each)
 constexpr uint32_t kSpinLimit = 1u << 24;
 constexpr uint32_t kHelperSpin = 1u << 12;   // polls of the offset helpers' counter before summing alone
+constexpr int kListRegs = 4;   // instances per thread the instance list keeps in registers
 constexpr uint32_t kIterLimit = 1u << 22;
 
 // ---------------------------------------------------------------- plan
@@ -1516,20 +1517,17 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   for (int e = tid; e <= E; e += nt) cnt[e] = 0;
   for (int i = tid; i < E * p.RW; i += nt) bm[i] = 0;
   __syncthreads();
-  for (int idx = tid; idx < M * I; idx += nt) {
-    const int e = p.seg_e[idx], q = p.seg_q[idx];
+  // the domains' instances (expert, share of self): the first kListRegs per
+  // thread are read once and kept in registers for the second pass
+  auto count = [&](int idx, int e, int q) {
     if ((unsigned)e < (unsigned)E && q > 0) {
       const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
       const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
       atomicAdd(&cnt[e], 1);
       atomicOr(&bm[e * p.RW + (r >> 5)], 1u << (r & 31));
     }
-  }
-  __syncthreads();
-  block_excl_scan(cnt, E + 1, tmp);
-  for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
-  for (int idx = tid; idx < M * I; idx += nt) {
-    const int e = p.seg_e[idx], q = p.seg_q[idx];
+  };
+  auto place = [&](int idx, int e, int q) {
     if ((unsigned)e < (unsigned)E && q > 0) {
       const int d = (int)fdiv((uint32_t)idx, p.fI), a = idx - d * I;
       const int r = d * G + (int)fdiv((uint32_t)a, p.fPN);
@@ -1541,7 +1539,23 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       p.csr_r[j] = r;
       cv[j] = q;
     }
+  };
+  int se[kListRegs], sq[kListRegs];
+#pragma unroll
+  for (int u = 0; u < kListRegs; ++u) {
+    const int idx = tid + u * nt;
+    se[u] = idx < M * I ? p.seg_e[idx] : -1;
+    sq[u] = idx < M * I ? p.seg_q[idx] : 0;
   }
+#pragma unroll
+  for (int u = 0; u < kListRegs; ++u) count(tid + u * nt, se[u], sq[u]);
+  for (int idx = tid + kListRegs * nt; idx < M * I; idx += nt) count(idx, p.seg_e[idx], p.seg_q[idx]);
+  __syncthreads();
+  block_excl_scan(cnt, E + 1, tmp);
+  for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
+#pragma unroll
+  for (int u = 0; u < kListRegs; ++u) place(tid + u * nt, se[u], sq[u]);
+  for (int idx = tid + kListRegs * nt; idx < M * I; idx += nt) place(idx, p.seg_e[idx], p.seg_q[idx]);
   __syncthreads();
   // cumulative shares per expert, in LDS, then out
   for (int e = tid; e < E; e += nt) {
