@@ -1371,6 +1371,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   if (!has_self && !noplan) row_self(p, hs, qcol, &misc[10]);
 
   // ---- domains hosting each expert: the main's domain plus stage-1 replicas
+  const bool one_domain = M <= nwg;
   if (!noplan) {
     for (int i = tid; i < E * p.MW; i += nt) mask[i] = 0;
     __syncthreads();
@@ -1380,10 +1381,11 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     }
     for (int i = tid; i < M * cap; i += nt) {
       const int e = p.repl1[i];
-      if ((unsigned)e < (unsigned)E) {
-        const int dd = (int)fdiv((uint32_t)i, p.fCap);
-        atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
-      }
+      const int dd = (int)fdiv((uint32_t)i, p.fCap);
+      // a workgroup of one domain keeps that domain's list (rows is free
+      // after stage 1: cap = G Neff <= G E words)
+      if (one_domain && dd == wg) rows[i - dd * cap] = e;
+      if ((unsigned)e < (unsigned)E) atomicOr(&mask[e * p.MW + (dd >> 5)], 1u << (dd & 31));
     }
   }
   __syncthreads();
@@ -1402,11 +1404,13 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       continue;
     }
     // stage-1 slots of the domain's ranks: candidate i sits on local rank
-    // i mod G, slot i / G; the chosen ones are a prefix of the list (read
-    // once into rows, free after stage 1: cap = G Neff <= G E words)
+    // i mod G, slot i / G; the chosen ones are a prefix of the list, in
+    // rows (kept there by the mask loop when the workgroup holds one domain)
     int *sel = rows;
-    for (int c = tid; c < cap; c += nt) sel[c] = p.repl1[(int64_t)d * cap + c];
-    lds_barrier();
+    if (!one_domain) {
+      for (int c = tid; c < cap; c += nt) sel[c] = p.repl1[(int64_t)d * cap + c];
+      lds_barrier();
+    }
     if (tid < 64) {
       // the chosen ones: the prefix before the first empty entry
       int nsel = cap;
