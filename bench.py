@@ -85,13 +85,22 @@ def algorithmic_bytes(cfg, N, kernels):
     }
 
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_35481_amd", "csrc", "topoep.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_35481_amd", "csrc", n) for n in ("topoep.hip", "wave.h")]
 
 
 def source_digest() -> str:
+    """Digest of the plan kernels' code: their source and the wave helpers
+    they include, with // comments and blank lines left out (a comment edit
+    keeps the committed counters valid, a code edit does not)."""
     import hashlib
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha1(f.read()).hexdigest()[:12]
+    h = hashlib.sha1()
+    for path in KERNEL_SRCS:
+        with open(path, encoding="utf-8") as f:
+            for line in f:
+                code = line.split("//", 1)[0].rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
+    return h.hexdigest()[:12]
 
 
 def measured_traffic(workload_name, kernel):
