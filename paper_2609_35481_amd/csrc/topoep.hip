@@ -1269,7 +1269,16 @@ __device__ GenCost general_tables(const Plan &p, int d, int *sm, const DomainLds
 }
 
 // ---------------------------------------------------------------- solver: one workgroup per domain
-
+//
+// Workgroups 0 .. n_solvers-1 each take the domains d = wg, wg + n_solvers,
+// ...; the n_helpers after them compute the histogram blocks' offsets for
+// the reroute and each expert's total (row self of Omega).  Per domain:
+// stage 1 (Eq. 9) from the domain's rows of Omega, then a bounded grid
+// barrier publishes every domain's replicas; the hosting masks, the
+// domain's instances, routing (Section 4.3), refinement (Eq. 10) and the
+// domain's outputs follow.  The last solver workgroup to finish (a ticket)
+// lists this rank's instances per expert for the reroute and writes the
+// final status.
 __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   extern __shared__ int64_t smem_s[];
   int *sm = reinterpret_cast<int *>(smem_s);
