@@ -769,9 +769,10 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // moved assignments come from the sources in the precomputed (c(s,rt) -
 // c(s,rb), s) order of gc, and the cost change uses the cost matrix and
 // ||W_e||.
-template <bool General = false>
+template <bool General = false, bool Pairs = false>
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                   int *Lr, uint64_t *em, uint32_t *flags, bool prepared, GenCost gc = GenCost{}) {
+  static_assert(!(General && Pairs), "the pair layout scores the two-level cost only");
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return 0;
@@ -835,7 +836,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     // take any expert, and the lightest of them form one level (lf, tf)
     const bool low = lane < G && lane != rbj && (int64_t)Lrb - lj >= 2;
     const uint64_t lowm = __ballot(low);
-    if (lowm == 0) break;
+    if (!Pairs && lowm == 0) break;   // (the pair layout needs none of these levels)
     const bool fr = low && uj < Neff;
     uint32_t lf = ~0u;
     uint64_t tf = 0;
@@ -848,84 +849,122 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     const int jf = tf ? __ffsll((long long)tf) - 1 : 0;
     uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull, best_hm = 0;
     int best_a = 0, best_u = 0, best_q = 0;
-    for (int rd = 0; rd < rounds; ++rd) {
-      const int ai = lane + rd * 64;
-      if (ai >= PN) continue;
-      const int a = rbj * PN + ai;
-      const int *qa = qcol + a * QS;
-      const bool two_level = !General && p.cI > 0;
-      const int e = e_of[a];
-      const int u = U[a];
-      const int qrb = two_level ? qa[rb] : 0;
-      const int qf = two_level ? qa[r0 + jf] : 0;
-      if (e < 0 || u <= 0) continue;
-      const uint64_t hmf = em[e];
-      // the lightest receivers already hosting e (no slot needed)
-      uint32_t lh = ~0u;
-      uint64_t th = 0;
-      for (uint64_t h = hmf & lowm; h; h &= h - 1) {
-        const int j = __ffsll((long long)h) - 1;
-        const uint32_t L = (uint32_t)Lr[j];
-        if (L < lh) {
-          lh = L;
-          th = 0;
-        }
-        if (L == lh) th |= 1ull << j;
-      }
-      const uint32_t lm = lf < lh ? lf : lh;
-      if (lm == ~0u) continue;
-      const uint64_t tset = (lf == lm ? tf : 0) | (lh == lm ? th : 0);
-      const int delta = imin(u, (Lrb - (int)lm) >> 1);
-      // lowest (cost change, rt) among the lightest receivers
-      int64_t bc = INT64_MAX;
-      int bj = 0, bq = 0;
-      for (uint64_t t = tset; t; t &= t - 1) {
-        const int rtj = __ffsll((long long)t) - 1;
-        const bool hosts = (hmf >> rtj) & 1ull;
+    if constexpr (Pairs) {
+      // one lane per (instance of rb, other rank) pair, PN (G - 1) <= 64:
+      // every load of a candidate issued at once
+      const int npair = PN * (G - 1);
+      if (lane < npair) {
+        const int pai = (int)fdiv((uint32_t)lane, p.fG1), pjj = lane - pai * (G - 1);
+        const int rtj = pjj < rbj ? pjj : pjj + 1;
         const int rt = r0 + rtj;
-        int64_t dcost = 0;
-        int qrt = 0;
-        if constexpr (General) {
-          // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
-          const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
-          const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
-          int rest = delta;
-          int64_t dt = 0;
-          for (int k = 0; k < R && rest > 0; ++k) {
-            const int s2 = o[k];
-            const int take = imin(rest, qa[s2]);
-            dt += (int64_t)take * (ct[s2] - cb[s2]);
-            rest -= take;
+        const int a = rbj * PN + pai;
+        const int *qa = qcol + a * QS;
+        const int e = e_of[a], u = U[a], Lrt = Lr[rtj], urt = used[rtj];
+        const int qrt = p.cI > 0 ? qa[rt] : 0, qrb = p.cI > 0 ? qa[rb] : 0;
+        const int64_t gap = (int64_t)Lrb - Lrt;
+        if (e >= 0 && u > 0 && gap >= 2) {
+          const uint64_t hmf = em[e];
+          const bool hosts = (hmf >> rtj) & 1ull;
+          if (hosts || urt < Neff) {
+            const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
+            int64_t dcost = 0;
+            if (p.cI > 0) {
+              const int m_rt = imin(delta, qrt);
+              const int rest = delta - m_rt;
+              const int m_rb = rest - imin(rest, u - qrt - qrb);
+              dcost = tokc * (int64_t)(m_rb - m_rt);
+            }
+            if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+            k1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
+            k2 = (uint64_t)dcost ^ (1ull << 63);
+            k3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)rt;
+            best_a = a;
+            best_u = u;
+            best_hm = hmf;
+            best_q = qrt;
           }
-          dcost = 2 * p.S * dt;
-          if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
-        } else {
-          if (p.cI > 0) {
-            qrt = rtj == jf ? qf : qa[rt];
-            const int m_rt = imin(delta, qrt);
-            const int rest = delta - m_rt;
-            const int m_rb = rest - imin(rest, u - qrt - qrb);
-            dcost = tokc * (int64_t)(m_rb - m_rt);
-          }
-          if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
-        }
-        if (dcost < bc) {
-          bc = dcost;
-          bj = rtj;
-          bq = qrt;
         }
       }
-      const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm;
-      const uint64_t c2 = (uint64_t)bc ^ (1ull << 63);
-      const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj);
-      if (lex_less(c1, c2, c3, k1, k2, k3)) {
-        k1 = c1;
-        k2 = c2;
-        k3 = c3;
-        best_a = a;
-        best_u = u;
-        best_hm = hmf;
-        best_q = bq;
+    } else {
+      for (int rd = 0; rd < rounds; ++rd) {
+        const int ai = lane + rd * 64;
+        if (ai >= PN) continue;
+        const int a = rbj * PN + ai;
+        const int *qa = qcol + a * QS;
+        const bool two_level = !General && p.cI > 0;
+        const int e = e_of[a];
+        const int u = U[a];
+        const int qrb = two_level ? qa[rb] : 0;
+        const int qf = two_level ? qa[r0 + jf] : 0;
+        if (e < 0 || u <= 0) continue;
+        const uint64_t hmf = em[e];
+        // the lightest receivers already hosting e (no slot needed)
+        uint32_t lh = ~0u;
+        uint64_t th = 0;
+        for (uint64_t h = hmf & lowm; h; h &= h - 1) {
+          const int j = __ffsll((long long)h) - 1;
+          const uint32_t L = (uint32_t)Lr[j];
+          if (L < lh) {
+            lh = L;
+            th = 0;
+          }
+          if (L == lh) th |= 1ull << j;
+        }
+        const uint32_t lm = lf < lh ? lf : lh;
+        if (lm == ~0u) continue;
+        const uint64_t tset = (lf == lm ? tf : 0) | (lh == lm ? th : 0);
+        const int delta = imin(u, (Lrb - (int)lm) >> 1);
+        // lowest (cost change, rt) among the lightest receivers
+        int64_t bc = INT64_MAX;
+        int bj = 0, bq = 0;
+        for (uint64_t t = tset; t; t &= t - 1) {
+          const int rtj = __ffsll((long long)t) - 1;
+          const bool hosts = (hmf >> rtj) & 1ull;
+          const int rt = r0 + rtj;
+          int64_t dcost = 0;
+          int qrt = 0;
+          if constexpr (General) {
+            // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
+            const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
+            const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
+            int rest = delta;
+            int64_t dt = 0;
+            for (int k = 0; k < R && rest > 0; ++k) {
+              const int s2 = o[k];
+              const int take = imin(rest, qa[s2]);
+              dt += (int64_t)take * (ct[s2] - cb[s2]);
+              rest -= take;
+            }
+            dcost = 2 * p.S * dt;
+            if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
+          } else {
+            if (p.cI > 0) {
+              qrt = rtj == jf ? qf : qa[rt];
+              const int m_rt = imin(delta, qrt);
+              const int rest = delta - m_rt;
+              const int m_rb = rest - imin(rest, u - qrt - qrb);
+              dcost = tokc * (int64_t)(m_rb - m_rt);
+            }
+            if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+          }
+          if (dcost < bc) {
+            bc = dcost;
+            bj = rtj;
+            bq = qrt;
+          }
+        }
+        const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm;
+        const uint64_t c2 = (uint64_t)bc ^ (1ull << 63);
+        const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj);
+        if (lex_less(c1, c2, c3, k1, k2, k3)) {
+          k1 = c1;
+          k2 = c2;
+          k3 = c3;
+          best_a = a;
+          best_u = u;
+          best_hm = hmf;
+          best_q = bq;
+        }
       }
     }
     const uint64_t m1 = wave_min_u64(k1);
@@ -1674,6 +1713,7 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 // Eq. 10 refinement) and writes replica_slots, send_counts, this rank's
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
+template <bool Pairs = false>
 __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
                             bool write_status = true, bool read_arrival = false) {
   uint64_t *ck = t.ck, *em = t.em;
@@ -1777,7 +1817,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
     // ranks' loads first; a domain without a free slot returns at once)
     uint32_t flags = 0, moves = 0;
     for (int d = wave; d < M; d += nw)
-      moves += refine_domain(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
+      moves += refine_domain<false, Pairs>(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
                              used + d * G, Lr + d * G, em + (int64_t)d * E, &flags, true);
     if (lane_id() == 0) {
       if (flags) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
@@ -2156,6 +2196,7 @@ __device__ void collect_counts(const Plan &p, int *hs, int *misc) {
 // histogram with row self of Omega, that plan stands (equal rows, so Omega'
 // = Omega) or is made again from Omega' on fresh state; then every chunk's
 // flag 2.
+template <bool Pairs>
 __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
@@ -2170,7 +2211,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   // this rank's own count), else it is redone below; nothing reads the
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
-  if (spec) single_plan(p, t, gst0, true, false, true);
+  if (spec) single_plan<Pairs>(p, t, gst0, true, false, true);
   // wait until every chunk has written its counts and the last one has
   // added its verdict
   if (tid == 0) {
@@ -2234,10 +2275,10 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
     lds_barrier();
     uint32_t gst = (uint32_t)t.misc[0];
     if (out_of_range(p, total0 + *reinterpret_cast<const unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
-    single_plan(p, t, gst, true);
+    single_plan<Pairs>(p, t, gst, true);
     planned = !(gst & kNoPlan);
   } else {
-    single_plan(p, t, TOPOEP_ST_SYNC, true);
+    single_plan<Pairs>(p, t, TOPOEP_ST_SYNC, true);
   }
   if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
   // release: every output the chunks read (the instance list, the final
@@ -2538,14 +2579,17 @@ __device__ inline Plan role_plan(const Plan &p) {
 #endif
 }
 
-template <int IPT>
+// Pairs: the refinement scores one (instance, target) pair per lane
+// (domains with PN (G - 1) <= 64 candidates), else each instance's lightest
+// receivers; one instantiation each keeps the other's registers out.
+template <int IPT, bool Pairs>
 __global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
   extern __shared__ int64_t smem_f[];
   int *sm = reinterpret_cast<int *>(smem_f);
   (void)p;
   if (blockIdx.x == 0) {
     const Plan q = solver_plan(role_plan(p));
-    fused_solver(q, sm);
+    fused_solver<Pairs>(q, sm);
   } else {
     const Plan q = role_plan(p);
     fused_chunk<IPT>(q, blockIdx.x - 1, sm);
@@ -2790,10 +2834,14 @@ void set_attrs() {
   allow_lds(reroute_kernel<8>);
   allow_lds(solve_kernel);
   allow_lds(solve_single_kernel);
-  allow_lds(plan_fused_kernel<1>);
-  allow_lds(plan_fused_kernel<2>);
-  allow_lds(plan_fused_kernel<4>);
-  allow_lds(plan_fused_kernel<8>);
+  allow_lds(plan_fused_kernel<1, false>);
+  allow_lds(plan_fused_kernel<1, true>);
+  allow_lds(plan_fused_kernel<2, false>);
+  allow_lds(plan_fused_kernel<2, true>);
+  allow_lds(plan_fused_kernel<4, false>);
+  allow_lds(plan_fused_kernel<4, true>);
+  allow_lds(plan_fused_kernel<8, false>);
+  allow_lds(plan_fused_kernel<8, true>);
   allow_lds(empty_kernel);
   g_attrs_set = true;
 }
@@ -2823,13 +2871,20 @@ void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
   else hipLaunchKernelGGL(solve_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
 }
 
+template <int IPT>
+void launch_fused_ipt(bool pairs, dim3 g, dim3 b, size_t lds, hipStream_t st, const Plan &p) {
+  if (pairs) hipLaunchKernelGGL((plan_fused_kernel<IPT, true>), g, b, lds, st, p);
+  else hipLaunchKernelGGL((plan_fused_kernel<IPT, false>), g, b, lds, st, p);
+}
+
 void launch_fused(const Plan &p, const Shape &s, hipStream_t st) {
   const dim3 g(p.nb + 1), b(s.st);
+  const bool pairs = p.PN * (p.G - 1) <= 64;   // the refinement's candidates fit one wavefront
   switch (s.ipt) {
-    case 1: hipLaunchKernelGGL(plan_fused_kernel<1>, g, b, s.lds_fused, st, p); break;
-    case 2: hipLaunchKernelGGL(plan_fused_kernel<2>, g, b, s.lds_fused, st, p); break;
-    case 4: hipLaunchKernelGGL(plan_fused_kernel<4>, g, b, s.lds_fused, st, p); break;
-    default: hipLaunchKernelGGL(plan_fused_kernel<8>, g, b, s.lds_fused, st, p); break;
+    case 1: launch_fused_ipt<1>(pairs, g, b, s.lds_fused, st, p); break;
+    case 2: launch_fused_ipt<2>(pairs, g, b, s.lds_fused, st, p); break;
+    case 4: launch_fused_ipt<4>(pairs, g, b, s.lds_fused, st, p); break;
+    default: launch_fused_ipt<8>(pairs, g, b, s.lds_fused, st, p); break;
   }
 }
 
