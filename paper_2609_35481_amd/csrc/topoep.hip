@@ -756,9 +756,10 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // 64 bits, scratch) receives, per expert, the mask of the domain's local
 // ranks hosting it.  Each iteration picks the busiest rank rb (ties to the
 // lowest rank), takes the best (instance of rb, other rank of the domain)
-// candidate by key (delta desc, L[rt] asc, cost change asc, e asc, rt asc),
-// scoring only each instance's lightest receivers (the others cannot win),
-// and commits it.  The moved assignments come from sources in
+// candidate by key (delta desc, L[rt] asc, cost change asc, e asc, rt asc)
+// and commits it.  With Pairs (at most 64 candidates) each lane scores one
+// pair; otherwise each lane takes an instance and scores only its lightest
+// receivers (the others cannot win).  The moved assignments come from sources in
 // ascending (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt
 // itself, then the other sources ascending, then rb (or plain ascending when
 // the intra-domain cost is zero).  The loop ends when no candidate has
