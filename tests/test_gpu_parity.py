@@ -4,7 +4,8 @@ for bit, through the C ABI.
 
 Integer work throughout, so the bar is exact equality.  Cases: the paper's
 worked example, seeded random tiny instances (ragged sizes, every topology
-shape), the five workload configurations at full size, larger replica
+shape), mid-size random instances (up to 96 ranks, domains of up to 16),
+the five workload configurations at full size, larger replica
 budgets that keep the refinement busy at scale, edge cases, launch-shape
 and repeat determinism, HIP-graph replay, and the single-stage entry point.
 """
@@ -129,6 +130,58 @@ def test_random_refinement_heavy(seed, solver):
     s = int(rng.integers(R))
     both(R, G, E, s, cI, cX, S, W, N, omega, topks[s], launch=SOLVERS[solver],
          what="refine seed %d %s" % (seed, solver))
+
+
+def random_mid_instance(seed):
+    """A mid-size instance: up to 96 ranks in domains of 1..16, up to 8
+    experts per rank, top-1..8, 0..3000 local tokens, 0..5 replica slots,
+    popularity from flat to one hot expert, and in one case of ten a row self
+    of Omega that is not the histogram of the ids."""
+    rng = np.random.default_rng(50000 + seed)
+    G = int(rng.choice([1, 2, 3, 4, 6, 8, 16]))
+    M = int(rng.choice([1, 2, 3, 4, 8]))
+    if G * M > 96:
+        M = max(1, 96 // G)
+    R = G * M
+    P = int(rng.choice([1, 2, 3, 4, 8]))
+    E = R * P
+    k = int(rng.integers(1, min(E, 8) + 1))
+    N = int(rng.integers(0, 6))
+    pop = rng.dirichlet(np.full(E, float(rng.choice([0.05, 0.2, 1.0, 5.0]))))
+    T = int(rng.choice([0, 1, 7, 64, 500, 3000]))
+    topks = [rng.choice(E, size=(int(rng.integers(0, 2 * T + 2)), k), p=pop).astype(np.int32) for _ in range(R)]
+    s = int(rng.integers(R))
+    topks[s] = rng.choice(E, size=(T, k), p=pop).astype(np.int32)
+    omega = np.stack([np.bincount(x.ravel(), minlength=E) for x in topks]).astype(np.int32)
+    if rng.random() < 0.1:
+        omega[s] = rng.integers(0, 50, size=E)
+    cI = int(rng.integers(0, 3))
+    cX = int(rng.integers(cI, 12))
+    S = int(rng.integers(1, 9))
+    D = int(omega.reshape(M, G, E).sum(1).max())
+    W = int(rng.integers(0, 2 * S * max(D, 1) + 2))
+    return (R, G, E, s, cI, cX, S, W, N, omega, topks[s])
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+def test_random_mid(solver):
+    """300 mid-size instances per solver (one test each: a failure names its
+    seed); a shape beyond the solver's LDS limit is skipped."""
+    done = 0
+    for seed in range(300):
+        args = random_mid_instance(seed)
+        try:
+            got = gpu_plan(*args, launch=SOLVERS[solver])
+        except topoep.TopoepError as ex:
+            if ex.rc == topoep.ELIMIT:
+                continue
+            raise
+        R, G, E, s, _, _, _, _, N, _, tk = args
+        assert_same(got, ref_plan(*args), "mid seed %d %s R%d G%d E%d k%d T%d N%d" % (
+            seed, solver, R, G, E, tk.shape[1], tk.shape[0], N))
+        done += 1
+    say("mid", solver, done, "instances")
+    assert done >= 200
 
 
 # ---------------------------------------------------------------- configurations
