@@ -285,6 +285,63 @@ def time_stage(torch, planners, dev_inputs, stage, reps):
     return a.elapsed_time(b) * 1e3 / (3 * reps * len(planners))   # microseconds
 
 
+# Phase stamps of the instrumented library (slot: what was just done), in
+# the one-launch plan; the solver's slots come from workgroup 0, the chunk
+# slots from chunk 0 except "last arrival done" (the last chunk).
+PHASE_SLOTS = [(0, "solver start"), (1, "Omega in LDS"), (23, "plan start"), (22, "stage 1 candidates"),
+               (2, "stage 1"), (3, "setup"), (4, "routing"), (5, "refinement"), (6, "outputs"),
+               (7, "instance list"), (8, "speculative plan"), (9, "verdict seen"), (10, "outputs drained"),
+               (12, "chunk 0 arrived"), (19, "last arrival start"), (13, "last arrival done"),
+               (16, "chunk 0 offsets"), (14, "chunk 0 sees flag"), (15, "chunk 0 done")]
+
+
+def run_phases(args):
+    """Phase timeline of the one-launch plan from the stamped library (run
+    with TOPOEP_STAMPS=1): every layer planned in one HIP graph, replayed;
+    each slot's median over layers and replays, in microseconds after the
+    solver's start (the stamps read the 100 MHz constant clock)."""
+    import torch
+    from paper_2609_35481_amd import topoep
+    if not topoep.LIB_PATH.endswith("libtopoep_stamps.so"):
+        raise SystemExit("--phases needs TOPOEP_STAMPS=1 (the instrumented library)")
+    cfg = workload.get(args.config)
+    layers = cfg.layers if args.layers <= 0 else args.layers
+    dev = torch.device("cuda:0")
+    inputs = make_inputs(cfg, layers)
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev)) for gl, tk in inputs]
+    launch = launch_from_args(args)
+    planners = [topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=dev, launch=launch) for _ in range(layers)]
+    if planners[0].shape.kernels != 1:
+        raise SystemExit("--phases covers the one-launch plan only")
+    samples = []
+    for rep in range(args.steps):
+        for p, (g, t) in zip(planners, dev_inputs):
+            p.plan(g, t)
+        torch.cuda.synchronize()
+        if rep < args.warmup:
+            continue
+        for p in planners:
+            w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
+            samples.append([((int(w[i]) - int(w[0])) & 0xFFFFFFFF) if i < 20 or i > 21 else 0
+                            for i, _ in PHASE_SLOTS])
+    clk = []
+    for p in planners:
+        w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
+        dt = (int(w[10]) - int(w[0])) & 0xFFFFFFFF
+        if dt:
+            clk.append(((int(w[21]) - int(w[20])) & 0xFFFFFFFF) / (dt * 0.01))
+    arr = np.array(samples, dtype=np.float64) * 0.01   # 100 MHz ticks -> microseconds
+    med = np.median(arr, axis=0)
+    out = {"phases": cfg.name, "layers": layers, "samples": len(samples),
+           "us_after_solver_start_median": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, med)},
+           "us_p10": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 10, axis=0))},
+           "us_p90": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 90, axis=0))},
+           "core_clock_MHz_median": round(float(np.median(clk)), 1) if clk else None,
+           "plan_shape": planners[0].shape.as_dict()}
+    return out
+
+
 def run_bench(args):
     import torch
     from paper_2609_35481_amd import topoep
@@ -598,6 +655,8 @@ def main():
     ap.add_argument("--sweep-max-log2", type=int, default=28)
     ap.add_argument("--sweep-experts", default="128,512")
     ap.add_argument("--pmc-pass", action="store_true", help="workload for rocprofv3 counter runs")
+    ap.add_argument("--phases", action="store_true",
+                    help="phase timeline of the one-launch plan (needs TOPOEP_STAMPS=1)")
     ap.add_argument("--solver", type=int, default=0,
                     help="0 auto, 1 one solver workgroup, 2 one per domain, 3 one launch")
     ap.add_argument("--ipt", type=int, default=0, help="ids per thread per tile (0 = default)")
@@ -614,6 +673,9 @@ def main():
         return
     if args.pmc_pass:
         run_pmc_pass(args)
+        return
+    if args.phases:
+        print(json.dumps(run_phases(args)), flush=True)
         return
     print(json.dumps(run_bench(args)), flush=True)
 

@@ -25,9 +25,15 @@
  *     may be captured in a HIP graph.  Outputs are valid once the stream
  *     reaches them.
  *   - One workspace serves one plan at a time: plans that share a workspace
- *     must be ordered on one stream.  A workspace is zero-filled once before
- *     its first plan (e.g. hipMemset after allocation); every plan leaves its
- *     control words zero again, so no later clearing is needed.
+ *     must be ordered on one stream.  A workspace serves one problem shape:
+ *     the topology, T, k, N_slot and the launch shape (its layout and its
+ *     hand-over words depend on all of them).  It is zero-filled before the
+ *     first plan of a shape (e.g. hipMemset after allocation, or again
+ *     before another shape reuses the memory); after that no clearing is
+ *     needed between plans, including after a plan that reported
+ *     TOPOEP_ST_SYNC: the words that order the kernels' hand-overs carry a
+ *     plan generation the kernels advance themselves, so nothing a plan
+ *     leaves behind can satisfy a later plan's wait.
  *   - main(e) = e / (E/R) (main instances spread contiguously and evenly,
  *     Section 3.2); dom(r) = r / G.  Cost c(s,r) = 0 if s == r, cost_intra
  *     inside a domain, cost_inter across domains (a two-level instance of
@@ -75,6 +81,14 @@ typedef struct topoep_launch {
                             /*     count, wait (bounded) for the solver and      */
                             /*     reroute; block_threads and tiles_per_block    */
                             /*     are ignored                                   */
+  int32_t spin_limit;       /* polls of each bounded in-kernel wait before it    */
+                            /* gives up with TOPOEP_ST_SYNC; 0 = the default     */
+                            /* (2^24), -1 = every such wait gives up at once     */
+                            /* (for testing the error path; the kernels still    */
+                            /* run to completion)                                */
+  int32_t iter_limit;       /* refinement moves per domain after which a domain  */
+                            /* that still has a move stops with TOPOEP_ST_ITER;  */
+                            /* 0 = the default (2^22)                            */
 } topoep_launch;
 
 /* Launch shape a plan will use (topoep_plan_shape). */
@@ -108,7 +122,9 @@ typedef struct topoep_shape {
                                  /* 4 S total max(c,1) + max(c,1) W >= 2^62, so the  */
                                  /* integer cost terms would not be exact            */
 #define TOPOEP_ST_SYNC 16u       /* a bounded in-kernel wait gave up (outputs wrong) */
-#define TOPOEP_ST_ITER 32u       /* refinement hit its iteration bound               */
+#define TOPOEP_ST_ITER 32u       /* a domain still had a refinement move after its   */
+                                 /* iteration bound (the plan is valid, less        */
+                                 /* refined; the CPU oracle applies the same bound)  */
 #define TOPOEP_ST_COST 64u       /* (topoep_plan_costs) the cost matrix is not        */
                                  /* symmetric, nonnegative and zero on its diagonal, */
                                  /* or an expert size is negative                    */

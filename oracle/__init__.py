@@ -21,7 +21,9 @@ ST_BAD_ID = 1
 ST_NEG_LOAD = 2
 ST_SELF_DIFF = 4
 ST_RANGE = 8
+ST_ITER = 32
 ST_COST = 64
+ITER_LIMIT = 1 << 22
 
 
 def build(force: bool = True) -> str:
@@ -73,6 +75,10 @@ def load_library(path: str):
     lib.topoep_plan_ref_general.argtypes = [ctypes.POINTER(RefTopology), _P32, _P64, _P32, _P32, ctypes.c_int32,
                                             ctypes.c_int32, ctypes.c_int32, _P32, _P32, _P32, _P32, _P32,
                                             ctypes.POINTER(RefDebug)]
+    lib.topoep_plan_ref_capped.restype = ctypes.c_int
+    lib.topoep_plan_ref_capped.argtypes = [ctypes.POINTER(RefTopology), _P32, _P64, _P32, _P32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_int32, _P32, _P32, _P32, _P32, _P32,
+                                           ctypes.POINTER(RefDebug), ctypes.c_int32]
     lib.topoep_layout_ref.restype = ctypes.c_int
     lib.topoep_layout_ref.argtypes = [ctypes.c_int32, _P32, ctypes.c_int64, _P32, _P32, _P32]
     _lib = lib
@@ -97,11 +103,13 @@ def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> RefTopology:
 
 def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
              debug: bool = False, move_cap: int = 0, raw_rc: bool = False, cost_matrix=None,
-             expert_bytes=None):
+             expert_bytes=None, iter_limit: int = ITER_LIMIT):
     """Run the oracle.  Returns a dict of numpy arrays.
 
     cost_matrix ([R, R] int32) and expert_bytes ([E] int64) select the full
-    model of Section 4.1 (a general cost and per-expert sizes).
+    model of Section 4.1 (a general cost and per-expert sizes).  iter_limit
+    bounds the refinement moves of each domain (ST_ITER when a domain still
+    had a move after that many).
 
     Keys: replica_slots [R, N], token_dest [T, k], send_counts [R],
     recv_counts [R] (what each rank sends to this one under the same plan),
@@ -145,9 +153,10 @@ def plan_ref(topo: RefTopology, global_load, local_topk, replica_budget: int,
         dbgp = ctypes.byref(dbg)
     cm = np.ascontiguousarray(cost_matrix, dtype=np.int32) if cost_matrix is not None else None
     wb = np.ascontiguousarray(expert_bytes, dtype=np.int64) if expert_bytes is not None else None
-    rc = lib.topoep_plan_ref_general(ctypes.byref(topo), _ptr(cm), _ptr(wb, _P64), _ptr(gl),
-                                     _ptr(tk) if T > 0 else None, T, k, N, _ptr(slots),
-                                     _ptr(dest) if T > 0 else None, _ptr(sc), _ptr(rcv), _ptr(st), dbgp)
+    rc = lib.topoep_plan_ref_capped(ctypes.byref(topo), _ptr(cm), _ptr(wb, _P64), _ptr(gl),
+                                    _ptr(tk) if T > 0 else None, T, k, N, _ptr(slots),
+                                    _ptr(dest) if T > 0 else None, _ptr(sc), _ptr(rcv), _ptr(st), dbgp,
+                                    int(iter_limit))
     if raw_rc:
         return rc
     if rc != 0:

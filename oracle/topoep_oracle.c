@@ -129,7 +129,20 @@ int topoep_plan_ref_general(const ref_topology *topo, const int32_t *cost_matrix
                             int32_t replica_budget, int32_t *replica_slots,
                             int32_t *token_dest, int32_t *send_counts,
                             int32_t *recv_counts, int32_t *status, ref_debug *dbg) {
+  return topoep_plan_ref_capped(topo, cost_matrix, expert_bytes, global_load, local_topk, T, k,
+                                replica_budget, replica_slots, token_dest, send_counts, recv_counts,
+                                status, dbg, REF_ITER_LIMIT);
+}
+
+int topoep_plan_ref_capped(const ref_topology *topo, const int32_t *cost_matrix,
+                           const int64_t *expert_bytes, const int32_t *global_load,
+                           const int32_t *local_topk, int32_t T, int32_t k,
+                           int32_t replica_budget, int32_t *replica_slots,
+                           int32_t *token_dest, int32_t *send_counts,
+                           int32_t *recv_counts, int32_t *status, ref_debug *dbg,
+                           int32_t iter_limit) {
   if (!topo || !global_load || !replica_slots || !send_counts || !status) return REF_EINVAL;
+  if (iter_limit < 0) return REF_EINVAL;
   if (T < 0 || k < 1 || replica_budget < 0) return REF_EINVAL;
   if (T > 0 && (!local_topk || !token_dest)) return REF_EINVAL;
   model m;
@@ -370,6 +383,15 @@ int topoep_plan_ref_general(const ref_topology *topo, const int32_t *cost_matrix
         }
       }
       if (!have) break;
+      /* The paper's loop has no bound: it ends because sum_r L_r^2 falls by
+       * at least 2 with every move, which still allows up to total^2 / 2
+       * moves.  A domain that has committed iter_limit moves and still has
+       * one stops here with ITER (the plan stays valid), so every plan's work
+       * is bounded; the GPU path applies the same rule. */
+      if (iters >= iter_limit) {
+        st |= REF_ST_ITER;
+        break;
+      }
       /* commit the selected move */
       int e = best_e, rt = best_rt;
       if (!X(e, rt)) {

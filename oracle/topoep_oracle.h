@@ -65,6 +65,8 @@ typedef struct {
 #define REF_ST_NEG_LOAD 2u    /* a negative entry in global_load                  */
 #define REF_ST_SELF_DIFF 4u   /* global_load[self] differs from the histogram     */
 #define REF_ST_RANGE 8u       /* loads or costs exceed the exact integer range    */
+#define REF_ST_ITER 32u       /* a domain still had a refinement move after       */
+                              /* iter_limit of them (the plan stays valid)         */
 #define REF_ST_COST 64u       /* a general cost matrix is not symmetric, has a    */
                               /* nonzero diagonal or a negative entry, or an      */
                               /* expert size is negative                          */
@@ -103,6 +105,20 @@ int topoep_plan_ref_general(const ref_topology *topo, const int32_t *cost_matrix
                             int32_t replica_budget, int32_t *replica_slots,
                             int32_t *token_dest, int32_t *send_counts,
                             int32_t *recv_counts, int32_t *status, ref_debug *dbg);
+
+/* Committed refinement moves per domain after which a domain that still
+ * has a move stops with REF_ST_ITER (the entry points above use it). */
+#define REF_ITER_LIMIT (1 << 22)
+
+/* topoep_plan_ref_general with an explicit bound iter_limit >= 0 on the
+ * refinement moves of each domain. */
+int topoep_plan_ref_capped(const ref_topology *topo, const int32_t *cost_matrix,
+                           const int64_t *expert_bytes, const int32_t *global_load,
+                           const int32_t *local_topk, int32_t T, int32_t k,
+                           int32_t replica_budget, int32_t *replica_slots,
+                           int32_t *token_dest, int32_t *send_counts,
+                           int32_t *recv_counts, int32_t *status, ref_debug *dbg,
+                           int32_t iter_limit);
 
 /* Dispatch layout of the rerouted assignments: send_offsets[R + 1] is the
  * exclusive prefix of send_counts; token_slot[n] = send_offsets[dest] + the

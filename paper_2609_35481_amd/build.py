@@ -18,16 +18,32 @@ HIPCC_FLAGS = [
 ]
 
 
+# The same library with phase stamps (-DTOPOEP_STAMPS): the solver and the
+# first chunk write the wall clock at phase boundaries into the workspace's
+# control words.  For measurement only (bench.py --phases); the product
+# library is LIB.
+STAMPS_LIB = os.path.join(HERE, "libtopoep_stamps.so")
+
+
 def build(verbose: bool = False) -> str:
+    """Compile LIB and STAMPS_LIB (two hipcc processes side by side)."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-o", tmp, *SRCS]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
-    if verbose:
-        print(res.stderr)
-    os.replace(tmp, LIB)
+    jobs = []
+    for out, extra in ((LIB, []), (STAMPS_LIB, ["-DTOPOEP_STAMPS"])):
+        tmp = out + ".tmp%d" % os.getpid()
+        cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, "-o", tmp, *SRCS]
+        jobs.append((out, tmp, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+    errors = []
+    for out, tmp, proc in jobs:
+        so, se = proc.communicate()
+        if proc.returncode != 0:
+            errors.append("hipcc failed for %s:\n%s%s" % (os.path.basename(out), so, se))
+            continue
+        if verbose:
+            print(se)
+        os.replace(tmp, out)
+    if errors:
+        raise RuntimeError("\n".join(errors))
     return LIB
 
 

@@ -37,6 +37,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+#include <vector>
+
 #include "fastdiv.h"
 #include "topoep.h"
 #include "wave.h"
@@ -55,13 +59,29 @@ constexpr int kCtrlFinal = 3;    // final status of the plan (read by reroute)
 constexpr int kCtrlTotal = 4;    // uint64 at words 4..5: sum of positive loads
 constexpr int kCtrlMoves = 6;    // refinement moves of the per-domain solver
 constexpr int kCtrlHelpers = 7;  // offset helpers that have published their experts' totals
-// one-launch plan: chunks whose counts are written, then the last chunk's
-// verdict on top: nb + kVerdictSame when the histogram equals row self of
-// Omega and no id is bad (the counts are cleared), nb + kVerdictRedo
-// otherwise (the counts stay for the solver)
+// one-launch plan.  Every word a wait reads carries the plan's generation g,
+// so a word left over by an earlier plan (one whose bounded wait gave up)
+// never satisfies a later wait, and no word needs clearing between plans:
+//   words 8..9   arrivals of the chunk workgroups, 64-bit, never reset: nb per
+//                plan, so the chunk that moves it from g nb + c learns g and
+//                whether it is the last (c = nb - 1);
+//   word 10      g itself, read by the solver at its start and advanced by it
+//                at its end (arrivals = g nb holds between plans);
+//   word 11      the last chunk's verdict ((g + 1) << 2) | v (the tag g + 1
+//                so that a zero-filled word is no generation's): v =
+//                kVerdictSame when the histogram equals row self of Omega and
+//                no id is bad, kVerdictRedo otherwise;
+//   flags[b]     word 0: g + 1 once the solver's plan is ready; word 1: g + 1
+//                once every chunk's counts are written;
+//   ghist[g & 1] the histogram of plan g (atomic adds of the chunks), cleared
+//                for plan g + 1 by the solver of plan g at its start.
 constexpr int kCtrlArrive = 8;
+constexpr int kCtrlGen = 10;
+constexpr int kCtrlVerdict = 11;
 constexpr uint32_t kVerdictSame = 1;
 constexpr uint32_t kVerdictRedo = 2;
+// words 16..63: phase stamps of the instrumented build (TOPOEP_STAMPS)
+constexpr int kCtrlStamps = 16;
 
 constexpr uint32_t kNoPlan = TOPOEP_ST_BAD_ID | TOPOEP_ST_NEG_LOAD | TOPOEP_ST_RANGE | TOPOEP_ST_COST;
 constexpr int kLdsLimit = 160 * 1024;   // LDS per workgroup on gfx950
@@ -72,10 +92,10 @@ constexpr int kOffsetExperts = 64;      // experts per offset workgroup
 constexpr int kFusedBlocks = 64;        // chunk workgroups the single-launch plan aims for
 constexpr int kMaxFusedBlocks = 128;    // and at most (all co-resident: 256 CUs)
 constexpr int kFlagStride = 32;         // words between ready flags (one 128-byte line each)
-constexpr uint32_t kSpinLimit = 1u << 24;
+constexpr uint32_t kSpinLimit = 1u << 24;    // polls of a bounded wait before it gives up
 constexpr uint32_t kHelperSpin = 1u << 12;   // polls of the offset helpers' counter before summing alone
 constexpr int kListRegs = 4;   // instances per thread the instance list keeps in registers
-constexpr uint32_t kIterLimit = 1u << 22;
+constexpr uint32_t kIterLimit = 1u << 22;    // refinement moves per domain before ITER
 
 // ---------------------------------------------------------------- plan
 
@@ -86,7 +106,8 @@ struct Plan {
   int64_t n, chunk;
   int nb, n_solvers, n_helpers;
   int rchunks_all, rchunks_dom;   // routing: source-domain chunks (divisors of M)
-  uint32_t spin_limit, iter_limit;
+  uint32_t spin_limit;   // polls of a bounded wait (0: every such wait gives up at once)
+  uint32_t iter_limit;   // committed refinement moves per domain before ITER
   FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
@@ -99,9 +120,47 @@ struct Plan {
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
   int32_t *htot;   // three-kernel plan: each expert's count over the histogram blocks [E]
-  uint32_t *pub, *flags, *ghist;   // one-launch plan: chunk counts, flags, histogram (E + 1 words)
+  // one-launch plan: each chunk's per-expert counts [nb][E], the histogram
+  // of the ids with a bad-id count [2][E + 1] (one buffer per generation
+  // parity), one flag line per chunk (kFlagStride words apart)
+  uint32_t *pub, *ghist, *flags;
 };
 
+
+// Phase stamps of the instrumented build (compiled with -DTOPOEP_STAMPS into
+// a separate library for measurement; the product library has none):
+// thread 0 of the calling workgroup keeps the low word of the 100 MHz
+// constant clock (STAMP) or of the core clock (STAMP_CLK) for slot i (0..47)
+// in LDS, and STAMP_FLUSH copies slots [lo, hi) to the control words 16..63
+// at the end of the role.  Stamps stay out of global memory until then: on
+// gfx9 a wait for any load also waits for every earlier store, so a store
+// per stamp would delay the phase that follows it.
+#ifdef TOPOEP_STAMPS
+__shared__ uint32_t stamp_lds[48];
+#define STAMP(p, i)                                                          \
+  do {                                                                       \
+    if (threadIdx.x == 0) stamp_lds[(i)] = (uint32_t)__builtin_readsteadycounter(); \
+  } while (0)
+#define STAMP_CLK(p, i)                                                      \
+  do {                                                                       \
+    if (threadIdx.x == 0) stamp_lds[(i)] = (uint32_t)__builtin_amdgcn_s_memtime(); \
+  } while (0)
+#define STAMP_FLUSH(p, lo, hi)                                               \
+  do {                                                                       \
+    if (threadIdx.x == 0)                                                    \
+      for (int s_ = (lo); s_ < (hi); ++s_) (p).ctrl[kCtrlStamps + s_] = stamp_lds[s_]; \
+  } while (0)
+#else
+#define STAMP(p, i) \
+  do {              \
+  } while (0)
+#define STAMP_CLK(p, i) \
+  do {                  \
+  } while (0)
+#define STAMP_FLUSH(p, lo, hi) \
+  do {                         \
+  } while (0)
+#endif
 
 // The solvers hold more uniform values (sizes, divisors, LDS offsets,
 // pointers) than the scalar register file takes; the spilled ones come back
@@ -215,7 +274,7 @@ __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
   l.ptr = o;  o += p.E + 1;                  // instance list: first entry per expert
   l.er = o;   o += p.nent_cap;               //   instance rank
   l.eend = o; o += p.nent_cap;               //   cumulative share
-  l.gs = o;   o += imax(nt, p.E);            // partial sums of the chunk's offsets
+  l.gs = o;   o += imax(nt, p.E);            // partial sums of the chunk's offsets, then counts per rank
   l.so = o;   o += p.R + 1 + (nt >> 6) + 1;  // send offsets and their scan scratch
   l.flag = o; o += 4;
   l.words = o;
@@ -428,7 +487,7 @@ __device__ void load_fast(const Plan &p, int *om, int *hs, int *scratch, int *mi
 // (offset workgroup h of n_helpers handles kOffsetExperts experts at a time),
 // and each expert's count over all blocks (htot, the histogram of
 // local_topk), announced by one increment of the helpers' counter.
-__device__ void block_offsets(const Plan &p, int h, int *scratch) {
+__device__ void block_offsets(const Plan &p, int h, int *scratch, bool announce) {
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, E = p.E, nb = p.nb;
   const int el = tid & 63, g = tid >> 6;
   const int per = (nb + nw - 1) / nw;
@@ -465,6 +524,8 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch) {
     __syncthreads();
   }
   // publish: every total written before the count of finished helpers
+  // (only the per-domain solver reads it)
+  if (!announce) return;
   drain_then_barrier();
   if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlHelpers], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -525,14 +586,13 @@ __device__ bool grid_barrier(uint32_t *count, uint32_t groups, uint32_t spin_lim
   drain_then_barrier();
   if (threadIdx.x == 0) {
     __hip_atomic_fetch_add(count, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t it = 0;
-    int ok = 1;
-    while (__hip_atomic_load(count, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < groups) {
-      if (++it > spin_limit) {
-        ok = 0;
+    int ok = 0;
+    for (uint32_t it = 0; it < spin_limit; ++it) {
+      if (it > 0) __builtin_amdgcn_s_sleep(1);
+      if (__hip_atomic_load(count, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) >= groups) {
+        ok = 1;
         break;
       }
-      __builtin_amdgcn_s_sleep(1);
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     *flag = ok;
@@ -549,16 +609,6 @@ __global__ __launch_bounds__(1024) void hist_kernel(Plan p) {
   int *h = smem_h;
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
-  if (b == 0 && tid == 0) {
-    // Reset the solver's control words; it runs after this kernel.
-    p.ctrl[kCtrlBar] = 0;
-    p.ctrl[kCtrlTicket] = 0;
-    p.ctrl[kCtrlStatus] = 0;
-    p.ctrl[kCtrlFinal] = 0;
-    p.ctrl[kCtrlMoves] = 0;
-    p.ctrl[kCtrlHelpers] = 0;
-    *reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal) = 0ull;
-  }
   for (int e = tid; e < p.E; e += nt) h[e] = 0;
   __syncthreads();
   const int64_t lo = (int64_t)b * p.chunk;
@@ -825,10 +875,6 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
   }
   uint32_t it = 0;
   for (;; ++it) {
-    if (it >= p.iter_limit) {
-      if (lane == 0) *flags |= TOPOEP_ST_ITER;
-      break;
-    }
     // busiest rank, lowest index on ties
     const int Lrb = (int)~min_u32(lane < G ? ~(uint32_t)lj : ~0u);
     const int rbj = __ffsll((long long)__ballot(lane < G && lj == Lrb)) - 1;
@@ -970,6 +1016,11 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     }
     const uint64_t m1 = wave_min_u64(k1);
     if (m1 == ~0ull) break;
+    // a move is still available after iter_limit of them: stop with ITER
+    if (it >= p.iter_limit) {
+      if (lane == 0) *flags |= TOPOEP_ST_ITER;
+      break;
+    }
     uint64_t win = __ballot(k1 == m1);
     if (__popcll(win) != 1) {
       const uint64_t m2 = wave_min_u64(k1 == m1 ? k2 : ~0ull);
@@ -1153,6 +1204,7 @@ __device__ int stage1_candidates_wave(const Plan &p, int d, const int *om, uint6
 // first cap ranks fill repl_d (pre-filled with -1) and ccnt[d] = the count.
 __device__ void stage1_domain_wave(const Plan &p, int d, const int *om, uint64_t *ck_d, int *ccnt, int *repl_d) {
   const int nc = stage1_candidates_wave(p, d, om, ck_d);
+  if (d == 0) STAMP(p, 22);
   for (int c = lane_id(); c < nc; c += 64) rank_candidates(c, nc, p.cap1, ck_d, repl_d);
   if (lane_id() == 0) ccnt[d] = nc;
 }
@@ -1323,7 +1375,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   extern __shared__ int64_t smem_s[];
   int *sm = reinterpret_cast<int *>(smem_s);
   if ((int)blockIdx.x >= p0.n_solvers) {
-    block_offsets(p0, blockIdx.x - p0.n_solvers, sm);
+    block_offsets(p0, blockIdx.x - p0.n_solvers, sm, true);
     return;
   }
   const Plan p = solver_plan(p0);
@@ -1630,8 +1682,16 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
                           ? 0
                           : (int32_t)__hip_atomic_load(&p.ctrl[kCtrlMoves], __ATOMIC_RELAXED,
                                                        __HIP_MEMORY_SCOPE_AGENT);
+    // every solver workgroup has taken its ticket, so the words it
+    // accumulated are final: restore them for the next solve (which may be
+    // this stage again, without a histogram kernel before it); the helpers'
+    // count goes back by their number (one still running adds its own last)
     p.ctrl[kCtrlBar] = 0;
     p.ctrl[kCtrlTicket] = 0;
+    p.ctrl[kCtrlStatus] = 0;
+    p.ctrl[kCtrlMoves] = 0;
+    *reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal) = 0ull;
+    __hip_atomic_fetch_sub(&p.ctrl[kCtrlHelpers], (uint32_t)p.n_helpers, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -1715,7 +1775,7 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
 template <bool Pairs = false>
-__device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
+__device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
                             bool write_status = true, bool read_arrival = false) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
@@ -1740,10 +1800,12 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
     return;
   }
   lds_barrier();
+  STAMP(p, 23);
 
   // ---- inter-node placement (Eq. 9): one wave per domain
   for (int d = wave; d < M; d += nw) stage1_domain_wave(p, d, om, ck + (int64_t)d * E, ccnt, repl + d * cap);
   lds_barrier();
+  STAMP(p, 2);
 
   // ---- hosting domains per expert; every rank's slots and instances, and
   // the local ranks hosting each expert in its domain (one pass: stage-1
@@ -1796,6 +1858,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
   }
   lds_barrier();
 
+  STAMP(p, 3);
   // ---- routing construction (Section 4.3) for every domain's instances;
   // instances of domains that cannot refine enter this rank's instance-list
   // bitmaps and send counts at once
@@ -1812,6 +1875,7 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
       p, M * I, p.fMI, p.rchunks_all, e_of, mask, fdt, qcol, U, [&](int, int e) { return om + e; }, E,
       [&](int i) { return (int)fdiv((uint32_t)i, p.fI); }, [&](int d) { return dfree[d] != 0; }, mark);
   lds_barrier();
+  STAMP(p, 4);
 
   if (misc[14]) {
     // ---- intra-node refinement (Eq. 10): one wave per domain (it sums its
@@ -1834,18 +1898,21 @@ __device__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, b
     lds_barrier();
   }
 
+  STAMP(p, 5);
   // ---- outputs: replica slots, send counts, this rank's instance list
   for (int i = tid; i < R * p.N; i += nt) {
     const int r = (int)fdiv((uint32_t)i, p.fN), t2 = i - r * p.N;
     p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
   }
   for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
-  // (one-launch plan: the arrival word read here is in by the end of the
+  // (one-launch plan: the verdict word read here is in by the end of the
   // instance list, so its wait costs no round trip once the chunks are done)
   uint32_t arrival = 0;
   if (read_arrival && tid == 0)
-    arrival = __hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    arrival = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  STAMP(p, 6);
   emit_instance_list(p, qcol, slots, used, bm, t.wt);
+  STAMP(p, 7);
   if (read_arrival && tid == 0) misc[6] = (int)arrival;
   if (write_status && tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
@@ -1891,7 +1958,7 @@ __global__ __launch_bounds__(1024) void solve_single_kernel(Plan p0) {
   extern __shared__ int64_t smem_1[];
   int *sm = reinterpret_cast<int *>(smem_1);
   if (blockIdx.x > 0) {
-    block_offsets(p0, blockIdx.x - 1, sm);
+    block_offsets(p0, blockIdx.x - 1, sm, false);
     return;
   }
   const Plan p = solver_plan(p0);
@@ -2104,26 +2171,32 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 
 // ---------------------------------------------------------------- single-launch plan
 //
-// Workgroup 0 solves; workgroups 1..nb each hold one chunk of ids.
-//   chunk -> solver: chunk b writes its count of every expert to
-//     pub[b * E + e], adds it to the histogram ghist[e] with an agent-scope
-//     atomic (integer adds commute: the sum does not depend on their order;
-//     ghist[E] collects a bad-id flag), then increments the arrival counter
-//     with release semantics.  Only the solver polls the counter (many
-//     pollers of one word serialise at the memory side); it reads the E + 1
-//     histogram words (one CU cannot pull every chunk's counts quickly) and
-//     clears them and the counter for the next plan.
-//   solver -> chunk b, flag 1 ("every chunk's counts are written"): set as
-//     soon as the counter is complete; chunk b then sums the counts of the
-//     chunks before it (its first occurrence index per expert) while the
-//     solver works.
-//   solver -> chunk b, flag 2 ("plan ready"): after the outputs and this
-//     rank's instance list are written (release).  Chunk b polls only its
-//     own flag word flags[b * kFlagStride] (one 128-byte line each) and
-//     clears it after seeing 2.
-// Between plans the counter and every flag are zero again; a workspace is
-// zero-filled before its first plan.  A bounded wait that gives up sets SYNC
-// and leaves that state undefined (the workspace is zero-filled again).
+// Workgroup 0 solves; workgroups 1..nb each hold one chunk of ids.  The
+// plan's generation g orders the hand-overs (control words 8..11 above):
+//   chunk -> everyone: chunk b writes its count of every expert to
+//     pub[b][e] and adds it to the histogram ghist[g & 1][e] with an
+//     agent-scope atomic (integer adds commute: the sum does not depend on
+//     their order; word E counts bad ids), then makes one release increment
+//     of the 64-bit arrival counter; the value it moves the counter from,
+//     g nb + c, gives g and tells the last arrival (c = nb - 1).  A chunk
+//     reads g from word 10 to pick the histogram buffer before it arrives;
+//     that read can only be stale when the solver has already given up on
+//     this plan, and the chunk then takes its adds back.
+//   last chunk -> chunks: word 1 of every chunk's flag line = g + 1
+//     (release): every count is written.  Chunk b then sums its first
+//     occurrence index of each expert from the counts of the chunks before
+//     it, or from the histogram less the counts of the chunks from b on,
+//     whichever reads fewer rows (at most nb / 2).
+//   last chunk -> solver: the histogram against row self of Omega, released
+//     as the verdict ((g + 1) << 2) | v.  Only the solver polls that word.
+//   solver -> chunk b: word 0 of chunk b's flag line = g + 1 (release) once
+//     the outputs, this rank's instance list and the final status are
+//     written.  Chunk b polls only its own 128-byte flag line, acquires, and
+//     reads the instance list in one round trip.
+// No word is cleared between plans except the other histogram buffer (by
+// the solver, before any chunk of the next plan can use it): a workspace is
+// zero-filled before its first plan, and a plan whose bounded wait gave up
+// (SYNC) leaves nothing that a later plan's waits could mistake for its own.
 
 // Omega to LDS with its status bits and total load (row self included as
 // gathered; the caller swaps in the histogram later).  `between` runs on
@@ -2175,17 +2248,15 @@ __device__ void load_omega(const Plan &p, int *om, int *misc, Between between) {
   }
 }
 
-// Solver side of the first hand-over, once every chunk has arrived: hs[e] =
-// ghist[e], the histogram of local_topk, BAD_ID from ghist[E]; then the
-// words are cleared for the next plan.
-__device__ void collect_counts(const Plan &p, int *hs, int *misc) {
+// Solver side of a redo: hs[e] = the histogram of local_topk, gh[e] (every
+// chunk's adds, acquired with the last chunk's verdict), BAD_ID from gh[E].
+__device__ __forceinline__ void read_histogram(const Plan &p, const uint32_t *gh, int *hs, int *misc) {
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
   bool bad = false;
   for (int e = tid; e <= E; e += nt) {
-    const uint32_t v = p.ghist[e];
+    const uint32_t v = gh[e];
     if (e < E) hs[e] = (int)v;
     else bad = v != 0;
-    __hip_atomic_store(p.ghist + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   const uint64_t any_bad = __ballot(bad);
   if (lane_id() == 0 && any_bad) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), TOPOEP_ST_BAD_ID);
@@ -2196,14 +2267,28 @@ __device__ void collect_counts(const Plan &p, int *hs, int *misc) {
 // from it while the chunks count; once the last chunk has compared the
 // histogram with row self of Omega, that plan stands (equal rows, so Omega'
 // = Omega) or is made again from Omega' on fresh state; then every chunk's
-// flag 2.
+// flag is set to g + 1 and the generation advances.
 template <bool Pairs>
 __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
+  // this plan's generation (stored by the previous plan's solver); wave 0
+  // waits for the verdict and sets the flags
+  uint32_t gen = 0;
+  if (tid < 64) {
+    gen = __hip_atomic_load(&p.ctrl[kCtrlGen], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the next plan's histogram buffer starts from zero (stored long before
+    // this plan ends, which is when that plan's chunks may start)
+    uint32_t *other = p.ghist + ((gen + 1u) & 1u) * (p.E + 1);
+    for (int e = tid; e <= p.E; e += 64) __hip_atomic_store(other + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  STAMP(p, 0);
+  STAMP_CLK(p, 20);
   if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
   load_omega(p, t.om, t.misc, [&] { single_init(p, t); });
+  if (tid == 0) t.misc[40] = (int)gen;   // (single_init clears words 0..15 only)
   lds_barrier();
+  STAMP(p, 1);
   const uint64_t total0 = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
   const uint32_t neg0 = (uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD;
   const uint32_t gst0 = neg0 | (out_of_range(p, total0) ? TOPOEP_ST_RANGE : 0u);
@@ -2213,30 +2298,31 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
   if (spec) single_plan<Pairs>(p, t, gst0, true, false, true);
-  // wait until every chunk has written its counts and the last one has
-  // added its verdict
+  STAMP(p, 8);
+  // the last chunk's verdict on this generation (the word read while the
+  // instance list was built is usually it already)
   if (tid == 0) {
-    const uint32_t nb = (uint32_t)p.nb;
-    uint32_t v = spec ? (uint32_t)t.misc[6] : 0u, it = 0;
-    int ok = 1;
-    while (v <= nb) {
-      if (++it > p.spin_limit) {
-        ok = 0;
+    const uint32_t want = (gen + 1u) & 0x3FFFFFFFu;
+    uint32_t w = (uint32_t)t.misc[6];
+    bool ok = false;
+    for (uint32_t it = 0; it < p.spin_limit; ++it) {
+      if (it > 0 || !spec) {
+        if (it > 0) __builtin_amdgcn_s_sleep(1);
+        w = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if ((w >> 2) == want) {
+        ok = true;
         break;
       }
-      __builtin_amdgcn_s_sleep(1);
-      v = __hip_atomic_load(&p.ctrl[kCtrlArrive], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (ok) {
-      v -= nb;
-      // the counts are read only when the plan is redone
-      if (v != kVerdictSame) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      __hip_atomic_store(&p.ctrl[kCtrlArrive], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    // acquire: the histogram of a redo, and (passed on by the flags' release)
+    // the chunks' offsets the last chunk wrote
+    if (ok) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     t.misc[2] = ok;
-    t.misc[3] = (int)v;
+    t.misc[3] = (int)(w & 3u);
   }
   __syncthreads();
+  STAMP(p, 9);
   const bool synced = t.misc[2] != 0;
   const uint32_t verdict = (uint32_t)t.misc[3];
   const bool stands = synced && verdict == kVerdictSame && spec;
@@ -2258,7 +2344,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
     // Omega' (row self = the histogram) on fresh state
     single_init(p, t);
     lds_barrier();
-    collect_counts(p, t.hs, t.misc);
+    read_histogram(p, p.ghist + (int64_t)(t.misc[40] & 1) * (E + 1), t.hs, t.misc);
     bool diff = false;
     int64_t adj = 0;
     for (int e = tid; e < E; e += nt) {
@@ -2283,64 +2369,112 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   }
   if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
   // release: every output the chunks read (the instance list, the final
-  // status, the send offsets) before the flags
+  // status, the send offsets) before the flags; then the next generation
   drain_then_barrier();
-  if (tid < 64)
+  STAMP(p, 10);
+  STAMP_CLK(p, 21);
+  if (tid < 64) {
     for (int b = tid; b < p.nb; b += 64)
-      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, 2u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, gen + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&p.ctrl[kCtrlGen], gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  STAMP_FLUSH(p, 0, 12);
+  STAMP_FLUSH(p, 20, 25);
   // receive counts of a plan that was made (a refused one wrote zeros):
   // for the caller only, so they are summed while the chunks route
   if (planned && p.recv_out) single_recv_counts(p, t);
 }
 
-// The last chunk to arrive (every count is written): flag 1 of every chunk,
-// so they sum their offsets; then the histogram (the summed counts) against
-// row self of Omega and the bad-id word, and the verdict added to the
-// arrival word (the counts cleared for the next plan unless the solver
-// needs them).
-__device__ void last_arrival(const Plan &p) {
+// x / d for x < 2^52 and 0 < d < 2^31: the quotient formed in double
+// precision (within one of the exact one there), then corrected to the floor.
+__device__ inline uint64_t div_u64_small(uint64_t x, uint32_t d) {
+  uint64_t q = (uint64_t)((double)x / (double)d);
+  int64_t r = (int64_t)(x - q * d);
+  while (r < 0) {
+    --q;
+    r += d;
+  }
+  while (r >= (int64_t)d) {
+    ++q;
+    r -= d;
+  }
+  return q;
+}
+
+// The last chunk to arrive (every chunk's counts are in pub and in
+// ghist[g & 1]): word 1 of every chunk's flag line (the chunks start summing
+// their offsets), then the histogram against row self of Omega and the
+// bad-id count, released as the verdict of generation g.
+__device__ __forceinline__ void last_arrival(const Plan &p, uint32_t g) {
   const int tid = threadIdx.x, E = p.E;
   if (tid < 64)
     for (int c = tid; c < p.nb; c += 64)
-      __hip_atomic_store(p.flags + (int64_t)c * kFlagStride, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(p.flags + (int64_t)c * kFlagStride + 1, g + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  const uint32_t *gh = p.ghist + (g & 1u) * (E + 1);
   bool diff = false;
   for (int e = tid; e <= E; e += blockDim.x) {
-    const uint32_t v = p.ghist[e];
+    const uint32_t v = gh[e];
     diff |= e < E ? (int)v != p.gl[(int64_t)p.self * E + e] : v != 0u;
   }
   const bool redo = __syncthreads_or(diff) != 0;
-  if (!redo)
-    for (int e = tid; e <= E; e += blockDim.x)
-      __hip_atomic_store(p.ghist + e, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  drain_then_barrier();
   if (tid == 0)
-    __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], redo ? kVerdictRedo : kVerdictSame, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&p.ctrl[kCtrlVerdict], (((g + 1u) & 0x3FFFFFFFu) << 2) | (redo ? kVerdictRedo : kVerdictSame),
+                       __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Bounded wait of chunk b's workgroup until its flag reaches `level`; after
-// level 2 it clears the flag for the next plan.  Thread 0 polls (more
-// pollers per chunk slow every agent-coherent load down), then acquires (the
-// L1 and L2 invalidations cover the whole CU).  Returns false (on every
-// thread) if the wait gave up.
-__device__ bool wait_flag(const Plan &p, int b, uint32_t level, int *flag) {
+// Bounded wait of chunk b's workgroup until word w of its flag line holds
+// `target` (the plan's generation + 1), at most spin_limit polls.  Thread 0
+// polls (more pollers per chunk slow every agent-coherent load down), then
+// acquires (the L1 and L2 invalidations cover the whole CU).  Returns false
+// (on every thread) if the wait gave up.
+__device__ __forceinline__ bool wait_flag(const Plan &p, int b, int w, uint32_t target, int *flag) {
   if (threadIdx.x == 0) {
-    uint32_t *f = p.flags + (int64_t)b * kFlagStride;
-    uint32_t it = 0;
-    int ok = 1;
-    while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < level) {
-      if (++it > p.spin_limit) {
-        ok = 0;
+    uint32_t *f = p.flags + (int64_t)b * kFlagStride + w;
+    int ok = 0;
+    for (uint32_t it = 0; it < p.spin_limit; ++it) {
+      if (it > 0) __builtin_amdgcn_s_sleep(2);
+      if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == target) {
+        ok = 1;
         break;
       }
-      __builtin_amdgcn_s_sleep(2);
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if (ok && level == 2u) __hip_atomic_store(f, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *flag = ok;
   }
   __syncthreads();
   return *flag != 0;
+}
+
+// Chunk b's first occurrence index of every expert (run[e]) once every
+// count is written: the sum of the counts of chunks 0 .. b - 1, or the
+// histogram gh less the counts of chunks b .. nb - 1 when that reads fewer
+// rows.  Thread (grp, e) sums its share of the rows with eight loads in
+// flight; gs: blockDim words of partial sums.
+__device__ __forceinline__ void chunk_offsets(const Plan &p, int b, const uint32_t *gh, int *run, int *gs) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, nb = p.nb;
+  const bool from_start = 2 * b <= nb;
+  const int r0 = from_start ? 0 : b, cnt = from_start ? b : nb - b;
+  const int groups = imax(1, nt / E);
+  const int per = (cnt + groups - 1) / groups;
+  for (int t = tid; t < groups * E; t += nt) {
+    const int g = (int)fdiv((uint32_t)t, p.fE), e = t - g * E;
+    const int b0 = r0 + g * per, n = imax(0, imin(r0 + cnt, b0 + per) - b0);
+    int sum = 0;
+    for (int j0 = 0; j0 < n; j0 += 8) {
+      uint32_t w[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) w[u] = p.pub[(int64_t)(b0 + imin(j0 + u, n - 1)) * E + e];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += j0 + u < n ? (int)w[u] : 0;
+    }
+    gs[t] = sum;
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += nt) {
+    int sum = 0;
+    for (int g = 0; g < groups; ++g) sum += gs[g * E + e];
+    run[e] = from_start ? sum : (int)gh[e] - sum;
+  }
 }
 
 // Send-buffer slots of a chunk of the one-launch plan, with three barriers:
@@ -2404,13 +2538,13 @@ __device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT],
 
 // Chunk role (workgroup 1 + b): ids [b * chunk, (b + 1) * chunk) stay in
 // registers for the whole plan.  Each wave ranks its ids among equal ids
-// (row-major order) and the workgroup writes its counts and arrives (the
-// last to arrive sets every chunk's flag 1 and checks the histogram); once
-// every chunk has, it sums the counts of the chunks before it; after the
-// plan is ready each id's occurrence index rho = (offset of the chunk) +
-// (offset of the wave in the chunk) + (rank in the wave) picks the
-// instance from this rank's instance list.  A bounded wait that gives up
-// writes -1 and SYNC.
+// (row-major order); the workgroup writes its counts, adds them to the
+// histogram and arrives (the last to arrive announces that every count is
+// written and sends the verdict); it then sums its first occurrence index
+// per expert; once the plan is ready each id's occurrence index rho =
+// (offset of the chunk) + (offset of the wave in the chunk) + (rank in the
+// wave) picks the instance from this rank's instance list.  A bounded wait
+// that gives up writes -1 and SYNC.
 template <int IPT>
 __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   const ChunkLds l = chunk_lds(p, blockDim.x);
@@ -2427,6 +2561,8 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
     const int64_t idx = wbase + i * 64;
     ev[i] = idx < hi ? p.topk[idx] : -1;
   }
+  // the generation as the solver left it: the histogram buffer to add to
+  const uint32_t gread = __hip_atomic_load(&p.ctrl[kCtrlGen], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   int *mywc = wc + wave * E;
   for (int e = lane; e < E; e += 64) mywc[e] = 0;
   wave_sync();
@@ -2446,6 +2582,7 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   }
   bad = __syncthreads_or(bad);
   // publish the chunk's counts; wc becomes each wave's offset in the chunk
+  uint32_t *gh = p.ghist + (gread & 1u) * (E + 1);
   for (int e = tid; e < E; e += nt) {
     int sum = 0;
     for (int w = 0; w < nw; ++w) {
@@ -2453,49 +2590,47 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
       wc[w * E + e] = sum;
       sum += c;
     }
-    p.pub[b * E + e] = (uint32_t)sum;
-    if (sum) atomicAdd(p.ghist + e, (uint32_t)sum);
+    p.pub[(int64_t)b * E + e] = (uint32_t)sum;
+    if (sum) atomicAdd(gh + e, (uint32_t)sum);
   }
-  if (tid == 0 && bad) atomicOr(p.ghist + E, 1u);
+  if (tid == 0 && bad) atomicAdd(gh + E, 1u);
   drain_then_barrier();
   if (tid == 0) {
-    const uint32_t before =
-        __hip_atomic_fetch_add(&p.ctrl[kCtrlArrive], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    const bool last = before + 1u == (uint32_t)p.nb;
+    const uint64_t before = __hip_atomic_fetch_add(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlArrive), 1ull,
+                                                   __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t g = div_u64_small(before, (uint32_t)p.nb);
+    const bool last = before - g * (uint64_t)p.nb == (uint64_t)(p.nb - 1);
     // the last arrival acquires every other chunk's counts
     if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     flag[1] = last;
+    flag[2] = (int)(uint32_t)g;
   }
   __syncthreads();
-  if (flag[1]) last_arrival(p);
-  // flag >= 1: every chunk's counts are written; this chunk's first
-  // occurrence index of e is the sum of the counts of chunks 0 .. b-1
-  bool ok = wait_flag(p, b, 1u, flag);
-  if (ok) {
-    const int groups = imax(1, nt / E);
-    const int per = (b + groups - 1) / groups;
-    for (int t = tid; t < groups * E; t += nt) {
-      const int g = (int)fdiv((uint32_t)t, p.fE), e = t - g * E;
-      const int b0 = g * per, cnt = imax(0, imin(b, b0 + per) - b0);
-      int sum = 0;
-      for (int j0 = 0; j0 < cnt; j0 += 8) {
-        uint32_t w[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) w[u] = p.pub[imin(b0 + j0 + u, b0 + cnt - 1) * E + e];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) sum += j0 + u < cnt ? (int)w[u] : 0;
-      }
-      gs[t] = sum;
-    }
-    __syncthreads();
+  if (b == 0) STAMP(p, 12);
+  const uint32_t gen = (uint32_t)flag[2];
+  if (gen != gread) {
+    // the solver has already given up on this plan and moved on: take the
+    // adds back out of the next plan's buffer (it starts after this kernel)
     for (int e = tid; e < E; e += nt) {
-      int sum = 0;
-      for (int g = 0; g < groups; ++g) sum += gs[g * E + e];
-      run[e] = sum;
+      const uint32_t c = p.pub[(int64_t)b * E + e];
+      if (c) atomicSub(gh + e, c);
     }
-    // flag 2: the plan is ready
-    ok = wait_flag(p, b, 2u, flag);
+    if (tid == 0 && bad) atomicSub(gh + E, 1u);
   }
+  if (flag[1]) {
+    STAMP(p, 19);
+    last_arrival(p, gen);
+    STAMP(p, 13);
+    STAMP_FLUSH(p, 13, 14);
+    STAMP_FLUSH(p, 19, 20);
+  }
+  // every count is written: this chunk's first occurrence index per expert
+  bool ok = wait_flag(p, b, 1, gen + 1u, flag);
+  if (ok) chunk_offsets(p, b, p.ghist + (gen & 1u) * (E + 1), run, gs);
+  if (b == 0) STAMP(p, 16);
+  // the plan is ready
+  ok = ok && wait_flag(p, b, 0, gen + 1u, flag);
+  if (b == 0) STAMP(p, 14);
   uint32_t fin = 0;
   if (ok) {
     // the instance list and the final status in one round trip: every load
@@ -2557,6 +2692,11 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
     dv[i] = dest;
   }
   if (p.slot_out) chunk_slots<IPT>(p, dv, wbase, hi, run, ptr, er, eend, so, gs, wc);
+  if (b == 0) {
+    STAMP(p, 15);
+    STAMP_FLUSH(p, 12, 13);
+    STAMP_FLUSH(p, 14, 17);
+  }
 }
 
 // The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold
@@ -2604,6 +2744,7 @@ __global__ __launch_bounds__(1024) void empty_kernel(Plan p) { (void)p; }
 
 struct Shape {
   int ipt, bt, st;
+  size_t zero_bytes;   // workspace prefix that must be zero before a first plan
   int mode;       // 1 single-workgroup solver, 2 per-domain solver (three kernels each), 3 one launch
   size_t lds_hist, lds_solve, lds_reroute, lds_fused;
   int solve_groups;
@@ -2616,6 +2757,55 @@ int ceil_log2(int v) {
   while ((1 << b) < v) ++b;
   return b;
 }
+
+template <typename K>
+void allow_lds(K kernel) {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
+}
+
+void set_attrs();
+
+// Workgroups of one kernel shape that the current device keeps resident at
+// once: its compute units times the shape's occupancy per unit.  Kernels
+// whose workgroups wait on each other (the one-launch plan, the per-domain
+// solver's grid barrier) are only chosen when every workgroup fits.  A
+// device that cannot be queried (no GPU: sizes only) counts as gfx950's
+// 256 compute units with one workgroup each, which every shape within the
+// LDS and thread limits checked here reaches.  Results are cached.
+int resident_capacity(const void *fn, int threads, size_t lds) {
+  struct Entry {
+    int dev;
+    const void *fn;
+    int threads;
+    size_t lds;
+    int cap;
+  };
+  static std::mutex mu;
+  static std::vector<Entry> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (const Entry &e : cache)
+      if (e.dev == dev && e.fn == fn && e.threads == threads && e.lds == lds) return e.cap;
+  }
+  set_attrs();
+  int cus = 0, occ = 0;
+  int cap = 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0 &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, threads, lds) == hipSuccess)
+    cap = cus * occ;
+  (void)hipGetLastError();   // a failed query is not the caller's error
+  std::lock_guard<std::mutex> lock(mu);
+  cache.push_back(Entry{dev, fn, threads, lds, cap});
+  return cap;
+}
+
+const void *fused_fn(int ipt, bool pairs);
 
 // Validate the arguments and fill the plan's sizes, launch shape and
 // workspace layout (pointers are offsets when ws == nullptr).
@@ -2653,6 +2843,12 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.n = (int64_t)T * k;
   q.spin_limit = kSpinLimit;
   q.iter_limit = kIterLimit;
+  if (lc) {
+    if (lc->spin_limit < -1 || lc->iter_limit < 0) return TOPOEP_EINVAL;
+    if (lc->spin_limit == -1) q.spin_limit = 0;   // every bounded wait gives up at once
+    else if (lc->spin_limit > 0) q.spin_limit = (uint32_t)lc->spin_limit;
+    if (lc->iter_limit > 0) q.iter_limit = (uint32_t)lc->iter_limit;
+  }
   q.general = general ? 1 : 0;
   if (general && R > 65535) return TOPOEP_ELIMIT;
   if ((int64_t)q.M * q.I * q.QS >= (1 << 30) || (int64_t)R * E >= (1 << 30)) return TOPOEP_ELIMIT;
@@ -2702,7 +2898,10 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     const int64_t chunk_words = (int64_t)chunk_lds(q, st).words;
     // (1 KiB left for the kernel's static LDS, which __syncthreads_or uses)
     const int64_t fused_words = single_words > chunk_words ? single_words : chunk_words;
-    const bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
+    bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
+    // every workgroup of the launch resident at once (they wait on each other)
+    if (fused_ok)
+      fused_ok = nbf + 1 <= resident_capacity(fused_fn(ipt, q.PN * (q.G - 1) <= 64), st, (size_t)fused_words * 4);
     if (solver == 3 && !fused_ok) return TOPOEP_ELIMIT;
     if (general && solver == 3) return TOPOEP_EINVAL;   // the general model runs the per-domain solver
     if (fused_ok && !general && (solver == 3 || solver == 0)) {
@@ -2753,6 +2952,9 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   if (s.st == 0) s.st = s.mode == 1 ? 1024 : 512;
   s.lds_solve = (size_t)(s.mode == 1 ? single_words : multi_words) * 4;
   q.n_solvers = s.mode == 1 ? 1 : imin(q.M, kMaxSolveGroups);
+  // the per-domain solver's workgroups meet at a grid barrier: all resident
+  if (s.mode == 2 && q.n_solvers > resident_capacity(reinterpret_cast<const void *>(solve_kernel), s.st, s.lds_solve))
+    return TOPOEP_ELIMIT;
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
   s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap +
@@ -2778,50 +2980,63 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     off = align256(off + bytes);
     return o;
   };
+  // every word a plan needs zero before its first use sits in the prefix
+  // [0, zero_bytes): the control words, then (one launch) the ready flags
+  const bool one = s.mode == 3;
+  const bool three = !one;
   const size_t o_ctrl = take(kCtrlBytes);
-  const size_t o_part = take((size_t)q.nb * E * 4);
-  const size_t o_offs = take((size_t)q.nb * E * 4);
-  const size_t o_berr = take((size_t)q.nb * 4);
-  const size_t o_repl = take((size_t)q.M * imax(q.cap1, 1) * 4);
-  const size_t o_sege = take((size_t)q.M * q.I * 4);
-  const size_t o_segq = take((size_t)q.M * q.I * 4);
+  const size_t o_flg = take(one ? (size_t)q.nb * kFlagStride * 4 : 0);
+  const size_t o_gh = take(one ? (size_t)2 * (E + 1) * 4 : 0);
+  s.zero_bytes = off;
+  const size_t o_part = take(three ? (size_t)q.nb * E * 4 : 0);
+  const size_t o_offs = take(three ? (size_t)q.nb * E * 4 : 0);
+  const size_t o_berr = take(three ? (size_t)q.nb * 4 : 0);
+  const size_t o_repl = take(s.mode == 2 ? (size_t)q.M * imax(q.cap1, 1) * 4 : 0);
+  const size_t o_sege = take(s.mode == 2 ? (size_t)q.M * q.I * 4 : 0);
+  const size_t o_segq = take(s.mode == 2 ? (size_t)q.M * q.I * 4 : 0);
   const size_t o_cptr = take((size_t)(E + 1) * 4);
   const size_t o_cr = take((size_t)q.nent_cap * 4);
   const size_t o_ce = take((size_t)q.nent_cap * 4);
-  const bool one = s.mode == 3;
-  const size_t o_ht = take(one ? 0 : (size_t)E * 4);
+  const size_t o_ht = take(three ? (size_t)E * 4 : 0);
   const size_t o_pub = take(one ? (size_t)q.nb * E * 4 : 0);
-  const size_t o_flg = take(one ? (size_t)q.nb * kFlagStride * 4 : 0);
-  const size_t o_gh = take(one ? (size_t)(E + 1) * 4 : 0);
   *ws_bytes = off;
   if (ws) {
-    q.ctrl = reinterpret_cast<uint32_t *>(ws + o_ctrl);
-    q.partials = reinterpret_cast<int32_t *>(ws + o_part);
-    q.offsets = reinterpret_cast<int32_t *>(ws + o_offs);
-    q.blk_err = reinterpret_cast<int32_t *>(ws + o_berr);
-    q.repl1 = reinterpret_cast<int32_t *>(ws + o_repl);
-    q.seg_e = reinterpret_cast<int32_t *>(ws + o_sege);
-    q.seg_q = reinterpret_cast<int32_t *>(ws + o_segq);
-    q.csr_ptr = reinterpret_cast<int32_t *>(ws + o_cptr);
-    q.csr_r = reinterpret_cast<int32_t *>(ws + o_cr);
-    q.csr_end = reinterpret_cast<int32_t *>(ws + o_ce);
-    q.htot = one ? nullptr : reinterpret_cast<int32_t *>(ws + o_ht);
-    q.pub = one ? reinterpret_cast<uint32_t *>(ws + o_pub) : nullptr;
-    q.flags = one ? reinterpret_cast<uint32_t *>(ws + o_flg) : nullptr;
-    q.ghist = one ? reinterpret_cast<uint32_t *>(ws + o_gh) : nullptr;
+    auto at = [&](size_t o, bool have) { return have ? reinterpret_cast<int32_t *>(ws + o) : nullptr; };
+    auto atu = [&](size_t o, bool have) { return have ? reinterpret_cast<uint32_t *>(ws + o) : nullptr; };
+    q.ctrl = atu(o_ctrl, true);
+    q.partials = at(o_part, three);
+    q.offsets = at(o_offs, three);
+    q.blk_err = at(o_berr, three);
+    q.repl1 = at(o_repl, s.mode == 2);
+    q.seg_e = at(o_sege, s.mode == 2);
+    q.seg_q = at(o_segq, s.mode == 2);
+    q.csr_ptr = at(o_cptr, true);
+    q.csr_r = at(o_cr, true);
+    q.csr_end = at(o_ce, true);
+    q.htot = at(o_ht, three);
+    q.flags = atu(o_flg, one);
+    q.pub = atu(o_pub, one);
+    q.ghist = atu(o_gh, one);
   }
   *p = q;
   *sh = s;
   return TOPOEP_OK;
 }
 
-template <typename K>
-void allow_lds(K kernel) {
-  (void)hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
-}
+std::atomic<bool> g_attrs_set{false};
 
-bool g_attrs_set = false;
+const void *fused_fn(int ipt, bool pairs) {
+  switch (ipt) {
+    case 1: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<1, true>)
+                         : reinterpret_cast<const void *>(plan_fused_kernel<1, false>);
+    case 2: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<2, true>)
+                         : reinterpret_cast<const void *>(plan_fused_kernel<2, false>);
+    case 4: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<4, true>)
+                         : reinterpret_cast<const void *>(plan_fused_kernel<4, false>);
+    default: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<8, true>)
+                          : reinterpret_cast<const void *>(plan_fused_kernel<8, false>);
+  }
+}
 
 void set_attrs() {
   if (g_attrs_set) return;
@@ -2844,6 +3059,8 @@ void set_attrs() {
   allow_lds(plan_fused_kernel<8, false>);
   allow_lds(plan_fused_kernel<8, true>);
   allow_lds(empty_kernel);
+  // (an attribute a kernel refuses must not linger as the caller's error)
+  (void)hipGetLastError();
   g_attrs_set = true;
 }
 

@@ -12,7 +12,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtopoep.so")
+# TOPOEP_STAMPS=1 loads the instrumented build (phase stamps in the
+# workspace's control words; bench.py --phases) instead of the product one.
+LIB_PATH = os.path.join(_HERE, "libtopoep_stamps.so" if os.environ.get("TOPOEP_STAMPS") == "1" else "libtopoep.so")
 
 OK = 0
 EINVAL = -1
@@ -48,10 +50,14 @@ class Topology(ctypes.Structure):
 
 
 class Launch(ctypes.Structure):
-    """topoep_launch: launch shape (results do not depend on it)."""
+    """topoep_launch: launch shape (results do not depend on it), and the
+    bounds of the in-kernel waits (spin_limit: 0 default, -1 give up at
+    once) and of the refinement (iter_limit: 0 default).  A tuple of up to
+    seven values fills the fields in order."""
     _fields_ = [("items_per_thread", ctypes.c_int32), ("block_threads", ctypes.c_int32),
                 ("tiles_per_block", ctypes.c_int32), ("solve_threads", ctypes.c_int32),
-                ("solver", ctypes.c_int32)]
+                ("solver", ctypes.c_int32), ("spin_limit", ctypes.c_int32),
+                ("iter_limit", ctypes.c_int32)]
 
 
 class Shape(ctypes.Structure):
@@ -249,9 +255,15 @@ class Planner:
                 self.send_counts.data_ptr(), self.status.data_ptr(), self.ws_ptr,
                 self.ws_bytes, sp)
 
-    def plan(self, global_load, local_topk, stream=None):
-        """Enqueue topoep_plan_ex; returns (replica_slots, token_dest, send_counts, status)."""
-        rc = _lib.topoep_plan_ex(*self._args(global_load, local_topk, stream), _launch_ptr(self.launch))
+    def plan(self, global_load, local_topk, stream=None, launch=None):
+        """Enqueue topoep_plan_ex; returns (replica_slots, token_dest, send_counts, status).
+        ``launch`` overrides the planner's launch for this call; it must keep
+        the same shape (only spin_limit and iter_limit may differ)."""
+        if launch is not None and plan_shape(self.topo, self.T, self.k, self.N, launch).as_dict() != \
+                self.shape.as_dict():
+            raise ValueError("a per-call launch must keep the planner's shape")
+        rc = _lib.topoep_plan_ex(*self._args(global_load, local_topk, stream),
+                                 _launch_ptr(self.launch if launch is None else launch))
         if rc != OK:
             raise TopoepError("topoep_plan", rc)
         return self.replica_slots, self.token_dest, self.send_counts, self.status

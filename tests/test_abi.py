@@ -38,7 +38,8 @@ def test_library_exports_every_declared_symbol(tp):
 def test_struct_layout_matches_header(tp):
     assert ctypes.sizeof(tp.Topology) == 6 * 4 + 2 * 8
     assert tp.Topology.tok_bytes.offset == 24
-    assert ctypes.sizeof(tp.Launch) == 20
+    assert ctypes.sizeof(tp.Launch) == 7 * 4
+    assert tp.Launch.spin_limit.offset == 20 and tp.Launch.iter_limit.offset == 24
     assert ctypes.sizeof(tp.Shape) == 13 * 4
 
 
@@ -93,6 +94,12 @@ def test_plan_rejects_null_and_small_workspace_without_launching(tp):
         tp.workspace_bytes(t, 16, 2, 1, launch=(3, 256, 0, 256))
     with pytest.raises(tp.TopoepError):
         tp.workspace_bytes(t, 16, 2, 1, launch=(4, 96, 0, 256))
+    # wait and refinement bounds: -1 (give up at once) is the only negative spin limit
+    assert tp.workspace_bytes(t, 16, 2, 1, launch=(0, 0, 0, 0, 0, -1, 5)) == ws
+    with pytest.raises(tp.TopoepError):
+        tp.workspace_bytes(t, 16, 2, 1, launch=(0, 0, 0, 0, 0, -2, 0))
+    with pytest.raises(tp.TopoepError):
+        tp.workspace_bytes(t, 16, 2, 1, launch=(0, 0, 0, 0, 0, 0, -1))
 
 
 def test_plan_shape_choices(tp):
@@ -130,11 +137,17 @@ def test_plan_shape_choices(tp):
 
 
 def _no_gpu():
+    """True only when this host certainly has no GPU: no /dev/kfd (the ROCm
+    kernel driver's node) and torch reports none.  Any doubt, an exception
+    included, counts as a GPU, so the placeholder-pointer launches below are
+    skipped rather than run where a kernel could start."""
+    if os.path.exists("/dev/kfd"):
+        return False
     try:
         import torch
         return not torch.cuda.is_available()
     except Exception:
-        return True
+        return False
 
 
 @pytest.mark.skipif(not _no_gpu(), reason="launches on placeholder pointers: only where no GPU is present")

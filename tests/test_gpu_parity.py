@@ -530,14 +530,17 @@ def test_single_stages_repeat():
 
 def test_one_launch_stage_and_control_words():
     """With one kernel, stage 0 is the whole plan; stages 1 and 2 are
-    rejected; after every plan the hand-over words of the one-launch plan are
-    zero again, so a plan on a reused workspace needs no clearing."""
+    rejected.  Between plans the one-launch plan's hand-over words hold its
+    generation: word 10 advances by one per plan and the 64-bit arrival
+    count (words 8..9) is that generation times the chunk count, so a plan
+    on a reused workspace needs no clearing."""
     cfg = workload.get("dsv3")
     gl, tk = workload.make_layer(cfg, 5, 0, 0)
     ref = ref_plan(*cfg_args(cfg, 0, gl, tk))
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
     p = topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=DEV, launch=SOLVERS["fused"])
     assert p.shape.kernels == 1 and p.shape.solver == topoep.SOLVER_FUSED
+    nb = p.shape.chunk_blocks
     gl_d = torch.from_numpy(gl).to(DEV)
     tk_d = torch.from_numpy(tk).to(DEV)
     for i in range(4):
@@ -548,16 +551,102 @@ def test_one_launch_stage_and_control_words():
             p.plan(gl_d, tk_d)
         torch.cuda.synchronize()
         assert np.array_equal(p.token_dest.cpu().numpy(), ref["token_dest"]), i
-        # the arrival counter (control word 8) and the ready flags (the
-        # last workspace region of the one-launch plan) are zero again
-        nb = p.shape.chunk_blocks
-        tail = -(-nb * 128 // 256) * 256
-        ws = p.workspace_view().cpu().numpy()
-        assert ws[:256].view(np.uint32)[8] == 0
-        assert not ws[len(ws) - tail:].any()
+        ctrl = p.workspace_view()[:256].cpu().numpy()
+        gen = int(ctrl.view(np.uint32)[10])
+        arrivals = int(ctrl[32:40].view(np.uint64)[0])
+        assert gen == i + 1 and arrivals == gen * nb, (i, gen, arrivals)
     for stage in (1, 2):
         with pytest.raises(topoep.TopoepError):
             p.stage(stage, gl_d, tk_d)
+
+
+def _planner_for(cfg, solver, N=None):
+    topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
+    return topoep.Planner(topo, cfg.T, cfg.k, cfg.N if N is None else N, device=DEV, launch=SOLVERS[solver])
+
+
+def _got(p):
+    torch.cuda.synchronize()
+    return dict(replica_slots=p.replica_slots.cpu().numpy(), token_dest=p.token_dest.cpu().numpy(),
+                send_counts=p.send_counts.cpu().numpy(), status=int(p.status[0].item()),
+                move_count=int(p.status[1].item()))
+
+
+@pytest.mark.parametrize("solver", ["fused", "perdomain"])
+def test_wait_that_gives_up_leaves_nothing_behind(solver):
+    """Every bounded wait of the plan is made to give up from the host
+    (spin_limit -1: no poll at all; every kernel still runs to its end):
+    the plan reports SYNC.  The next plans on the same workspace, without
+    clearing it, equal the oracle, also when their inputs differ from the
+    plan that gave up and when one of them must be redone (row self of Omega
+    differing from the histogram)."""
+    cfg = workload.get("qwen3" if solver == "fused" else "stress")
+    layers = [workload.make_layer(cfg, l, 0, 0) for l in (0, 1)]
+    p = _planner_for(cfg, solver)
+    give_up = tuple(SOLVERS[solver]) + (-1, 0)
+    dev = [(torch.from_numpy(g).to(DEV), torch.from_numpy(t).to(DEV)) for g, t in layers]
+    refs = [ref_plan(*cfg_args(cfg, 0, g, t)) for g, t in layers]
+    # a row self that differs from the histogram: the one-launch plan redoes it
+    g_diff = layers[1][0].copy()
+    g_diff[0] = np.roll(g_diff[0], 3)
+    ref_diff = ref_plan(*cfg_args(cfg, 0, g_diff, layers[1][1]))
+    g_diff_d = torch.from_numpy(g_diff).to(DEV)
+    for rnd in range(3):
+        say("give up", solver, "round", rnd)
+        p.plan(*dev[0])
+        assert_same(_got(p), refs[0], "%s before, round %d" % (solver, rnd))
+        p.token_dest.fill_(-9)
+        p.plan(*dev[1], launch=give_up)
+        got = _got(p)
+        assert got["status"] & topoep.ST_SYNC, got["status"]
+        assert (got["token_dest"] == -1).all()
+        p.plan(*dev[1])
+        assert_same(_got(p), refs[1], "%s after, round %d" % (solver, rnd))
+        p.plan(g_diff_d, dev[1][1], launch=give_up)
+        assert _got(p)["status"] & topoep.ST_SYNC
+        p.plan(g_diff_d, dev[1][1])
+        assert_same(_got(p), ref_diff, "%s redo after, round %d" % (solver, rnd))
+
+
+def test_single_stages_repeat_per_domain_solver():
+    """The per-domain solver restores its own control words: its stage
+    repeated alone, many times after one full plan, reproduces every output
+    and the status words (moves, no RANGE) each time."""
+    cfg = workload.get("stress")
+    gl, tk = workload.make_layer(cfg, 0, 0, 0)
+    ref = ref_plan(*cfg_args(cfg, 0, gl, tk, N=8))
+    p = _planner_for(cfg, "perdomain", N=8)
+    assert p.shape.kernels == 3 and p.shape.solver == topoep.SOLVER_PER_DOMAIN
+    gl_d = torch.from_numpy(gl).to(DEV)
+    tk_d = torch.from_numpy(tk).to(DEV)
+    p.plan(gl_d, tk_d)
+    assert_same(_got(p), ref, "per-domain full plan")
+    assert ref["move_count"] > 0
+    for rep in range(70):
+        p.token_dest.fill_(-9)
+        p.replica_slots.fill_(-9)
+        p.status.fill_(-9)
+        p.stage(1, gl_d, tk_d)
+        p.stage(2, gl_d, tk_d)
+        if rep % 10 == 9:
+            assert_same(_got(p), ref, "per-domain stage repeat %d" % rep)
+
+
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("limit", [1, 2, 5])
+def test_refinement_iteration_bound(solver, limit):
+    """A domain that still has a move after iter_limit committed moves stops
+    with ITER; the oracle applies the same bound, so the plans are equal."""
+    cfg = workload.get("mixtral")
+    gl, tk = workload.make_layer(cfg, 3, 0, 0)
+    args = cfg_args(cfg, 0, gl, tk, N=3)
+    full = ref_plan(*args)
+    assert full["move_count"] > limit
+    topo = oracle.topology(*args[:8])
+    ref = oracle.plan_ref(topo, gl, tk, 3, iter_limit=limit)
+    assert ref["status"] & oracle.ST_ITER and ref["move_count"] == limit
+    got = gpu_plan(*args, launch=tuple(SOLVERS[solver]) + (0, limit))
+    assert_same(got, ref, "iter limit %d %s" % (limit, solver))
 
 
 @pytest.mark.parametrize("solver", sorted(SOLVERS))

@@ -49,18 +49,31 @@ def kernel_metadata(lib_path, tmp):
     return out
 
 
-@pytest.fixture(scope="module")
-def kernels(tmp_path_factory):
+def _library_kernels(tmp_path_factory, path):
     if not all(os.path.exists(t) for t in TOOLS):
         pytest.skip("ROCm LLVM tools not installed")
-    from paper_2609_35481_amd import topoep
-    if not os.path.exists(topoep.LIB_PATH):
-        pytest.skip("libtopoep.so is not built")
+    if not os.path.exists(path):
+        pytest.skip("%s is not built" % os.path.basename(path))
     tmp = str(tmp_path_factory.mktemp("codeobj"))
     try:
-        return kernel_metadata(topoep.LIB_PATH, tmp)
+        return kernel_metadata(path, tmp)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
+
+
+@pytest.fixture(scope="module")
+def kernels(tmp_path_factory):
+    from paper_2609_35481_amd import topoep
+    return _library_kernels(tmp_path_factory, topoep.LIB_PATH)
+
+
+@pytest.fixture(scope="module")
+def stamp_kernels(tmp_path_factory):
+    """The instrumented build used for phase timings: its kernels must keep
+    the product's register budget, or the stamps would time a different
+    kernel."""
+    from paper_2609_35481_amd import build
+    return _library_kernels(tmp_path_factory, build.STAMPS_LIB)
 
 
 def test_every_kernel_is_in_the_library(kernels):
@@ -81,3 +94,11 @@ def test_no_kernel_spills_to_scratch(kernels):
         else:
             assert priv == 0, (name, priv)
         assert vgpr <= 512, (name, vgpr)
+
+
+def test_stamped_build_spills_nothing_either(stamp_kernels):
+    for name, priv, vgpr in stamp_kernels:
+        if "12solve_kernel" in name:
+            assert priv <= 64, (name, priv)
+        else:
+            assert priv == 0, (name, priv)
