@@ -347,6 +347,31 @@ int topoep_plan_costs(const topoep_topology *topo, const topoep_costs *costs, co
                       int32_t *replica_slots, int32_t *token_dest, int32_t *send_counts, int32_t *status,
                       void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * topoep_plan for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * It takes no workspace: the plan runs in a device array of
+ * TOPOEP_NOALLOC_SCRATCH_BYTES held by the library, one per GPU it runs
+ * on, until the process ends.  Each call first clears what the plan needs
+ * zero there with a small kernel on `stream` (no hipMemset, no allocation,
+ * no host synchronisation), then enqueues the plan of topoep_plan with the
+ * default launch shape; successive calls may use different shapes.
+ *
+ * All calls on one GPU share that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (two streams, or two threads
+ * without ordering) race and give wrong outputs; order them on one stream.
+ *
+ * Arguments, outputs and status bits as topoep_plan.  TOPOEP_EWORKSPACE:
+ * the plan needs more than TOPOEP_NOALLOC_SCRATCH_BYTES of workspace
+ * (topoep_workspace_bytes; every workload size up to that runs).
+ * TOPOEP_EHIP: the array's device address could not be obtained, or a
+ * launch failed.  Other return codes as topoep_plan.
+ */
+#define TOPOEP_NOALLOC_SCRATCH_BYTES (4u << 20)
+int topoep_plan_noalloc(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
+                        int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots, int32_t *token_dest,
+                        int32_t *send_counts, int32_t *status, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -3176,9 +3176,79 @@ int enqueue(int stage_mask, const topoep_topology *topo, const int32_t *global_l
   return hipGetLastError() == hipSuccess ? TOPOEP_OK : TOPOEP_EHIP;
 }
 
+// ---------------------------------------------------------------- no-allocation entry point
+//
+// topoep_plan_noalloc plans into `scratch`, a device array of fixed size in
+// place of a caller's workspace: one copy per GPU the library runs on, held
+// until the process ends.  In host code the array's name is only a
+// host-side stand-in; kernels and the clearing launch get the device
+// address hipGetSymbolAddress returns for the current device, looked up
+// once per device and kept.
+
+constexpr size_t kScratchBytes = TOPOEP_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+int scratch_address(void **out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return TOPOEP_EHIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+      (void)hipGetLastError();
+      return TOPOEP_EHIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return TOPOEP_OK;
+}
+
+// Zero n words (the workspace prefix a first plan needs zero): a kernel, so
+// that the clearing can be captured in a HIP graph like the plan itself.
+__global__ __launch_bounds__(256) void zero_words(uint32_t *w, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    w[i] = 0u;
+}
+
 }  // namespace
 
 extern "C" {
+
+int topoep_plan_noalloc(const topoep_topology *topo, const int32_t *global_load, const int32_t *local_topk,
+                        int32_t T, int32_t k, int32_t replica_budget, int32_t *replica_slots, int32_t *token_dest,
+                        int32_t *send_counts, int32_t *status, void *stream) {
+  Plan p;
+  Shape s;
+  size_t need = 0;
+  int rc = setup(topo, T, k, replica_budget, nullptr, &p, &s, &need, nullptr);
+  if (rc != TOPOEP_OK) return rc;
+  // the argument checks of topoep_plan, before anything is enqueued
+  if (!global_load || !send_counts || !status) return TOPOEP_EINVAL;
+  if ((int64_t)topo->num_ranks * replica_budget > 0 && !replica_slots) return TOPOEP_EINVAL;
+  if (T > 0 && (!local_topk || !token_dest)) return TOPOEP_EINVAL;
+  if (need > kScratchBytes) return TOPOEP_EWORKSPACE;
+  void *ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc != TOPOEP_OK) return rc;
+  // the previous call may have been another shape: clear what this plan
+  // needs zero (control words, flags, histogram buffers)
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  const int64_t words = (int64_t)(s.zero_bytes / 4);
+  hipLaunchKernelGGL(zero_words, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, st, static_cast<uint32_t *>(ws),
+                     words);
+  if (hipGetLastError() != hipSuccess) return TOPOEP_EHIP;
+  return enqueue(7, topo, global_load, local_topk, T, k, replica_budget, replica_slots, token_dest, send_counts,
+                 status, ws, kScratchBytes, stream, nullptr);
+}
 
 int topoep_workspace_bytes_ex(const topoep_topology *topo, int32_t T, int32_t k, int32_t replica_budget,
                               const topoep_launch *launch, size_t *bytes_out) {

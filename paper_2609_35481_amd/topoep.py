@@ -133,11 +133,15 @@ _lib.topoep_plan_costs.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(Cost
 _lib.topoep_gather_replicas.restype = ctypes.c_int
 _lib.topoep_gather_replicas.argtypes = [ctypes.POINTER(Topology), _i32, _vp, _vp, _vp, ctypes.c_int64, _vp, _vp]
 
+_lib.topoep_plan_noalloc.restype = ctypes.c_int
+_lib.topoep_plan_noalloc.argtypes = [ctypes.POINTER(Topology), _vp, _vp, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]
+NOALLOC_SCRATCH_BYTES = 4 << 20
+
 EXPORTS = ("topoep_workspace_bytes", "topoep_workspace_bytes_ex", "topoep_plan",
            "topoep_plan_ex", "topoep_plan_stage", "topoep_plan_shape",
            "topoep_layout_workspace_bytes", "topoep_dispatch_layout",
            "topoep_dispatch_workspace_bytes", "topoep_plan_dispatch", "topoep_gather_replicas",
-           "topoep_costs_workspace_bytes", "topoep_plan_costs")
+           "topoep_costs_workspace_bytes", "topoep_plan_costs", "topoep_plan_noalloc")
 
 
 def topology(R, G, E, self_rank, c_intra, c_inter, S, W) -> Topology:
@@ -406,6 +410,30 @@ class LayoutPlanner:
         if rc != OK:
             raise TopoepError("topoep_dispatch_layout", rc)
         return self.send_offsets, self.token_slot
+
+
+def plan_noalloc(topo: Topology, global_load, local_topk, replica_budget: int, replica_slots, token_dest,
+                 send_counts, status, stream=None):
+    """Enqueue topoep_plan_noalloc into caller-given outputs (nothing is
+    allocated, here or in the library); raises TopoepError on a nonzero
+    return code."""
+    R, E = topo.num_ranks, topo.num_experts
+    _dev_i32(global_load, "global_load", (R, E))
+    T, k = (local_topk.shape[0], local_topk.shape[1]) if local_topk is not None else (0, 1)
+    if T > 0:
+        _dev_i32(local_topk, "local_topk", (T, k))
+        _dev_i32(token_dest, "token_dest", (T, k))
+    _dev_i32(send_counts, "send_counts", (R,))
+    _dev_i32(status, "status", (2,))
+    if replica_slots.numel():
+        _dev_i32(replica_slots, "replica_slots", (R, replica_budget))
+    rc = _lib.topoep_plan_noalloc(
+        ctypes.byref(topo), global_load.data_ptr(), local_topk.data_ptr() if T > 0 else None, T, k,
+        int(replica_budget), replica_slots.data_ptr() if replica_slots.numel() else None,
+        token_dest.data_ptr() if T > 0 else None, send_counts.data_ptr(), status.data_ptr(),
+        _stream_ptr(stream, global_load.device))
+    if rc != OK:
+        raise TopoepError("topoep_plan_noalloc", rc)
 
 
 def gather_replicas(topo: Topology, replica_slots, expert_params, slot_params, prev_slots=None, stream=None):

@@ -25,7 +25,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert "topoep_plan" in names and "topoep_workspace_bytes" in names
-    assert len(names) == 13
+    assert len(names) == 14
 
 
 def test_library_exports_every_declared_symbol(tp):
@@ -253,3 +253,22 @@ def test_valid_costs_call_reaches_the_launch(tp):
                                      2560, 8192 * 2, ws, None) == tp.EHIP
     assert tp._lib.topoep_plan_costs(ctypes.byref(t), ctypes.byref(c), None, 256, 16, 2, 1, 512, 1024, 2048,
                                      2560, 8192 * 2, ws, None) == tp.EINVAL
+
+
+def test_noalloc_host_checks(tp):
+    """topoep_plan_noalloc refuses bad arguments and shapes beyond its array
+    before any device call (placeholder pointers are never launched on)."""
+    t = base(tp)
+    P = tp._lib.topoep_plan_noalloc
+    assert P(None, 256, 256, 16, 2, 1, 512, 1024, 2048, 4096, None) == tp.EINVAL
+    assert P(ctypes.byref(t), None, 256, 16, 2, 1, 512, 1024, 2048, 4096, None) == tp.EINVAL
+    assert P(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, None, 4096, None) == tp.EINVAL
+    big = tp.topology(32, 8, 256, 0, 1, 8, 14336, 88080384)
+    assert tp.workspace_bytes(big, 1 << 20, 8, 2) > tp.NOALLOC_SCRATCH_BYTES
+    assert P(ctypes.byref(big), 256, 256, 1 << 20, 8, 2, 512, 1024, 2048, 4096, None) == tp.EWORKSPACE
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="only where no GPU is present")
+def test_noalloc_without_a_device_is_a_hip_error(tp):
+    t = base(tp)
+    assert tp._lib.topoep_plan_noalloc(ctypes.byref(t), 256, 256, 16, 2, 1, 512, 1024, 2048, 4096, None) == tp.EHIP
