@@ -202,3 +202,20 @@ def make_layer(cfg: Config, layer: int = 0, mb: int = 0, self_rank: int = 0):
 def all_rank_topk(cfg: Config, layer: int = 0, mb: int = 0) -> np.ndarray:
     """Top-k arrays of every simulated rank, [R, T, k] int32 (read-only)."""
     return _layer_all_ranks(cfg, layer, mb)
+
+
+def _make_layer_job(args):
+    cfg, layer, mb, self_rank = args
+    return make_layer(cfg, layer, mb, self_rank)
+
+
+def make_layers(cfg: Config, keys, self_rank: int = 0, workers: int = 8):
+    """make_layer for every (layer, microbatch) of keys, in a pool of fresh
+    interpreter processes (spawned, so a caller that holds a GPU does not
+    hand it to them); returns the inputs in the order of keys."""
+    jobs = [(cfg, layer, mb, self_rank) for layer, mb in keys]
+    if workers <= 1 or len(jobs) <= 1:
+        return [_make_layer_job(j) for j in jobs]
+    import multiprocessing as mp
+    with mp.get_context("spawn").Pool(min(workers, len(jobs))) as pool:
+        return pool.map(_make_layer_job, jobs)
