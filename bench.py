@@ -70,19 +70,29 @@ STAGE_NAMES = {1: ("plan",), 3: ("hist", "solve", "reroute")}
 
 
 def algorithmic_bytes(cfg, N, kernels):
-    """Bytes the method must move per layer, by kernel: the ids once per
-    kernel that reads them, Omega, the destinations and the small outputs
-    (slots, send counts, two status words)."""
+    """Bytes the method must move per layer (the plan's algorithmic traffic),
+    by kernel: 4 per assignment to count the ids, 8 per assignment to read
+    them again and write the destinations, Omega (4 R E) and the outputs
+    (4 R (N + 1): replica slots and send counts); in all 12 B per assignment
+    + 4 R E + 4 R (N + 1).  One launch does all of it.  The kernels' own
+    count (``kernel_bytes``) differs: the one-launch kernel keeps the ids in
+    registers and reads them once, and every plan writes two status words."""
+    a = cfg.T * cfg.k
+    omega = 4 * cfg.R * cfg.E
+    outs = 4 * cfg.R * (N + 1)
+    if kernels == 1:
+        return {"plan": 12 * a + omega + outs}
+    return {"hist": 4 * a, "solve": omega + outs, "reroute": 8 * a}
+
+
+def kernel_bytes(cfg, N, kernels):
+    """Bytes each kernel itself must read and write (its own count)."""
     a = cfg.T * cfg.k
     omega = 4 * cfg.R * cfg.E
     outs = 4 * cfg.R * (N + 1) + 8
     if kernels == 1:
-        return {"plan": 4 * a + omega + 4 * a + outs}   # ids read once, held in registers
-    return {
-        "hist": 4 * a,              # read the ids
-        "solve": omega + outs,      # read Omega, write slots, counts, status
-        "reroute": 8 * a,           # read the ids again, write destinations
-    }
+        return {"plan": 8 * a + omega + outs}
+    return {"hist": 4 * a, "solve": omega + outs, "reroute": 8 * a}
 
 
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_35481_amd", "csrc", n) for n in ("topoep.hip", "wave.h")]
@@ -161,15 +171,22 @@ def run_pmc_pass(args):
                       "copy_bytes": src.numel() * 4, "kernel_source_sha1": source_digest()}), flush=True)
 
 
-def _cpu_model():
+def _host_cpu():
+    """nproc and the lscpu model name of this host (None where unavailable)."""
+    import subprocess
+    out = {"nproc": None, "lscpu_model_name": None}
     try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
-    except OSError:
+        out["nproc"] = int(subprocess.run(["nproc"], capture_output=True, text=True, timeout=10).stdout.strip())
+    except Exception:
+        out["nproc"] = os.cpu_count()
+    try:
+        for line in subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout.splitlines():
+            if line.startswith("Model name:"):
+                out["lscpu_model_name"] = line.split(":", 1)[1].strip()
+                break
+    except Exception:
         pass
-    return None
+    return out
 
 
 def cpu_baseline(cfg, inputs, budget_s=15.0, dev_inputs=None):
@@ -197,7 +214,7 @@ def cpu_baseline(cfg, inputs, budget_s=15.0, dev_inputs=None):
     out = {"value": n * cfg.T * cfg.k / dt, "unit": "assignments/s", "cores": 1, "kind": "oracle",
            "sample": "%d layer plans (the %d layers of the %s workload, cycled, back to back, one "
                      "thread): %.0f us per layer, %.1f s" % (n, len(inputs), cfg.name, per_layer * 1e6, dt),
-           "cpu_model": _cpu_model()}
+           **_host_cpu()}
     # (ii) every core: about budget/2 seconds of work
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
     cores = max(1, min(cores, 64))
@@ -342,23 +359,16 @@ def run_phases(args):
     return out
 
 
-def run_bench(args):
-    import torch
-    from paper_2609_35481_amd import topoep
-
-    cfg = workload.get(args.config)
-    N = cfg.N
-    layers = cfg.layers if args.layers <= 0 else args.layers
+def measure(torch, topoep, cfg, N, inputs, steps, warmup, stage_reps, launch=None):
+    """Time every layer's plan of one microbatch as one HIP graph (inputs
+    resident in HBM), then each kernel of the plan alone and the launch
+    floor.  Returns the measurement and the planners (each holding a full
+    plan of its layer)."""
+    layers = len(inputs)
     dev = torch.device("cuda:0")
-    t_gen = time.perf_counter()
-    inputs = make_inputs(cfg, layers)
-    t_gen = time.perf_counter() - t_gen
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
-    dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev))
-                  for gl, tk in inputs]
-    launch = launch_from_args(args)
+    dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev)) for gl, tk in inputs]
     planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev, launch=launch) for _ in range(layers)]
-
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(stream):
@@ -376,12 +386,10 @@ def run_bench(args):
             for p, (g, t) in zip(planners, dev_inputs):
                 p.plan(g, t)
     torch.cuda.synchronize()
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         graph.replay()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for a, b in ev:
@@ -391,16 +399,13 @@ def run_bench(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     step_ms = np.array([a.elapsed_time(b) for a, b in ev]) / copies
-    ms_per_step = wall / (args.steps * copies) * 1e3
-    assign = layers * cfg.T * cfg.k
-    value = assign / (ms_per_step / 1e3)
-
+    ms_per_step = wall / (steps * copies) * 1e3
+    value = layers * cfg.T * cfg.k / (ms_per_step / 1e3)
     # every plan of the last replay must be a valid plan (status 0)
     st = torch.stack([p.status for p in planners]).cpu().numpy()
     if (st[:, 0] & ~topoep.ST_SELF_DIFF).any():
-        raise SystemExit("plan status bits set: %s" % np.unique(st[:, 0]))
+        raise SystemExit("%s: plan status bits set: %s" % (cfg.name, np.unique(st[:, 0])))
     moves = st[:, 1].astype(np.int64)
-
     # per-kernel durations (a graph of back-to-back launches of one kernel,
     # HIP events on its stream), and the launch floor (empty kernels, same
     # shapes, same graph structure)
@@ -408,50 +413,117 @@ def run_bench(args):
     kernels = shape.kernels
     stages = {}
     for sid, name in enumerate(STAGE_NAMES[kernels]):
-        stages[name] = time_stage(torch, planners, dev_inputs, sid, max(args.stage_reps, copies))
-    floor_us = time_stage(torch, planners, dev_inputs, topoep.STAGE_FLOOR, max(args.stage_reps, copies))
-    # restore complete plans in every workspace
+        stages[name] = time_stage(torch, planners, dev_inputs, sid, max(stage_reps, copies))
+    floor_us = time_stage(torch, planners, dev_inputs, topoep.STAGE_FLOOR, max(stage_reps, copies))
     for p, (g, t) in zip(planners, dev_inputs):
         p.plan(g, t)
     torch.cuda.synchronize()
-
     nbytes = algorithmic_bytes(cfg, N, kernels)
+    own = kernel_bytes(cfg, N, kernels)
     dom = max(stages, key=lambda k: stages[k])
     avg_us = stages[dom]
     achieved = nbytes[dom] / (avg_us * 1e-6) / 1e9
     roof = {"bound": "hbm", "kernel": dom + "_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-            "traffic": measured_traffic(cfg.name, dom),
-            "algorithmic_bytes_per_launch": nbytes[dom], "avg_kernel_us": avg_us}
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name, dom),
+            "algorithmic_bytes_per_launch": nbytes[dom], "kernel_own_bytes_per_launch": own[dom],
+            "frac_kernel_own_bytes": own[dom] / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, "avg_kernel_us": avg_us,
+            "floor_ratio": avg_us / (floor_us / kernels) if floor_us > 0 else None}
+    per_layer = ms_per_step * 1e3 / layers
+    layer_bytes = sum(nbytes.values())
+    res = {
+        "workload": DESCR.get(cfg.name, cfg.name), "layers": layers, "replica_slots": N,
+        "passes_per_replay": copies, "plan_shape": shape.as_dict(), "ms_per_step": ms_per_step,
+        "assignments_per_s": value, "plan_latency_us_per_layer": per_layer,
+        "plan_latency_us_per_layer_p10_p50_p90": [float(np.percentile(step_ms, q)) * 1e3 / layers
+                                                  for q in (10, 50, 90)],
+        "kernel_avg_us": {k: round(v, 3) for k, v in stages.items()},
+        "launch_floor_us_per_layer": round(floor_us, 3),
+        "floor_ratio": per_layer / floor_us if floor_us > 0 else None,
+        "refinement_moves_per_layer": {"mean": float(moves.mean()), "max": int(moves.max()),
+                                       "layers_with_moves": int((moves > 0).sum())},
+        "algorithmic_bytes_per_layer": layer_bytes,
+        "hbm_frac_per_layer": layer_bytes / (per_layer * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "roofline": roof,
+    }
+    return res, planners, dev_inputs, topo
 
+
+# extra workloads of the all-configs object: name, configuration, replica
+# slots (the refinement-heavy cases: DeepSeek-V3-like with 4 slots, where
+# stage 1 leaves slots free, and Mixtral-like, which refines every layer)
+ALL_CONFIGS = [("tiny", "tiny", None), ("mixtral", "mixtral", None), ("qwen3", "qwen3", None),
+               ("dsv3", "dsv3", None), ("stress", "stress", None), ("dsv3_N4", "dsv3", 4)]
+
+
+def all_configs(torch, topoep, args, headline=None):
+    """Every configuration (first microbatch, all its layers) and the
+    refinement-heavy DeepSeek-V3-like case with 4 slots, fewer steps each."""
+    out = {}
+    for key, name, N in ALL_CONFIGS:
+        cfg = workload.get(name)
+        n_slots = cfg.N if N is None else N
+        if headline is not None and key == args.config:
+            res = headline
+        else:
+            t = time.perf_counter()
+            inputs = workload.make_layers(cfg, [(l, 0) for l in range(cfg.layers)],
+                                          workers=min(16, os.cpu_count() or 1))
+            gen_s = time.perf_counter() - t
+            res, _, _, _ = measure(torch, topoep, cfg, n_slots, inputs, args.all_steps, max(3, args.warmup // 4),
+                                   args.stage_reps)
+            res["input_generation_s"] = round(gen_s, 2)
+        out[key] = {k: res[k] for k in ("workload", "layers", "replica_slots", "plan_shape",
+                                        "plan_latency_us_per_layer", "plan_latency_us_per_layer_p10_p50_p90",
+                                        "assignments_per_s", "kernel_avg_us", "launch_floor_us_per_layer",
+                                        "floor_ratio", "refinement_moves_per_layer", "algorithmic_bytes_per_layer",
+                                        "hbm_frac_per_layer", "roofline")}
+        print("all_configs %s: %.2f us per layer" % (key, res["plan_latency_us_per_layer"]), file=sys.stderr,
+              flush=True)
+        torch.cuda.empty_cache()
+    return out
+
+
+def run_bench(args):
+    import torch
+    from paper_2609_35481_amd import topoep
+
+    cfg = workload.get(args.config)
+    N = cfg.N
+    layers = cfg.layers if args.layers <= 0 else args.layers
+    t_gen = time.perf_counter()
+    inputs = make_inputs(cfg, layers)
+    t_gen = time.perf_counter() - t_gen
+    launch = launch_from_args(args)
+    res, planners, dev_inputs, topo = measure(torch, topoep, cfg, N, inputs, args.steps, args.warmup,
+                                              args.stage_reps, launch)
+    res["input_generation_s"] = round(t_gen, 2)
     out = {
         "metric": METRIC,
-        "value": value,
+        "value": res["assignments_per_s"],
         "unit": "assignments/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
         "launch": launch,
-        "passes_per_replay": copies,
-        "plan_shape": shape.as_dict(),
+        "passes_per_replay": res["passes_per_replay"],
+        "plan_shape": res["plan_shape"],
         "config": {"workload": DESCR[cfg.name], "layers_per_step": layers, "tokens_per_rank": cfg.T,
                    "top_k": cfg.k, "ranks": cfg.R, "experts": cfg.E, "replica_slots": N,
                    "assignments_per_layer": cfg.T * cfg.k},
-        "plan_latency_us_per_layer": ms_per_step * 1e3 / layers,
-        "plan_latency_us_per_layer_p10_p50_p90": [float(np.percentile(step_ms, q)) * 1e3 / layers
-                                                  for q in (10, 50, 90)],
-        "kernel_avg_us": {k: round(v, 3) for k, v in stages.items()},
-        "launch_floor_us_per_layer": round(floor_us, 3),
-        "refinement_moves_per_layer": {"mean": float(moves.mean()), "max": int(moves.max()),
-                                       "layers_with_moves": int((moves > 0).sum())},
-        "roofline": roof,
-        "input_generation_s": round(t_gen, 2),
+        "plan_latency_us_per_layer": res["plan_latency_us_per_layer"],
+        "plan_latency_us_per_layer_p10_p50_p90": res["plan_latency_us_per_layer_p10_p50_p90"],
+        "kernel_avg_us": res["kernel_avg_us"],
+        "launch_floor_us_per_layer": res["launch_floor_us_per_layer"],
+        "floor_ratio": res["floor_ratio"],
+        "refinement_moves_per_layer": res["refinement_moves_per_layer"],
+        "roofline": res["roofline"],
+        "input_generation_s": res["input_generation_s"],
     }
     if not args.no_dispatch:
         out["dispatch"] = bench_dispatch(torch, topoep, cfg, topo, planners, dev_inputs, args)
@@ -459,6 +531,8 @@ def run_bench(args):
         out["replica_gather"] = bench_gather(torch, topoep, cfg, topo, planners)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, inputs, args.cpu_seconds, dev_inputs)
+    if not args.no_all_configs and args.layers <= 0 and launch is None:
+        out["all_configs"] = all_configs(torch, topoep, args, headline=res)
     return out
 
 
@@ -650,6 +724,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-dispatch", action="store_true", help="skip the dispatch-side measurement")
     ap.add_argument("--no-gather", action="store_true", help="skip the replica-slot gather measurement")
+    ap.add_argument("--no-all-configs", action="store_true", help="skip the all-configurations object")
+    ap.add_argument("--all-steps", type=int, default=50, help="timed steps per configuration of all_configs")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-min-log2", type=int, default=16)
     ap.add_argument("--sweep-max-log2", type=int, default=28)
