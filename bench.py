@@ -309,7 +309,8 @@ PHASE_SLOTS = [(0, "solver start"), (1, "Omega in LDS"), (23, "plan start"), (22
                (2, "stage 1"), (3, "setup"), (4, "routing"), (5, "refinement"), (6, "outputs"),
                (7, "instance list"), (8, "speculative plan"), (9, "verdict seen"), (10, "outputs drained"),
                (12, "chunk 0 arrived"), (19, "last arrival start"), (13, "last arrival done"),
-               (16, "chunk 0 offsets"), (14, "chunk 0 sees flag"), (15, "chunk 0 done")]
+               (16, "chunk 0 offsets"), (14, "chunk 0 sees flag"), (15, "chunk 0 done"),
+               (24, "s1: candidates"), (26, "s1: ranks"), (27, "ff: lists and hosting"), (28, "ff: counts"), (30, "ff: entries")]
 
 
 def run_phases(args):

@@ -234,7 +234,7 @@ struct SingleLds {
 __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   SingleLds l;
   int o = 0;
-  l.ck = o;    o += 2 * p.M * p.E;            // uint64 stage-1 candidate keys per domain
+  l.ck = o;    o += 2 * p.M * ((p.E + 15) & ~15);   // uint64 stage-1 candidate keys per domain (stride E rounded to 16)
   l.em = o;    o += 2 * p.M * p.E;            // uint64 per domain and expert: local ranks hosting it
   l.fdt = o;   o += 2 * (p.M + 1);            // divisors 1..M
   l.hs = o;    o += p.E;                      // histogram of local_topk
@@ -243,7 +243,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
   l.mask = o;  o += p.E * p.MW;               // per expert: hosting domains
   l.bm = o;    o += p.E * p.RW;               // per expert: ranks in this rank's instance list
   l.sendl = o; o += p.R;                      // send counts being summed
-  l.wt = o;    o += 16;                       // per-wave totals of a scan (up to 1024 threads)
+  l.wt = o;    o += imax(32, (p.E + 63) / 64);   // per-wave totals of a scan (and their sum), or per 64 experts
   l.repl = o;  o += p.M * imax(p.cap1, 1);    // stage-1 replicas per domain
   l.slots = o; o += p.R * imax(p.Neff, 1);    // replica slots of every rank
   l.used = o;  o += p.R;
@@ -1210,6 +1210,81 @@ __device__ void stage1_domain_wave(const Plan &p, int d, const int *om, uint64_t
 }
 
 
+// Stage 1 (Eq. 9) of every domain by the whole workgroup.  Item (d, e):
+// D[d][e] summed over the domain's rows of Omega; an expert whose main lies
+// outside d with b = 2 D S - W > 0 is a candidate and takes a slot of
+// ck + d E16 (E16 = E rounded up to 16; the keys were set to ~0, which sorts
+// after every candidate) from the domain's LDS counter ccnt[d] (the slots'
+// order is arbitrary).  Each candidate's rank among its domain's candidates
+// by key (D descending, e ascending; keys are distinct) is then counted in
+// parts of 16 keys: the workgroup's threads are split into one block per
+// domain (whole waves; one domain after another when there are more domains
+// than waves), a block's items being (candidate c, part h) with Hp parts
+// per candidate (ceil(nc / 16) rounded up to a power of two).  rk[d E + c]
+// = the rank of the domain's candidate in slot c.  The ranks below cap1
+// name the domain's stage-1 replicas.  rk: M E words.
+__device__ __forceinline__ void stage1_ranks(const Plan &p, const int *om, uint64_t *ck, int *ccnt, int *rk) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, G = p.G, M = p.M, E16 = (E + 15) & ~15;
+  // item idx = d E + e, walked with (d, e) kept as the index advances
+  const int dstep = (int)fdiv((uint32_t)nt, p.fE), estep = nt - dstep * E;
+  int d = (int)fdiv((uint32_t)tid, p.fE), e = tid - d * E;
+  for (int idx = tid; idx < M * E; idx += nt, d += dstep, e += estep) {
+    if (e >= E) {
+      e -= E;
+      ++d;
+    }
+    rk[idx] = 0;
+    if ((int)fdiv((uint32_t)e, p.fGP) == d) continue;   // main inside the domain
+    const int *col = om + d * G * E + e;
+    int D = 0;
+#pragma unroll 8
+    for (int j = 0; j < G; ++j) D += col[j * E];
+    if ((int64_t)2 * D * p.S > p.W) {
+      const int pos = atomicAdd(&ccnt[d], 1);
+      ck[d * E16 + pos] = cand_key(D, e);
+    }
+  }
+  lds_barrier();
+  STAMP(p, 24);
+  const int nw = nt >> 6;
+  const int wpd = M <= nw ? nw / M : 0;
+  const int d0 = wpd ? (tid >> 6) / wpd : 0;
+  const int tpd = wpd ? wpd * 64 : nt;
+  const int lt = wpd ? tid - d0 * tpd : tid;
+  for (d = d0; d < (wpd ? imin(d0 + 1, M) : M); ++d) {
+    const int nc = uniform_i32(ccnt[d]);   // (d is the same in the whole wave)
+    const int parts = (nc + 15) >> 4;
+    const int lh = parts <= 1 ? 0 : 32 - __clz(parts - 1);
+    const uint64_t *kd = ck + d * E16;
+    for (int v = lt; v < (nc << lh); v += tpd) {
+      const int c = v >> lh, h = v & ((1 << lh) - 1);
+      if (16 * h >= nc) continue;
+      const uint64_t kc = kd[c];
+      const uint64_t *kp = kd + 16 * h;
+      uint64_t k[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) k[i] = kp[i];
+      int below = 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) below += k[i] < kc ? 1 : 0;
+      if (below) atomicAdd(&rk[d * E + c], below);
+    }
+  }
+  lds_barrier();
+  STAMP(p, 26);
+}
+
+// The stage-1 replica lists from the ranks: repl[d cap1 + rank] = e for the
+// ranks below cap1 (repl holds -1 elsewhere).  Ends with a barrier.
+__device__ __forceinline__ void stage1_lists(const Plan &p, const uint64_t *ck, const int *ccnt, const int *rk,
+                                             int *repl) {
+  for (int idx = threadIdx.x; idx < p.M * p.E; idx += blockDim.x) {
+    const int d = (int)fdiv((uint32_t)idx, p.fE), c = idx - d * p.E;
+    if (c < ccnt[d] && rk[idx] < p.cap1) repl[d * p.cap1 + rk[idx]] = (int)(uint32_t)ck[d * ((p.E + 15) & ~15) + c];
+  }
+  lds_barrier();
+}
+
 // This rank's per-expert instance list: bm[e * RW ...] marks the ranks
 // whose instance of e has a nonzero share q[self][e][r].  Thread t takes
 // experts [t * K, (t + 1) * K), K = ceil(E / blockDim): it counts their
@@ -1766,7 +1841,135 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
   for (int i = tid; i < p.R; i += nt) t.sendl[i] = 0;
   for (int i = tid; i < p.M * p.cap1; i += nt) t.repl[i] = -1;
   for (int i = tid; i < p.M * p.E; i += nt) t.em[i] = 0;
+  // candidate keys: ~0 sorts after every candidate (stage1_ranks reads
+  // whole parts of 16)
+  for (int i = tid; i < p.M * ((p.E + 15) & ~15); i += nt) t.ck[i] = ~0ull;
   build_divisors(p.M, t.fdt);
+}
+
+// The rest of the plan when no domain can refine: every domain's replica
+// slots are all taken by stage 1 (or a domain holds one rank).  Every expert
+// then has at most one instance per domain (stage 1 places one replica per
+// domain and expert, never in the main's own domain), a refinement move
+// needs a free slot on its target, so none is committed; and this rank's
+// share of expert e follows from the routing rule of Section 4.3 alone: all
+// of w = omega[self][e] to the instance in dom(self) if there is one, else
+// the even split over the n instances, one per hosting domain in ascending
+// order: the i-th takes floor(w / n) + [i < w mod n].  The instances with a
+// nonzero share are then the first min(n, w), and the i-th of them ends at
+// the cumulative share (i + 1) floor(w / n) + min(i + 1, w mod n).
+// Phases: the stage-1 lists with the hosting domains and instance ranks;
+// per expert its number of entries, scanned within each wave; per (expert,
+// domain) the entry of that domain's instance, the send counts and the
+// replica slots.  rr: M E words (rank of e's instance in domain d); ex:
+// E words (each expert's first entry inside its wave).  Sets misc[15].
+__device__ __forceinline__ void fast_finish(const Plan &p, const SingleState &t, const uint64_t *ck, const int *rk,
+                                            int *rr, int *ex) {
+  const int tid = threadIdx.x, nt = blockDim.x, E = p.E, G = p.G, M = p.M, R = p.R, cap = p.cap1;
+  const int E16 = (E + 15) & ~15, lane = tid & 63, wave = tid >> 6, nw = nt >> 6;
+  const int *om = t.om, *ccnt = t.ccnt;
+  int *repl = t.repl;
+  uint32_t *mask = t.mask;
+  int *sendl = t.sendl, *misc = t.misc, *wt = t.wt;
+  const int ds = (int)fdiv((uint32_t)p.self, p.fG);
+  if (tid == 0) misc[15] = 1;   // (single_recv_counts: the plan came from here; barriers follow)
+  // the stage-1 lists, hosting domains and the rank of each instance
+  for (int e = tid; e < E; e += nt) {
+    const int dm = (int)fdiv((uint32_t)e, p.fGP);
+    atomicOr(&mask[e * p.MW + (dm >> 5)], 1u << (dm & 31));
+    rr[dm * E + e] = (int)fdiv((uint32_t)e, p.fP);
+  }
+  // items idx = d E + c, walked with (d, c) kept as the index advances
+  const int dstep = (int)fdiv((uint32_t)nt, p.fE), estep = nt - dstep * E;
+  const int dfirst = (int)fdiv((uint32_t)tid, p.fE), efirst = tid - dfirst * E;
+  int d = dfirst, c = efirst;
+  for (int idx = tid; idx < M * E; idx += nt, d += dstep, c += estep) {
+    if (c >= E) {
+      c -= E;
+      ++d;
+    }
+    const int rank = rk[idx];
+    if (c >= ccnt[d] || rank >= cap) continue;
+    const int e = (int)(uint32_t)ck[d * E16 + c];
+    repl[d * cap + rank] = e;
+    atomicOr(&mask[e * p.MW + (d >> 5)], 1u << (d & 31));
+    rr[d * E + e] = d * G + (rank - (int)fdiv_hi((uint32_t)rank, p.fG) * G);
+  }
+  lds_barrier();
+  STAMP(p, 27);
+  // per expert: its entries, scanned inside the wave; the waves' totals
+  // (experts e and e + blockDim ... take rounds; wt holds 16 totals a round)
+  const int rounds = (E + nt - 1) / nt;
+  for (int r0 = 0; r0 < rounds; ++r0) {
+    const int e = r0 * nt + tid;
+    int c = 0;
+    if (e < E) {
+      const int w = om[p.self * E + e];
+      const uint32_t *me = mask + e * p.MW;
+      int n = 0;
+      for (int wd = 0; wd < p.MW; ++wd) n += __popc(me[wd]);
+      c = w <= 0 ? 0 : (((me[ds >> 5] >> (ds & 31)) & 1u) ? 1 : imin(n, w));
+    }
+    const int incl = wave_incl_scan(c);
+    if (e < E) ex[e] = incl - c;
+    if (lane == 63 && r0 * nt + wave * 64 < E) wt[r0 * nw + wave] = incl;   // per block of 64 experts
+  }
+  lds_barrier();
+  STAMP(p, 28);
+  // per (expert, domain): the entry of the domain's instance
+  d = dfirst;
+  int e = efirst;
+  for (int idx = tid; idx < M * E; idx += nt, d += dstep, e += estep) {
+    if (e >= E) {
+      e -= E;
+      ++d;
+    }
+    const uint32_t *me = mask + e * p.MW;
+    const int w = om[p.self * E + e];
+    // the expert's first entry: its place in its wave plus the totals of the
+    // waves (and rounds) before it
+    int first = ex[e];
+    for (int b = 0; b < (e >> 6); ++b) first += wt[b];
+    if (d == 0) p.csr_ptr[e] = first;
+    if (w <= 0 || !((me[d >> 5] >> (d & 31)) & 1u)) continue;
+    const bool local = (me[ds >> 5] >> (ds & 31)) & 1u;
+    int i = 0, q = w, end = w;
+    if (local) {
+      if (d != ds) continue;   // all of w to the instance in dom(self)
+    } else {
+      int n = 0;
+      for (int wd = 0; wd < p.MW; ++wd) {
+        n += __popc(me[wd]);
+        const int lo = wd * 32;
+        if (d >= lo + 32) i += __popc(me[wd]);
+        else if (d > lo) i += __popc(me[wd] & ((1u << (d - lo)) - 1u));
+      }
+      const FastDiv fn = t.fdt[n];
+      const int qq = (int)fdiv_hi((uint32_t)w, fn), rem = w - qq * n;
+      q = qq + (i < rem ? 1 : 0);
+      if (q <= 0) continue;
+      end = (i + 1) * qq + imin(i + 1, rem);
+    }
+    const int r = rr[d * E + e];
+    p.csr_r[first + i] = r;
+    p.csr_end[first + i] = end;
+    atomicAdd(&sendl[r], q);
+  }
+  if (tid == 0) {
+    int all = 0;
+    for (int b = 0; b < (E + 63) >> 6; ++b) all += wt[b];
+    p.csr_ptr[E] = all;
+  }
+  // replica slots: slot t of local rank j of domain d holds stage-1 entry
+  // t G + j (entries are a prefix of the domain's list)
+  for (int i = tid; i < R * p.N; i += nt) {
+    const int r = (int)fdiv((uint32_t)i, p.fN), s2 = i - r * p.N;
+    const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
+    p.slots_out[i] = s2 < p.Neff ? repl[d * cap + s2 * G + j] : -1;
+  }
+  lds_barrier();
+  STAMP(p, 30);
+  for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
 }
 
 // Every step after the load: with Omega' in om (row self = the histogram hs)
@@ -1775,8 +1978,7 @@ __device__ inline void single_init(const Plan &p, const SingleState &t) {
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
 template <bool Pairs = false>
-__device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
-                            bool write_status = true, bool read_arrival = false) {
+__device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
   int *hs = t.hs, *ccnt = t.ccnt, *dfree = t.dfree, *repl = t.repl, *slots = t.slots, *used = t.used;
@@ -1802,9 +2004,29 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
   lds_barrier();
   STAMP(p, 23);
 
-  // ---- inter-node placement (Eq. 9): one wave per domain
-  for (int d = wave; d < M; d += nw) stage1_domain_wave(p, d, om, ck + (int64_t)d * E, ccnt, repl + d * cap);
-  lds_barrier();
+  // ---- inter-node placement (Eq. 9), every domain by the whole workgroup
+  // (qcol is free until the routing)
+  stage1_ranks(p, om, ck, ccnt, qcol);
+
+  // ---- no domain can refine (all slots taken, or one rank per domain):
+  // the routing rule alone gives this rank's shares
+  {
+    bool full = true;
+    for (int d = 0; d < M && full; ++d) full = uniform_i32(ccnt[d]) >= cap;
+    if (full || G < 2) {
+      fast_finish(p, t, ck, qcol, reinterpret_cast<int *>(em), U);
+      STAMP(p, 7);
+      if (tid == 0) {
+        const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
+        p.ctrl[kCtrlFinal] = fin;
+        if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
+        else p.status_out[0] = (int32_t)fin;
+        p.status_out[1] = 0;
+      }
+      return;
+    }
+  }
+  stage1_lists(p, ck, ccnt, qcol, repl);
   STAMP(p, 2);
 
   // ---- hosting domains per expert; every rank's slots and instances, and
@@ -1905,16 +2127,10 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
     p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
   }
   for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
-  // (one-launch plan: the verdict word read here is in by the end of the
-  // instance list, so its wait costs no round trip once the chunks are done)
-  uint32_t arrival = 0;
-  if (read_arrival && tid == 0)
-    arrival = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   STAMP(p, 6);
   emit_instance_list(p, qcol, slots, used, bm, t.wt);
   STAMP(p, 7);
-  if (read_arrival && tid == 0) misc[6] = (int)arrival;
-  if (write_status && tid == 0) {
+  if (tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;
     if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
@@ -1925,10 +2141,23 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
 
 // Receive counts from the single-workgroup solver's final LDS state (after
 // single_plan made a plan): the instances on rank self, full columns when
-// its domain was routed for every source.
-__device__ void single_recv_counts(const Plan &p, const SingleState &t) {
+// its domain was routed for every source.  A plan of fast_finish (misc[15])
+// kept no instance state: rank self's instances are its mains and its
+// stage-1 replicas (slot t = entry t G + j of its domain's list), and the
+// routing rule gives every source's share.
+__device__ __forceinline__ void single_recv_counts(const Plan &p, const SingleState &t) {
   const int ds = (int)fdiv((uint32_t)p.self, p.fG), E = p.E;
   const int *om = t.om;
+  if (t.misc[15]) {
+    int *selfe = t.U;
+    const int js = p.self - ds * p.G;
+    for (int a = threadIdx.x; a < p.PN; a += blockDim.x)
+      selfe[a] = a < p.P ? p.self * p.P + a : t.repl[ds * p.cap1 + (a - p.P) * p.G + js];
+    lds_barrier();
+    write_recv_counts(p, 0, selfe, nullptr, false, t.mask, t.fdt, [&](int s, int e) { return om[s * E + e]; },
+                      t.hs);
+    return;
+  }
   // (hs, the histogram, is no longer needed: it is the scratch)
   write_recv_counts(p, ds * p.I + (p.self - ds * p.G) * p.PN, t.e_of, t.qcol, t.dfree[ds] != 0, t.mask, t.fdt,
                     [&](int s, int e) { return om[s * E + e]; }, t.hs);
@@ -1936,7 +2165,7 @@ __device__ void single_recv_counts(const Plan &p, const SingleState &t) {
 
 // Send offsets of the one-launch plan (exclusive prefix of the send counts
 // sendl, total at [R]) by wave 0, for the caller and for the chunks.
-__device__ void solver_send_offsets(const Plan &p, const int *sendl) {
+__device__ __forceinline__ void solver_send_offsets(const Plan &p, const int *sendl) {
   if (threadIdx.x >= 64) return;
   const int lane = threadIdx.x, R = p.R;
   const int per = (R + 63) / 64, lo = imin(R, lane * per), hi = imin(R, lo + per);
@@ -2203,7 +2432,7 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
 // every thread once the first loads are issued (LDS set-up that overlaps
 // their latency); the status words are written after a barrier behind it.
 template <typename Between>
-__device__ void load_omega(const Plan &p, int *om, int *misc, Between between) {
+__device__ __forceinline__ void load_omega(const Plan &p, int *om, int *misc, Between between) {
   const int tid = threadIdx.x, nt = blockDim.x, n = p.R * p.E;
   bool neg = false;
   uint64_t tot = 0;
@@ -2289,25 +2518,27 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   if (tid == 0) t.misc[40] = (int)gen;   // (single_init clears words 0..15 only)
   lds_barrier();
   STAMP(p, 1);
-  const uint64_t total0 = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
-  const uint32_t neg0 = (uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD;
+  const uint64_t total0 = uniform_u64(*reinterpret_cast<const unsigned long long *>(t.misc + 8));
+  const uint32_t neg0 = (uint32_t)uniform_i32(t.misc[0]) & TOPOEP_ST_NEG_LOAD;
   const uint32_t gst0 = neg0 | (out_of_range(p, total0) ? TOPOEP_ST_RANGE : 0u);
   // Speculative plan from Omega as gathered while the chunks count: it is
   // the plan whenever the histogram equals row self (the gathered row is
   // this rank's own count), else it is redone below; nothing reads the
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
-  if (spec) single_plan<Pairs>(p, t, gst0, true, false, true);
+  if (spec) single_plan<Pairs>(p, t, gst0, true);   // (with its status: it usually stands)
   STAMP(p, 8);
-  // the last chunk's verdict on this generation (the word read while the
-  // instance list was built is usually it already)
+  // the last chunk's verdict on this generation: its first read overlaps
+  // the drain of the speculative outputs
+  uint32_t w = 0;
+  if (tid == 0) w = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  drain_then_barrier();
   if (tid == 0) {
     const uint32_t want = (gen + 1u) & 0x3FFFFFFFu;
-    uint32_t w = (uint32_t)t.misc[6];
     bool ok = false;
     for (uint32_t it = 0; it < p.spin_limit; ++it) {
-      if (it > 0 || !spec) {
-        if (it > 0) __builtin_amdgcn_s_sleep(1);
+      if (it > 0) {
+        __builtin_amdgcn_s_sleep(1);
         w = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       if ((w >> 2) == want) {
@@ -2316,7 +2547,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
       }
     }
     // acquire: the histogram of a redo, and (passed on by the flags' release)
-    // the chunks' offsets the last chunk wrote
+    // the chunks' counts
     if (ok) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     t.misc[2] = ok;
     t.misc[3] = (int)(w & 3u);
@@ -2327,16 +2558,10 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   const uint32_t verdict = (uint32_t)t.misc[3];
   const bool stands = synced && verdict == kVerdictSame && spec;
   bool planned = stands;
-  // a rewrite of the speculative outputs is ordered after their stores
-  if (spec && !stands) drain_then_barrier();
+  // a plan that does not stand: its status bits go (a chunk's SYNC stays)
+  if (spec && !stands && tid == 0) atomicAnd(reinterpret_cast<unsigned *>(p.status_out), TOPOEP_ST_SYNC);
   if (stands) {
-    // the speculative plan stands (Omega' = Omega): its status
-    if (tid == 0) {
-      const uint32_t fin = (uint32_t)t.misc[0];
-      p.ctrl[kCtrlFinal] = fin;
-      atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
-      p.status_out[1] = t.misc[12];
-    }
+    // the speculative plan stands (Omega' = Omega) with its status
   } else if (synced && verdict == kVerdictSame) {
     single_plan(p, t, gst0, true);   // Omega itself refused: blank outputs
   } else if (synced) {
@@ -2379,7 +2604,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
     if (tid == 0) __hip_atomic_store(&p.ctrl[kCtrlGen], gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   STAMP_FLUSH(p, 0, 12);
-  STAMP_FLUSH(p, 20, 25);
+  STAMP_FLUSH(p, 20, 32);
   // receive counts of a plan that was made (a refused one wrote zeros):
   // for the caller only, so they are summed while the chunks route
   if (planned && p.recv_out) single_recv_counts(p, t);

@@ -123,6 +123,15 @@ __device__ inline int row16_incl_scan(int x) {
 
 __device__ inline int readlane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 
+// A value every lane of the wave holds alike (read from LDS, say), made
+// scalar: work on it then runs once on the scalar unit instead of in every
+// lane of every wave.
+__device__ inline int uniform_i32(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ inline uint64_t uniform_u64(uint64_t v) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(v >> 32)) << 32) |
+         (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
 __device__ inline bool lex_less(uint64_t a1, uint64_t a2, uint64_t a3, uint64_t b1, uint64_t b2,
                                 uint64_t b3) {
   if (a1 != b1) return a1 < b1;
