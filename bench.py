@@ -313,6 +313,9 @@ PHASE_SLOTS = [(0, "solver start"), (1, "Omega in LDS"), (23, "plan start"), (22
                (24, "s1: candidates"), (26, "s1: ranks"), (27, "ff: lists and hosting"), (28, "ff: counts"), (30, "ff: entries")]
 
 
+REFINE_SECTIONS = ["busiest and levels", "scoring", "selection", "target instance", "transfer", "updates"]
+
+
 def run_phases(args):
     """Phase timeline of the one-launch plan from the stamped library (run
     with TOPOEP_STAMPS=1): every layer planned in one HIP graph, replayed;
@@ -329,10 +332,11 @@ def run_phases(args):
     topo = topoep.topology(cfg.R, cfg.G, cfg.E, 0, cfg.c_intra, cfg.c_inter, cfg.S, cfg.W)
     dev_inputs = [(torch.from_numpy(gl.copy()).to(dev), torch.from_numpy(tk.copy()).to(dev)) for gl, tk in inputs]
     launch = launch_from_args(args)
-    planners = [topoep.Planner(topo, cfg.T, cfg.k, cfg.N, device=dev, launch=launch) for _ in range(layers)]
+    N = cfg.N if args.slots < 0 else args.slots
+    planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev, launch=launch) for _ in range(layers)]
     if planners[0].shape.kernels != 1:
         raise SystemExit("--phases covers the one-launch plan only")
-    samples = []
+    samples, refine = [], []
     for rep in range(args.steps):
         for p, (g, t) in zip(planners, dev_inputs):
             p.plan(g, t)
@@ -343,6 +347,8 @@ def run_phases(args):
             w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
             samples.append([((int(w[i]) - int(w[0])) & 0xFFFFFFFF) if i < 20 or i > 21 else 0
                             for i, _ in PHASE_SLOTS])
+            if w[38] > 0:
+                refine.append([w[32 + k] / w[38] for k in range(6)] + [w[38]])
     clk = []
     for p in planners:
         w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
@@ -351,11 +357,17 @@ def run_phases(args):
             clk.append(((int(w[21]) - int(w[20])) & 0xFFFFFFFF) / (dt * 0.01))
     arr = np.array(samples, dtype=np.float64) * 0.01   # 100 MHz ticks -> microseconds
     med = np.median(arr, axis=0)
-    out = {"phases": cfg.name, "layers": layers, "samples": len(samples),
+    out = {"phases": cfg.name, "replica_slots": N, "layers": layers, "samples": len(samples),
            "us_after_solver_start_median": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, med)},
            "us_p10": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 10, axis=0))},
            "us_p90": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 90, axis=0))},
            "core_clock_MHz_median": round(float(np.median(clk)), 1) if clk else None,
+           # domain 0's refinement loop: core-clock cycles per iteration by
+           # section (median over the plans that refined it)
+           "refine_cycles_per_iteration": (
+               {name: round(float(v), 1) for name, v in zip(REFINE_SECTIONS + ["iterations"],
+                                                             np.median(np.array(refine, dtype=np.float64), axis=0))}
+               if refine else None),
            "plan_shape": planners[0].shape.as_dict()}
     return out
 
@@ -719,6 +731,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="dsv3", choices=sorted(DESCR))
     ap.add_argument("--layers", type=int, default=0, help="0 = the configuration's layer count")
+    ap.add_argument("--slots", type=int, default=-1, help="replica slots per rank for --phases (-1: the configuration's)")
     ap.add_argument("--stage-reps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU baseline budget: half for one thread, a quarter for every core")

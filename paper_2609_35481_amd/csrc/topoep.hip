@@ -108,7 +108,7 @@ struct Plan {
   int rchunks_all, rchunks_dom;   // routing: source-domain chunks (divisors of M)
   uint32_t spin_limit;   // polls of a bounded wait (0: every such wait gives up at once)
   uint32_t iter_limit;   // committed refinement moves per domain before ITER
-  FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fG1, fN, fMI;
+  FastDiv fE, fG, fGP, fP, fI, fPN, fCap, fN, fMI;
   const int32_t *gl, *topk;
   int32_t *slots_out, *dest_out, *send_out, *status_out;
   int32_t *recv_out;   // receive counts [R], or null
@@ -150,6 +150,28 @@ __shared__ uint32_t stamp_lds[48];
     if (threadIdx.x == 0)                                                    \
       for (int s_ = (lo); s_ < (hi); ++s_) (p).ctrl[kCtrlStamps + s_] = stamp_lds[s_]; \
   } while (0)
+#define STAMP_CLEAR(lo, hi)                                       \
+  do {                                                            \
+    if (threadIdx.x == 0)                                         \
+      for (int s_ = (lo); s_ < (hi); ++s_) stamp_lds[s_] = 0;     \
+  } while (0)
+// Core-clock cycles of the refinement loop of domain 0 by section, summed
+// over its iterations (slots 32..37, the iteration count in slot 38).
+#define RSECT_DECL(d)           \
+  const bool rs_on_ = (d) == 0; \
+  uint64_t rs_last_ = __builtin_amdgcn_s_memtime();
+#define RSECT(k)                                                                     \
+  do {                                                                               \
+    if (rs_on_) {                                                                    \
+      const uint64_t n_ = __builtin_amdgcn_s_memtime();                              \
+      if (lane_id() == 0) atomicAdd(&stamp_lds[32 + (k)], (uint32_t)(n_ - rs_last_)); \
+      rs_last_ = n_;                                                                 \
+    }                                                                                \
+  } while (0)
+#define RSECT_END(iters)                                           \
+  do {                                                             \
+    if (rs_on_ && lane_id() == 0) atomicAdd(&stamp_lds[38], (iters)); \
+  } while (0)
 #else
 #define STAMP(p, i) \
   do {              \
@@ -159,6 +181,16 @@ __shared__ uint32_t stamp_lds[48];
   } while (0)
 #define STAMP_FLUSH(p, lo, hi) \
   do {                         \
+  } while (0)
+#define STAMP_CLEAR(lo, hi) \
+  do {                      \
+  } while (0)
+#define RSECT_DECL(d)
+#define RSECT(k) \
+  do {           \
+  } while (0)
+#define RSECT_END(iters) \
+  do {                   \
   } while (0)
 #endif
 
@@ -174,7 +206,7 @@ __device__ inline int vgpr(int v) {
 
 // The plan with its divisors in vector registers (see vgpr).
 __device__ inline Plan solver_plan(Plan q) {
-  FastDiv *fds[] = {&q.fE, &q.fG, &q.fGP, &q.fP, &q.fI, &q.fPN, &q.fCap, &q.fG1, &q.fN, &q.fMI};
+  FastDiv *fds[] = {&q.fE, &q.fG, &q.fGP, &q.fP, &q.fI, &q.fPN, &q.fCap, &q.fN, &q.fMI};
   for (FastDiv *f : fds) {
     f->m = (uint32_t)vgpr((int)f->m);
     f->sh = (uint32_t)vgpr((int)f->sh);
@@ -801,16 +833,311 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
   return -1;
 }
 
+// Forms of the refinement loop: the register form where the domain fits it
+// (refine_in_registers), else the LDS form; a kernel that knows its form
+// carries only that one's code.
+constexpr int kRefineAny = 0, kRefineReg = 1, kRefineLds = 2;
+__host__ __device__ inline bool refine_in_registers(int G, int I, int PN) { return G <= 16 && I <= 128 && PN <= 64; }
+
+// Minimum over each row of 16 lanes, left in every lane of the row.
+__device__ inline uint32_t row_min_all_u32(uint32_t v) {
+  uint32_t o;
+  o = dpp_mov<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov<0x121>(v); v = o < v ? o : v;
+  return v;
+}
+__device__ inline uint64_t row_min_all_u64(uint64_t v) {
+  uint64_t o;
+  o = dpp_mov64<0x128>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x124>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x122>(v); v = o < v ? o : v;
+  o = dpp_mov64<0x121>(v); v = o < v ? o : v;
+  return v;
+}
+// Lane l's value in a vector register (the same in every lane), and a lane
+// predicate as 0 or 1 in a vector register.  A single wave pays about 20
+// cycles each time the scalar unit consumes a vector result (a lane mask
+// combined with s_and, a branch on a compare, arithmetic on a readlane), and
+// plain bool logic lives in scalar lane masks; values passed through these
+// keep such logic in vector instructions (selects, ands) instead.
+__device__ inline int vlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ inline uint64_t vlane64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)vlane((int)(v >> 32), l) << 32) | (uint32_t)vlane((int)v, l);
+}
+__device__ inline int vb(bool b) { return b ? 1 : 0; }
+__device__ inline int row_max_all_i32(int v) {
+  int o;
+  o = (int)dpp_mov<0x128>((uint32_t)v); v = o > v ? o : v;
+  o = (int)dpp_mov<0x124>((uint32_t)v); v = o > v ? o : v;
+  o = (int)dpp_mov<0x122>((uint32_t)v); v = o > v ? o : v;
+  o = (int)dpp_mov<0x121>((uint32_t)v); v = o > v ? o : v;
+  return v;
+}
+
+// Register form of the refinement loop below (two-level cost, G <= GM <= 16
+// ranks, I <= 128 instances, PN <= 64): lane l keeps instances l and l + 64
+// (expert, load, the domain ranks hosting that expert) and lane j < G rank
+// j's load and used slots; only the q columns stay in LDS.  It makes the
+// same moves in the same order as the LDS form (the busiest rank rb, lowest
+// index on ties; one lane per instance of rb scoring its lightest
+// receivers; the minimum of (delta descending, L[rt], cost change, e, rt);
+// the transfer from rt's own assignments, then the other sources
+// ascending, rb's own last), as straight-line vector code with few scalar
+// hand-overs (see vlane and vb).  e_of, U, Lr, used, slots, em and the q
+// columns hold the final state on return.
+template <int GM>
+__device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
+                                      int *Lr, uint64_t *em, uint32_t *flags) {
+  const int lane = lane_id();
+  const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, I = p.I;
+  const int r0 = d * G;
+  const bool two_level = p.cI > 0;
+  const int64_t tokc = 2 * p.S * (int64_t)p.cI;
+  const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
+  const bool one_row = PN <= 16;
+  const int vl = vgpr(lane);
+  const int rank_lane = vb(vl < G), rb_lane = vb(vl < PN), src_lane = vb(vl < R);
+  // instance registers: lane l holds instances l and l + 64
+  int ie0 = vl < I ? e_of[vl] : -1, ie1 = vl + 64 < I ? e_of[vl + 64] : -1;
+  int iu0 = vl < I ? U[vl] : 0, iu1 = vl + 64 < I ? U[vl + 64] : 0;
+  uint32_t ih0 = ie0 >= 0 ? (uint32_t)em[ie0] : 0u, ih1 = ie1 >= 0 ? (uint32_t)em[ie1] : 0u;
+  // rank registers (lanes >= G: never the busiest, never a receiver)
+  int lj = rank_lane ? Lr[vl] : -1;
+  int uj = rank_lane ? used[vl] : Neff;
+  uint32_t it = 0;
+  RSECT_DECL(d);
+  for (;; ++it) {
+    // ---- busiest rank rb: the largest L, lowest index on ties
+    const int Lrb = vlane(row_max_all_i32(lj), 0);
+    const int rbj_s = __ffsll((long long)__ballot(rank_lane && lj == Lrb)) - 1;
+    const int rbj = vgpr(rbj_s);
+    const int rb = r0 + rbj;
+    // ---- receivers: L[rt] <= L[rb] - 2; the lightest with a free slot form
+    // one level (lf, tfm); hosting receivers matter up to that level (lightm)
+    const int low = rank_lane & vb(vl != rbj) & vb(Lrb - lj >= 2);
+    const int fr = low & vb(uj < Neff);
+    const uint32_t lf = (uint32_t)vlane((int)row_min_all_u32(fr ? (uint32_t)lj : ~0u), 0);
+    const uint32_t tfm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr & vb((uint32_t)lj == lf)));
+    const uint32_t lightm = (uint32_t)vgpr((int)(uint32_t)__ballot(low & vb((uint32_t)lj <= lf)));
+    RSECT(0);
+    // ---- lane c < PN: rb's instance a = rbj PN + c, its fields from the lane
+    // holding it
+    const int a = rbj * PN + vl;
+    const int src = (a & 63) << 2;
+    const int e0 = __builtin_amdgcn_ds_bpermute(src, ie0), e1 = __builtin_amdgcn_ds_bpermute(src, ie1);
+    const int u0 = __builtin_amdgcn_ds_bpermute(src, iu0), u1 = __builtin_amdgcn_ds_bpermute(src, iu1);
+    const int h0 = __builtin_amdgcn_ds_bpermute(src, (int)ih0), h1 = __builtin_amdgcn_ds_bpermute(src, (int)ih1);
+    const int *qa = qcol + (rb_lane ? a : 0) * QS;
+    const int qrb = two_level ? qa[rb] : 0;
+    const int hi = vb(a >= 64);
+    const int e = hi ? e1 : e0, u = hi ? u1 : u0;
+    const uint32_t hm = (uint32_t)(hi ? h1 : h0);
+    const int cand = rb_lane & vb(e >= 0) & vb(u > 0);
+    // the lightest receivers hosting e, no heavier than the free level
+    const uint32_t hl = cand ? hm & lightm : 0u;
+    uint32_t lh = ~0u, th = 0u;
+    if (__ballot(hl != 0u)) {
+#pragma unroll
+      for (int j = 0; j < GM; ++j) {
+        const uint32_t Lj = (uint32_t)__builtin_amdgcn_readlane(lj, j);
+        const uint32_t c = (hl >> j) & 1u ? Lj : ~0u;
+        th = c < lh ? 1u << j : (c == lh ? th | (1u << j) : th);
+        lh = c < lh ? c : lh;
+      }
+    }
+    const uint32_t lm = lf < lh ? lf : lh;
+    const int valid = cand & vb(lm != ~0u);
+    const uint32_t tset = valid ? ((lf == lm ? tfm : 0u) | (lh == lm ? th : 0u)) : 0u;
+    const int delta = imin(u, (Lrb - (int)lm) >> 1);
+    // ---- cost change at each target of tset, lowest (cost, rt) kept
+    auto cost_at = [&](int jt, int &qt) {
+      int64_t dc = 0;
+      qt = 0;
+      if (two_level) {
+        qt = qa[r0 + jt];
+        const int m_rt = imin(delta, qt);
+        const int rest = delta - m_rt;
+        const int m_rb = rest - imin(rest, u - qt - qrb);
+        dc = tokc * (int64_t)(m_rb - m_rt);
+      }
+      const int64_t rep = ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+      return ((hm >> jt) & 1u) ? dc : dc + rep;
+    };
+    int bj = valid ? __ffs(tset) - 1 : 0;
+    int bq;
+    int64_t bc = cost_at(bj, bq);
+    const uint32_t more = tset & (tset - 1u);
+    if (__ballot(more != 0u)) {
+      for (uint32_t t = more; t; t &= t - 1u) {
+        const int jt = __ffs(t) - 1;
+        int qt;
+        const int64_t dc = cost_at(jt, qt);
+        if (dc < bc) {
+          bc = dc;
+          bj = jt;
+          bq = qt;
+        }
+      }
+    }
+    RSECT(1);
+    // ---- minimum key: (delta descending, L[rt]) first, then cost, e, rt
+    const uint64_t k1 = valid ? ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm : ~0ull;
+    uint64_t m1 = row_min_all_u64(k1);
+    if (!one_row) {
+      const uint64_t x1 = vlane64(m1, 16), x2 = vlane64(m1, 32), x3 = vlane64(m1, 48);
+      m1 = vlane64(m1, 0);
+      m1 = x1 < m1 ? x1 : m1;
+      m1 = x2 < m1 ? x2 : m1;
+      m1 = x3 < m1 ? x3 : m1;
+    } else {
+      m1 = vlane64(m1, 0);
+    }
+    if (m1 == ~0ull) break;
+    if (it >= p.iter_limit) {
+      if (lane == 0) *flags |= TOPOEP_ST_ITER;
+      break;
+    }
+    uint64_t win = __ballot(k1 == m1);
+    if (__popcll(win) != 1) {
+      const bool in2 = k1 == m1;
+      const uint64_t kc = in2 ? (uint64_t)bc ^ (1ull << 63) : ~0ull;
+      const uint64_t m3 = wave_min_u64(kc);
+      win &= __ballot(kc == m3);
+      if (__popcll(win) != 1) {
+        const bool in3 = ((win >> lane) & 1ull) != 0;
+        const uint64_t ke = in3 ? ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj) : ~0ull;
+        const uint64_t m4 = wave_min_u64(ke);
+        win &= __ballot(ke == m4);
+      }
+    }
+    const int wl = __ffsll((long long)win) - 1;
+    const int dw = vlane(delta, wl);
+    const int Lrt = vlane((int)lm, wl);
+    const int ew = vlane(e, wl);
+    const int rtj_s = __builtin_amdgcn_readlane(bj, wl);
+    const int rtj = vgpr(rtj_s);
+    const int rt = r0 + rtj;
+    const int uw = vlane(u, wl);
+    const int qrt = vlane(bq, wl);
+    const uint32_t hw = (uint32_t)vlane((int)hm, wl);
+    const int aw_s = rbj_s * PN + wl;
+    const int aw = vgpr(aw_s);
+    const int fresh = vb(((hw >> rtj) & 1u) == 0u);
+    RSECT(2);
+    // ---- rt's instance of e: the one it holds (rt's instances are rtj PN ..
+    // rtj PN + PN - 1), or its first free slot
+    const int base = rtj * PN;
+    const uint64_t f0 = __ballot(vb(ie0 == ew) & vb((uint32_t)(vl - base) < (uint32_t)PN));
+    const uint64_t f1 = __ballot(vb(ie1 == ew) & vb((uint32_t)(vl + 64 - base) < (uint32_t)PN));
+    const int held = f0 ? __ffsll((long long)f0) - 1 : 64 + __ffsll((long long)f1) - 1;
+    const int a2 = fresh ? base + P + vlane(uj, rtj_s) : vgpr(held);
+    RSECT(3);
+    // ---- the transfer of dw assignments from aw's column to a2's
+    int *qw = qcol + aw_s * QS;
+    int *qb = qcol + a2 * QS;
+    if (R <= 64) {
+      // one pass: rt's own first, the other sources ascending, rb's own last;
+      // lanes >= R take the spare word after the sources (QS > R)
+      const int sv = src_lane ? vl : R;
+      const int av = src_lane ? qw[sv] : 0;
+      int excl;
+      if (two_level) {
+        const int is_rt = vb(vl == rt), is_rb = vb(vl == rb);
+        const int other = (is_rt | is_rb) ? 0 : av;
+        const int incl = wave_incl_scan(other);
+        const int tot = vlane(incl, 63);
+        excl = is_rt ? 0 : (is_rb ? qrt + tot : qrt + incl - other);
+      } else {
+        excl = wave_incl_scan(av) - av;
+      }
+      int m = dw - excl;
+      m = m < 0 ? 0 : (m > av ? av : m);
+      qw[sv] = av - m;
+      atomicAdd(&qb[sv], m);
+    } else {
+      int rest = dw;
+      int m_rt = 0;
+      if (two_level) {
+        m_rt = imin(rest, qrt);
+        rest -= m_rt;
+      }
+      for (int s0 = 0; s0 < R && rest > 0; s0 += 64) {
+        const int sv = s0 + lane;
+        int av = 0;
+        if (sv < R && (!two_level || (sv != rt && sv != rb))) av = qw[sv];
+        const int incl = wave_incl_scan(av);
+        const int excl = incl - av;
+        int m = rest - excl;
+        m = m < 0 ? 0 : (m > av ? av : m);
+        if (m) {
+          qw[sv] = av - m;
+          atomicAdd(&qb[sv], m);
+        }
+        const int total = readlane_i32(incl, 63);
+        rest -= total < rest ? total : rest;
+      }
+      if (lane == 0) {
+        if (m_rt) {
+          atomicSub(&qw[rt], m_rt);
+          atomicAdd(&qb[rt], m_rt);
+        }
+        if (rest > 0) {
+          atomicSub(&qw[rb], rest);
+          atomicAdd(&qb[rb], rest);
+        }
+      }
+    }
+    RSECT(4);
+    // ---- registers: the two instances' loads, a new replica's expert and the
+    // hosting mask of its expert, the two ranks
+    const uint32_t hn = hw | (1u << rtj);
+    const int at0 = vb(vl == a2), at1 = vb(vl + 64 == a2);
+    iu0 = vl == aw ? uw - dw : iu0;
+    iu1 = vl + 64 == aw ? uw - dw : iu1;
+    iu0 = at0 ? iu0 + dw : iu0;
+    iu1 = at1 ? iu1 + dw : iu1;
+    ie0 = (fresh & at0) ? ew : ie0;
+    ie1 = (fresh & at1) ? ew : ie1;
+    ih0 = (fresh & vb(ie0 == ew)) ? hn : ih0;
+    ih1 = (fresh & vb(ie1 == ew)) ? hn : ih1;
+    lj = vl == rbj ? Lrb - dw : (vl == rtj ? Lrt + dw : lj);
+    uj = (fresh & vb(vl == rtj)) ? uj + 1 : uj;
+    RSECT(5);
+  }
+  RSECT_END(it);
+  // final state: instances, their slots, the hosting masks, the ranks
+  auto put = [&](int a, int ex, int ux, uint32_t hx) {
+    if (a < I) {
+      e_of[a] = ex;
+      U[a] = ux;
+      const int j = (int)fdiv((uint32_t)a, p.fPN), pos = a - j * PN;
+      if (pos >= P) slots[j * Neff + pos - P] = ex;
+      if (ex >= 0) em[ex] = (uint64_t)hx;
+    }
+  };
+  put(vl, ie0, iu0, ih0);
+  put(vl + 64, ie1, iu1, ih1);
+  if (rank_lane) {
+    Lr[vl] = lj;
+    used[vl] = uj;
+  }
+  wave_sync();
+  return it;
+}
+
 // Intra-node refinement of domain d (Section 4.3, Eq. 10), by one wave.
 // e_of/U/qcol/slots/used/Lr point at the domain's own state; em (E words of
 // 64 bits, scratch) receives, per expert, the mask of the domain's local
 // ranks hosting it.  Each iteration picks the busiest rank rb (ties to the
 // lowest rank), takes the best (instance of rb, other rank of the domain)
 // candidate by key (delta desc, L[rt] asc, cost change asc, e asc, rt asc)
-// and commits it.  With Pairs (at most 64 candidates) each lane scores one
-// pair; otherwise each lane takes an instance and scores only its lightest
-// receivers (the others cannot win).  The moved assignments come from sources in
-// ascending (c(s,rt) - c(s,rb), s) order: with the two-level cost that is rt
+// and commits it: each lane takes an instance of rb and scores only its
+// lightest receivers (the others cannot win).  Domains that fit it run the
+// register form (refine_domain_reg); Form pins one form at compile time.
+// The moved assignments come from sources in ascending (c(s,rt) - c(s,rb),
+// s) order: with the two-level cost that is rt
 // itself, then the other sources ascending, then rb (or plain ascending when
 // the intra-domain cost is zero).  The loop ends when no candidate has
 // delta >= 1.  Returns the number of moves committed (at once 0 when no rank
@@ -820,10 +1147,10 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // moved assignments come from the sources in the precomputed (c(s,rt) -
 // c(s,rb), s) order of gc, and the cost change uses the cost matrix and
 // ||W_e||.
-template <bool General = false, bool Pairs = false>
+template <bool General = false, int Form = kRefineAny>
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                   int *Lr, uint64_t *em, uint32_t *flags, bool prepared, GenCost gc = GenCost{}) {
-  static_assert(!(General && Pairs), "the pair layout scores the two-level cost only");
+  static_assert(!(General && Form == kRefineReg), "the register form scores the two-level cost only");
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return 0;
@@ -853,6 +1180,15 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     }
   }
   wave_sync();
+  if constexpr (!General && Form != kRefineLds) {
+    if (Form == kRefineReg || refine_in_registers(G, I, PN)) {
+      return G <= 8 ? refine_domain_reg<8>(p, d, e_of, U, qcol, slots, used, Lr, em, flags)
+                    : refine_domain_reg<16>(p, d, e_of, U, qcol, slots, used, Lr, em, flags);
+    }
+  }
+  if constexpr (Form == kRefineReg) {
+    return 0;   // (not reached: the host picks the register form only where it applies)
+  } else {
   // One lane per instance of rb.  Among the targets an instance may move to
   // (the domain's other ranks with L[rt] <= L[rb] - 2 that host its expert
   // or have a free slot) delta = min(u, (L[rb] - L[rt]) / 2) only grows as
@@ -874,6 +1210,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     uj = used[lane];
   }
   uint32_t it = 0;
+  RSECT_DECL(d);
   for (;; ++it) {
     // busiest rank, lowest index on ties
     const int Lrb = (int)~min_u32(lane < G ? ~(uint32_t)lj : ~0u);
@@ -883,7 +1220,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     // take any expert, and the lightest of them form one level (lf, tf)
     const bool low = lane < G && lane != rbj && (int64_t)Lrb - lj >= 2;
     const uint64_t lowm = __ballot(low);
-    if (!Pairs && lowm == 0) break;   // (the pair layout needs none of these levels)
+    if (lowm == 0) break;
     const bool fr = low && uj < Neff;
     uint32_t lf = ~0u;
     uint64_t tf = 0;
@@ -894,45 +1231,10 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     // the first rank of the free level: its q is read with the instance's
     // own words (it is usually the one target scored)
     const int jf = tf ? __ffsll((long long)tf) - 1 : 0;
+    RSECT(0);
     uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull, best_hm = 0;
     int best_a = 0, best_u = 0, best_q = 0;
-    if constexpr (Pairs) {
-      // one lane per (instance of rb, other rank) pair, PN (G - 1) <= 64:
-      // every load of a candidate issued at once
-      const int npair = PN * (G - 1);
-      if (lane < npair) {
-        const int pai = (int)fdiv((uint32_t)lane, p.fG1), pjj = lane - pai * (G - 1);
-        const int rtj = pjj < rbj ? pjj : pjj + 1;
-        const int rt = r0 + rtj;
-        const int a = rbj * PN + pai;
-        const int *qa = qcol + a * QS;
-        const int e = e_of[a], u = U[a], Lrt = Lr[rtj], urt = used[rtj];
-        const int qrt = p.cI > 0 ? qa[rt] : 0, qrb = p.cI > 0 ? qa[rb] : 0;
-        const int64_t gap = (int64_t)Lrb - Lrt;
-        if (e >= 0 && u > 0 && gap >= 2) {
-          const uint64_t hmf = em[e];
-          const bool hosts = (hmf >> rtj) & 1ull;
-          if (hosts || urt < Neff) {
-            const int delta = (int)((int64_t)u < gap / 2 ? (int64_t)u : gap / 2);
-            int64_t dcost = 0;
-            if (p.cI > 0) {
-              const int m_rt = imin(delta, qrt);
-              const int rest = delta - m_rt;
-              const int m_rb = rest - imin(rest, u - qrt - qrb);
-              dcost = tokc * (int64_t)(m_rb - m_rt);
-            }
-            if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
-            k1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | (uint32_t)Lrt;
-            k2 = (uint64_t)dcost ^ (1ull << 63);
-            k3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)rt;
-            best_a = a;
-            best_u = u;
-            best_hm = hmf;
-            best_q = qrt;
-          }
-        }
-      }
-    } else {
+    {
       for (int rd = 0; rd < rounds; ++rd) {
         const int ai = lane + rd * 64;
         if (ai >= PN) continue;
@@ -1014,6 +1316,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
         }
       }
     }
+    RSECT(1);
     const uint64_t m1 = wave_min_u64(k1);
     if (m1 == ~0ull) break;
     // a move is still available after iter_limit of them: stop with ITER
@@ -1042,6 +1345,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     const int ua = readlane_i32(best_u, wl);
     const int qrt = readlane_i32(best_q, wl);
     const bool hosts = (readlane64(best_hm, wl) >> rtj) & 1ull;
+    RSECT(2);
     // rt's instance of e: its main expert, the replica slot holding it, or a
     // new replica in rt's first free slot
     int a2 = -1;
@@ -1058,6 +1362,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
         if (hit) a2 = rtj * PN + P + t0 + __ffsll((long long)hit) - 1;
       }
     }
+    RSECT(3);
     int *qa = qcol + a * QS;
     int *qb = qcol + a2 * QS;
     int rest = delta;
@@ -1103,6 +1408,7 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
         rest -= total < rest ? total : rest;
       }
     }
+    RSECT(4);
     // (the sources above exclude rt and rb, so these words are disjoint
     // from the lanes' updates; LDS atomics without return need no wait)
     if (lane == 0) {
@@ -1131,8 +1437,11 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
       uj += fresh ? 1 : 0;
     }
     wave_sync();
+    RSECT(5);
   }
+  RSECT_END(it);
   return it;   // one move per completed iteration
+  }
 }
 
 // Stage-1 candidate key: (D descending, e ascending) as one unsigned
@@ -1977,7 +2286,7 @@ __device__ __forceinline__ void fast_finish(const Plan &p, const SingleState &t,
 // Eq. 10 refinement) and writes replica_slots, send_counts, this rank's
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
-template <bool Pairs = false>
+template <int Form = kRefineAny>
 __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
@@ -2104,7 +2413,7 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
     // ranks' loads first; a domain without a free slot returns at once)
     uint32_t flags = 0, moves = 0;
     for (int d = wave; d < M; d += nw)
-      moves += refine_domain<false, Pairs>(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
+      moves += refine_domain<false, Form>(p, d, e_of + d * I, U + d * I, qcol + d * I * p.QS, slots + d * G * Neff,
                              used + d * G, Lr + d * G, em + (int64_t)d * E, &flags, true);
     if (lane_id() == 0) {
       if (flags) atomicOr(reinterpret_cast<unsigned *>(&misc[0]), flags);
@@ -2497,7 +2806,7 @@ __device__ __forceinline__ void read_histogram(const Plan &p, const uint32_t *gh
 // histogram with row self of Omega, that plan stands (equal rows, so Omega'
 // = Omega) or is made again from Omega' on fresh state; then every chunk's
 // flag is set to g + 1 and the generation advances.
-template <bool Pairs>
+template <int Form>
 __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   const SingleState t = single_state(p, sm);
   const int tid = threadIdx.x, nt = blockDim.x, E = p.E;
@@ -2513,6 +2822,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   }
   STAMP(p, 0);
   STAMP_CLK(p, 20);
+  STAMP_CLEAR(32, 39);
   if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
   load_omega(p, t.om, t.misc, [&] { single_init(p, t); });
   if (tid == 0) t.misc[40] = (int)gen;   // (single_init clears words 0..15 only)
@@ -2526,7 +2836,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   // this rank's own count), else it is redone below; nothing reads the
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
-  if (spec) single_plan<Pairs>(p, t, gst0, true);   // (with its status: it usually stands)
+  if (spec) single_plan<Form>(p, t, gst0, true);   // (with its status: it usually stands)
   STAMP(p, 8);
   // the last chunk's verdict on this generation: its first read overlaps
   // the drain of the speculative outputs
@@ -2563,7 +2873,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   if (stands) {
     // the speculative plan stands (Omega' = Omega) with its status
   } else if (synced && verdict == kVerdictSame) {
-    single_plan(p, t, gst0, true);   // Omega itself refused: blank outputs
+    single_plan<Form>(p, t, gst0, true);   // Omega itself refused: blank outputs
   } else if (synced) {
     // row self differs from the histogram, or a bad id: plan again from
     // Omega' (row self = the histogram) on fresh state
@@ -2587,10 +2897,10 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
     lds_barrier();
     uint32_t gst = (uint32_t)t.misc[0];
     if (out_of_range(p, total0 + *reinterpret_cast<const unsigned long long *>(t.misc + 8))) gst |= TOPOEP_ST_RANGE;
-    single_plan<Pairs>(p, t, gst, true);
+    single_plan<Form>(p, t, gst, true);
     planned = !(gst & kNoPlan);
   } else {
-    single_plan<Pairs>(p, t, TOPOEP_ST_SYNC, true);
+    single_plan<Form>(p, t, TOPOEP_ST_SYNC, true);
   }
   if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
   // release: every output the chunks read (the instance list, the final
@@ -2604,7 +2914,7 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
     if (tid == 0) __hip_atomic_store(&p.ctrl[kCtrlGen], gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   STAMP_FLUSH(p, 0, 12);
-  STAMP_FLUSH(p, 20, 32);
+  STAMP_FLUSH(p, 20, 39);
   // receive counts of a plan that was made (a refused one wrote zeros):
   // for the caller only, so they are summed while the chunks route
   if (planned && p.recv_out) single_recv_counts(p, t);
@@ -2945,17 +3255,17 @@ __device__ inline Plan role_plan(const Plan &p) {
 #endif
 }
 
-// Pairs: the refinement scores one (instance, target) pair per lane
-// (domains with PN (G - 1) <= 64 candidates), else each instance's lightest
-// receivers; one instantiation each keeps the other's registers out.
-template <int IPT, bool Pairs>
+// Reg: the refinement runs in registers (refine_in_registers holds for the
+// shape), else in LDS; one instantiation each keeps the other's registers
+// out.
+template <int IPT, bool Reg>
 __global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
   extern __shared__ int64_t smem_f[];
   int *sm = reinterpret_cast<int *>(smem_f);
   (void)p;
   if (blockIdx.x == 0) {
     const Plan q = solver_plan(role_plan(p));
-    fused_solver<Pairs>(q, sm);
+    fused_solver<Reg ? kRefineReg : kRefineLds>(q, sm);
   } else {
     const Plan q = role_plan(p);
     fused_chunk<IPT>(q, blockIdx.x - 1, sm);
@@ -3030,7 +3340,7 @@ int resident_capacity(const void *fn, int threads, size_t lds) {
   return cap;
 }
 
-const void *fused_fn(int ipt, bool pairs);
+const void *fused_fn(int ipt, bool reg);
 
 // Validate the arguments and fill the plan's sizes, launch shape and
 // workspace layout (pointers are offsets when ws == nullptr).
@@ -3060,7 +3370,9 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.rbits = ceil_log2(R);
   q.cap1 = G * q.Neff;
   q.nent_cap = E + R * q.Neff;
-  q.QS = R | 1;   // odd row stride of the q columns: no LDS bank conflicts
+  // odd row stride of the q columns (no LDS bank conflicts) with at least
+  // one spare word after the R sources
+  q.QS = (R + 1) | 1;
   q.cI = t->cost_intra;
   q.cX = t->cost_inter;
   q.S = t->tok_bytes;
@@ -3084,7 +3396,6 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.fI = make_fastdiv((uint32_t)q.I);
   q.fPN = make_fastdiv((uint32_t)q.PN);
   q.fCap = make_fastdiv((uint32_t)imax(q.cap1, 1));
-  q.fG1 = make_fastdiv((uint32_t)imax(G - 1, 1));
   q.fN = make_fastdiv((uint32_t)imax(N, 1));
   q.fMI = make_fastdiv((uint32_t)(q.M * q.I));
 
@@ -3126,7 +3437,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
     // every workgroup of the launch resident at once (they wait on each other)
     if (fused_ok)
-      fused_ok = nbf + 1 <= resident_capacity(fused_fn(ipt, q.PN * (q.G - 1) <= 64), st, (size_t)fused_words * 4);
+      fused_ok = nbf + 1 <= resident_capacity(fused_fn(ipt, refine_in_registers(q.G, q.I, q.PN)), st, (size_t)fused_words * 4);
     if (solver == 3 && !fused_ok) return TOPOEP_ELIMIT;
     if (general && solver == 3) return TOPOEP_EINVAL;   // the general model runs the per-domain solver
     if (fused_ok && !general && (solver == 3 || solver == 0)) {
@@ -3250,16 +3561,16 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
 
 std::atomic<bool> g_attrs_set{false};
 
-const void *fused_fn(int ipt, bool pairs) {
+const void *fused_fn(int ipt, bool reg) {
   switch (ipt) {
-    case 1: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<1, true>)
-                         : reinterpret_cast<const void *>(plan_fused_kernel<1, false>);
-    case 2: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<2, true>)
-                         : reinterpret_cast<const void *>(plan_fused_kernel<2, false>);
-    case 4: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<4, true>)
-                         : reinterpret_cast<const void *>(plan_fused_kernel<4, false>);
-    default: return pairs ? reinterpret_cast<const void *>(plan_fused_kernel<8, true>)
-                          : reinterpret_cast<const void *>(plan_fused_kernel<8, false>);
+    case 1: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<1, true>)
+                       : reinterpret_cast<const void *>(plan_fused_kernel<1, false>);
+    case 2: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<2, true>)
+                       : reinterpret_cast<const void *>(plan_fused_kernel<2, false>);
+    case 4: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<4, true>)
+                       : reinterpret_cast<const void *>(plan_fused_kernel<4, false>);
+    default: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<8, true>)
+                        : reinterpret_cast<const void *>(plan_fused_kernel<8, false>);
   }
 }
 
@@ -3315,19 +3626,19 @@ void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
 }
 
 template <int IPT>
-void launch_fused_ipt(bool pairs, dim3 g, dim3 b, size_t lds, hipStream_t st, const Plan &p) {
-  if (pairs) hipLaunchKernelGGL((plan_fused_kernel<IPT, true>), g, b, lds, st, p);
+void launch_fused_ipt(bool reg, dim3 g, dim3 b, size_t lds, hipStream_t st, const Plan &p) {
+  if (reg) hipLaunchKernelGGL((plan_fused_kernel<IPT, true>), g, b, lds, st, p);
   else hipLaunchKernelGGL((plan_fused_kernel<IPT, false>), g, b, lds, st, p);
 }
 
 void launch_fused(const Plan &p, const Shape &s, hipStream_t st) {
   const dim3 g(p.nb + 1), b(s.st);
-  const bool pairs = p.PN * (p.G - 1) <= 64;   // the refinement's candidates fit one wavefront
+  const bool reg = refine_in_registers(p.G, p.I, p.PN);
   switch (s.ipt) {
-    case 1: launch_fused_ipt<1>(pairs, g, b, s.lds_fused, st, p); break;
-    case 2: launch_fused_ipt<2>(pairs, g, b, s.lds_fused, st, p); break;
-    case 4: launch_fused_ipt<4>(pairs, g, b, s.lds_fused, st, p); break;
-    default: launch_fused_ipt<8>(pairs, g, b, s.lds_fused, st, p); break;
+    case 1: launch_fused_ipt<1>(reg, g, b, s.lds_fused, st, p); break;
+    case 2: launch_fused_ipt<2>(reg, g, b, s.lds_fused, st, p); break;
+    case 4: launch_fused_ipt<4>(reg, g, b, s.lds_fused, st, p); break;
+    default: launch_fused_ipt<8>(reg, g, b, s.lds_fused, st, p); break;
   }
 }
 
