@@ -685,10 +685,11 @@ def run_sweep(args):
             topo = topoep.topology(R, G, E, 0, 1, 8, 4096, 9 << 20)
             # the three-kernel path, so the histogram and reroute kernels run
             # alone (the per-domain solver where one workgroup's LDS is too small)
+            shape = (args.ipt, args.block_threads, args.tiles_per_block, 0)
             try:
-                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_SINGLE))
+                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=shape + (topoep.SOLVER_SINGLE,))
             except topoep.TopoepError:
-                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=(0, 0, 0, 0, topoep.SOLVER_PER_DOMAIN))
+                pl = topoep.Planner(topo, T, k, 2, device=dev, launch=shape + (topoep.SOLVER_PER_DOMAIN,))
             pl.plan(gl, tk_d)
             torch.cuda.synchronize()
             st = int(pl.status[0].item())

@@ -2544,8 +2544,7 @@ __device__ void slot_offsets(const Plan &p, int *offs, int *tmp, bool first) {
 
 // excl[r] = assignments to rank r before the tile (run[e]: occurrences of e
 // before it; ptr/er/eend: this rank's instance list).  Ends with a barrier.
-__device__ void slot_before(const Plan &p, const int *run, const int *ptr, const int *er, const int *eend,
-                            int *excl) {
+__device__ void slot_before(const Plan &p, const int *run, const int *ptr, const int2 *ent, int *excl) {
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int r = tid; r < p.R; r += nt) excl[r] = 0;
   lds_barrier();
@@ -2553,22 +2552,49 @@ __device__ void slot_before(const Plan &p, const int *run, const int *ptr, const
     const int re = run[e], j1 = ptr[e + 1];
     int start = 0;
     for (int j = ptr[e]; j < j1; ++j) {
-      const int end = eend[j];
-      const int c = imin(imax(re - start, 0), end - start);
-      if (c > 0 && (unsigned)er[j] < (unsigned)p.R) atomicAdd(&excl[er[j]], c);
-      start = end;
+      const int2 en = ent[j];   // (cumulative share, rank)
+      const int c = imin(imax(re - start, 0), en.x - start);
+      if (c > 0 && (unsigned)en.y < (unsigned)p.R) atomicAdd(&excl[en.y], c);
+      start = en.x;
     }
   }
   lds_barrier();
 }
 
+// Per-wave counts to offsets, one column per key: wc[w * ws + k] (w < nw <=
+// 16 waves, k < n keys, ws > n odd so a column's words sit in distinct
+// banks) becomes base[k] + the counts of waves 0..w-1, and base[k] grows by
+// the column's total (base may be null: offsets from 0).  A group of g
+// lanes (g = nw rounded up to a power of two) per key scans the column in
+// registers instead of walking it with nw dependent LDS round trips.
+__device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *base) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63;
+  const int lg = nw <= 1 ? 0 : 32 - __clz(nw - 1);   // log2 of the group size
+  const int g = 1 << lg, w = lane & (g - 1);
+  for (int k = tid >> lg; k < n; k += nt >> lg) {
+    const int v = w < nw ? wc[w * ws + k] : 0;
+    int x = v;
+    // inclusive scan inside the group (row shifts; a group never crosses a row)
+    int y;
+    y = (int)dpp_mov<0x111>((uint32_t)x); x += w >= 1 ? y : 0;
+    y = (int)dpp_mov<0x112>((uint32_t)x); x += w >= 2 ? y : 0;
+    y = (int)dpp_mov<0x114>((uint32_t)x); x += w >= 4 ? y : 0;
+    y = (int)dpp_mov<0x118>((uint32_t)x); x += w >= 8 ? y : 0;
+    const int tot = __shfl(x, lane | (g - 1));
+    const int b0 = base ? base[k] : 0;
+    if (w < nw) wc[w * ws + k] = b0 + x - v;
+    if (base && w == 0) base[k] = b0 + tot;
+  }
+}
+
 // Slots of one tile (destinations dv in registers; index order: wave, then
-// i, then lane); wcd: blockDim/64 * R words of scratch.
+// i, then lane); wcd: blockDim/64 * (R | 1) words of scratch.
 template <int IPT>
 __device__ void slot_write(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi, const int *offs,
                            const int *excl, int *wcd) {
-  const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6, R = p.R;
-  int *mw = wcd + wave * R;
+  const int nt = blockDim.x, nw = nt >> 6, lane = threadIdx.x & 63, wave = threadIdx.x >> 6, R = p.R;
+  const int ws = R | 1;
+  int *mw = wcd + wave * ws;
   for (int r = lane; r < R; r += 64) mw[r] = 0;
   wave_sync();
   int lr[IPT];
@@ -2583,14 +2609,7 @@ __device__ void slot_write(const Plan &p, const int (&dv)[IPT], int64_t wbase, i
     wave_sync();
   }
   lds_barrier();
-  for (int r = tid; r < R; r += nt) {
-    int run = 0;
-    for (int w = 0; w < nw; ++w) {
-      const int t = wcd[w * R + r];
-      wcd[w * R + r] = run;
-      run += t;
-    }
-  }
+  scan_wave_columns(wcd, ws, R, nw, nullptr);
   lds_barrier();
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
@@ -2608,14 +2627,14 @@ template <int IPT>
 __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   extern __shared__ int smem_r[];
   const int nt = blockDim.x, nw = nt >> 6;
-  const int E = p.E;
-  int *run = smem_r;                 // E: running offset per expert
-  int *wc = run + E;                 // nw * E: per-wave counts, then offsets
-  int *ptr = wc + nw * E;            // E + 1
-  int *er = ptr + E + 1;             // nent_cap: instance rank
-  int *eend = er + p.nent_cap;       // nent_cap: cumulative share
-  int *wcd = eend + p.nent_cap;      // nw * R: send-buffer slots: per-wave counts
-  int *excl = wcd + nw * p.R;        // R: assignments per rank before the tile
+  const int E = p.E, ws = E | 1;
+  int2 *ent = reinterpret_cast<int2 *>(smem_r);   // nent_cap: (cumulative share, rank) per entry
+  int2 *cur = ent + p.nent_cap;      // E: (entry holding the next occurrence, end of e's entries)
+  int *run = reinterpret_cast<int *>(cur + E);   // E: running offset per expert
+  int *wc = run + E;                 // nw * ws: per-wave counts, then offsets
+  int *ptr = wc + nw * ws;           // E + 1
+  int *wcd = ptr + E + 1;            // nw * (R | 1): send-buffer slots: per-wave counts
+  int *excl = wcd + nw * (p.R | 1);  // R: assignments per rank before the tile
   int *so = excl + p.R;              // R + 1 + nw + 1: send offsets, scan scratch
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
@@ -2630,6 +2649,19 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
       for (int r = tid; r <= p.R; r += nt) p.offs_out[r] = 0;
     return;
   }
+  // the first tile's ids are on their way while the block reads its offsets
+  // and the instance list
+  const int64_t tile = (int64_t)nt * IPT;
+  int evn[IPT];
+  auto load_tile = [&](int64_t base) {
+    const int64_t wbase = base + (int64_t)wave * 64 * IPT + lane;
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int64_t idx = wbase + i * 64;
+      evn[i] = idx < hi ? p.topk[idx] : -1;
+    }
+  };
+  load_tile(lo);
   if (p.offs_out) {
     for (int r = tid; r < p.R; r += nt) so[r] = p.send_out[r];
     slot_offsets(p, so, so + p.R + 1, b == 0);
@@ -2641,25 +2673,31 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   }
   __syncthreads();
   const int nent = ptr[E];
-  for (int j = tid; j < nent; j += nt) {
-    er[j] = p.csr_r[j];
-    eend[j] = p.csr_end[j];
-  }
+  for (int j = tid; j < nent; j += nt) ent[j] = make_int2(p.csr_end[j], p.csr_r[j]);
+  for (int e = tid; e < E; e += nt) cur[e] = make_int2(ptr[e], ptr[e + 1]);
   __syncthreads();
-  int *mywc = wc + wave * E;
-  const int64_t tile = (int64_t)nt * IPT;
+  int *mywc = wc + wave * ws;
   for (int64_t base = lo; base < hi; base += tile) {
-    // run[e] counts e's occurrences before this tile
-    if (p.slot_out) slot_before(p, run, ptr, er, eend, excl);
+    int ev[IPT];
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) ev[i] = evn[i];
+    // the next tile's ids load while this one is ranked (the barriers below
+    // order LDS only, so they do not wait for these loads)
+    if (base + tile < hi) load_tile(base + tile);
+    // run[e] counts e's occurrences before this tile: each expert's cursor
+    // moves to the entry holding occurrence run[e]
+    for (int e = tid; e < E; e += nt) {
+      int2 c = cur[e];
+      const int re = run[e];
+      const int c0 = c.x;
+      while (c.x < c.y && ent[c.x].x <= re) ++c.x;
+      if (c.x != c0) cur[e] = c;
+    }
+    if (p.slot_out) slot_before(p, run, ptr, ent, excl);
     for (int e = lane; e < E; e += 64) mywc[e] = 0;
     wave_sync();
     const int64_t wbase = base + (int64_t)wave * 64 * IPT + lane;
-    int ev[IPT], lr[IPT];
-#pragma unroll
-    for (int i = 0; i < IPT; ++i) {
-      const int64_t idx = wbase + i * 64;
-      ev[i] = idx < hi ? p.topk[idx] : -1;
-    }
+    int lr[IPT];
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
       const int64_t idx = wbase + i * 64;
@@ -2671,17 +2709,9 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
       if (valid && (peers & lanemask_lt()) == 0) mywc[ev[i]] = c + __popcll(peers);
       wave_sync();
     }
-    __syncthreads();
-    for (int e = tid; e < E; e += nt) {
-      int s = run[e];
-      for (int w = 0; w < nw; ++w) {
-        const int t = wc[w * E + e];
-        wc[w * E + e] = s;
-        s += t;
-      }
-      run[e] = s;
-    }
-    __syncthreads();
+    lds_barrier();
+    scan_wave_columns(wc, ws, E, nw, run);
+    lds_barrier();
     int dv[IPT];
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
@@ -2689,11 +2719,14 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
       int dest = -1;
       if (idx < hi) {
         if ((unsigned)ev[i] < (unsigned)E) {
+          // occurrence rho of e: the entry at e's cursor holds it unless the
+          // occurrences of this tile run past that instance's share
           const int rho = mywc[ev[i]] + lr[i];
-          const int j1 = ptr[ev[i] + 1];
-          for (int j = ptr[ev[i]]; j < j1; ++j) {
-            if (rho < eend[j]) {
-              dest = er[j];
+          const int2 c = cur[ev[i]];
+          for (int j = c.x; j < c.y; ++j) {
+            const int2 en = ent[j];
+            if (rho < en.x) {
+              dest = en.y;
               break;
             }
           }
@@ -2703,7 +2736,7 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
       dv[i] = dest;
     }
     if (p.slot_out) slot_write<IPT>(p, dv, wbase, hi, so, excl, wcd);
-    __syncthreads();
+    lds_barrier();
   }
 }
 
@@ -3493,8 +3526,8 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     return TOPOEP_ELIMIT;
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
-  s.lds_reroute = ((size_t)E * (2 + s.bt / 64) + 1 + 2 * (size_t)q.nent_cap +
-                   (size_t)R * (s.bt / 64 + 2) + 1 + s.bt / 64 + 1) * 4;
+  s.lds_reroute = (2 * (size_t)q.nent_cap + 2 * (size_t)E + 2 * (size_t)E + (size_t)(E | 1) * (s.bt / 64) + 1 +
+                   (size_t)(R | 1) * (s.bt / 64) + 2 * (size_t)R + 1 + s.bt / 64 + 1) * 4;
   s.lds_fused = 0;
   if (s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
   }

@@ -18,14 +18,21 @@ __device__ inline int lane_id() { return threadIdx.x & 63; }
 __device__ inline uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
 
 // Lanes of this wave holding the same (valid) value: one ballot per id bit.
+// A lane differs from lane x where some bit of x's value, as read from that
+// bit's ballot, differs from its own; the differences accumulate in one
+// three-input bit operation per mask half (v_bitop3 on gfx950).
 __device__ inline uint64_t peer_mask(int v, bool valid, int nbits) {
-  uint64_t m = __ballot(valid);
-  for (int b = 0; b < nbits; ++b) {
-    const bool bit = (v >> b) & 1;
-    const uint64_t on = __ballot(bit);
-    m &= bit ? on : ~on;
+  const uint64_t vm = __ballot(valid);
+  uint32_t dlo = 0, dhi = 0;
+#pragma unroll
+  for (int b = 0; b < 31; ++b) {
+    if (b >= nbits) break;
+    const int sb = (v << (31 - b)) >> 31;   // bit b as 0 or all ones
+    const uint64_t on = __ballot(sb != 0);
+    dlo |= (uint32_t)on ^ (uint32_t)sb;
+    dhi |= (uint32_t)(on >> 32) ^ (uint32_t)sb;
   }
-  return m;
+  return vm & ~(((uint64_t)dhi << 32) | dlo);
 }
 
 // Order LDS traffic of the lanes of one wave (the refinement runs on one
