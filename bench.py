@@ -313,6 +313,13 @@ PHASE_SLOTS = [(0, "solver start"), (1, "Omega in LDS"), (23, "plan start"), (22
                (24, "s1: candidates"), (26, "s1: ranks"), (27, "ff: lists and hosting"), (28, "ff: counts"), (30, "ff: entries")]
 
 
+# the per-domain solver (three-kernel plan): workgroup 0's phases, then the
+# last workgroup's instance list
+SOLVE_SLOTS = [(0, "solver start"), (1, "stage 1"), (2, "grid barrier passed"), (3, "row self and hosting masks"),
+               (4, "domain instances"), (5, "q columns"), (6, "routing"), (7, "refinement"), (8, "outputs"),
+               (9, "drained"), (10, "list start (last workgroup)"), (11, "list counted"), (12, "list placed"),
+               (13, "list done"), (14, "s1: rows copied"), (15, "s1: row self"), (16, "s1: candidates")]
+
 REFINE_SECTIONS = ["busiest and levels", "scoring", "selection", "target instance", "transfer", "updates"]
 
 
@@ -334,8 +341,7 @@ def run_phases(args):
     launch = launch_from_args(args)
     N = cfg.N if args.slots < 0 else args.slots
     planners = [topoep.Planner(topo, cfg.T, cfg.k, N, device=dev, launch=launch) for _ in range(layers)]
-    if planners[0].shape.kernels != 1:
-        raise SystemExit("--phases covers the one-launch plan only")
+    slots = PHASE_SLOTS if planners[0].shape.kernels == 1 else SOLVE_SLOTS
     samples, refine = [], []
     for rep in range(args.steps):
         for p, (g, t) in zip(planners, dev_inputs):
@@ -346,21 +352,21 @@ def run_phases(args):
         for p in planners:
             w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
             samples.append([((int(w[i]) - int(w[0])) & 0xFFFFFFFF) if i < 20 or i > 21 else 0
-                            for i, _ in PHASE_SLOTS])
+                            for i, _ in slots])
             if w[38] > 0:
                 refine.append([w[32 + k] / w[38] for k in range(6)] + [w[38]])
     clk = []
     for p in planners:
         w = p.workspace_view()[64:256].cpu().numpy().view(np.uint32).astype(np.int64)
         dt = (int(w[10]) - int(w[0])) & 0xFFFFFFFF
-        if dt:
+        if dt and slots is PHASE_SLOTS:
             clk.append(((int(w[21]) - int(w[20])) & 0xFFFFFFFF) / (dt * 0.01))
     arr = np.array(samples, dtype=np.float64) * 0.01   # 100 MHz ticks -> microseconds
     med = np.median(arr, axis=0)
     out = {"phases": cfg.name, "replica_slots": N, "layers": layers, "samples": len(samples),
-           "us_after_solver_start_median": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, med)},
-           "us_p10": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 10, axis=0))},
-           "us_p90": {name: round(float(v), 3) for (_, name), v in zip(PHASE_SLOTS, np.percentile(arr, 90, axis=0))},
+           "us_after_solver_start_median": {name: round(float(v), 3) for (_, name), v in zip(slots, med)},
+           "us_p10": {name: round(float(v), 3) for (_, name), v in zip(slots, np.percentile(arr, 10, axis=0))},
+           "us_p90": {name: round(float(v), 3) for (_, name), v in zip(slots, np.percentile(arr, 90, axis=0))},
            "core_clock_MHz_median": round(float(np.median(clk)), 1) if clk else None,
            # domain 0's refinement loop: core-clock cycles per iteration by
            # section (median over the plans that refined it)

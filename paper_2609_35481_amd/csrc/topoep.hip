@@ -155,6 +155,7 @@ __shared__ uint32_t stamp_lds[48];
     if (threadIdx.x == 0)                                         \
       for (int s_ = (lo); s_ < (hi); ++s_) stamp_lds[s_] = 0;     \
   } while (0)
+__device__ inline void stamp_nc(int nc) { stamp_lds[17] = (uint32_t)nc; }
 // Core-clock cycles of the refinement loop of domain 0 by section, summed
 // over its iterations (slots 32..37, the iteration count in slot 38).
 #define RSECT_DECL(d)           \
@@ -185,6 +186,7 @@ __shared__ uint32_t stamp_lds[48];
 #define STAMP_CLEAR(lo, hi) \
   do {                      \
   } while (0)
+__device__ inline void stamp_nc(int) {}
 #define RSECT_DECL(d)
 #define RSECT(k) \
   do {           \
@@ -1784,6 +1786,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   const int E = p.E, G = p.G, R = p.R, M = p.M, I = p.I, P = p.P, PN = p.PN, Neff = p.Neff;
   const int cap = p.cap1;
 
+  if (wg == 0) STAMP(p, 0);
   if (tid < 16) misc[tid] = 0;
   build_divisors(M, fdt);
   uint64_t cmax = (uint64_t)imax(p.cI, p.cX), wmax = (uint64_t)p.W;
@@ -1804,7 +1807,9 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   // ---- inter-node placement (Eq. 9), each domain independently
   for (int d = wg; d < M; d += nwg) {
     copy_to_lds(rows, p.gl + (int64_t)d * G * E, G * E);
+    if (wg == 0) STAMP(p, 14);
     if (d == dself) row_self(p, hs, qcol, &misc[10]);
+    if (wg == 0) STAMP(p, 15);
     if (tid == 0) misc[1] = 0;
     lds_barrier();
     scan_rows(p, d * G, (d + 1) * G, rows, hs, misc);
@@ -1830,7 +1835,9 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       }
     }
     lds_barrier();
+    if (wg == 0) STAMP(p, 16);
     const int nc = misc[1];
+    if (wg == 0 && tid == 0) stamp_nc(nc);
     for (int c = tid; c < nc; c += nt) {
       if (p.general) rank_candidates_b(c, nc, cap, ck, qcol, p.repl1 + (int64_t)d * cap);
       else rank_candidates(c, nc, cap, ck, p.repl1 + (int64_t)d * cap);
@@ -1845,7 +1852,9 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   }
 
   // ---- every domain's replicas are needed by every routing construction
+  if (wg == 0) STAMP(p, 1);
   const bool synced = grid_barrier(&p.ctrl[kCtrlBar], (uint32_t)nwg, p.spin_limit, &misc[2]);
+  if (wg == 0) STAMP(p, 2);
   uint32_t gst = __hip_atomic_load(&p.ctrl[kCtrlStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const uint64_t total = __hip_atomic_load(reinterpret_cast<unsigned long long *>(p.ctrl + kCtrlTotal),
                                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1874,6 +1883,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     }
   }
   __syncthreads();
+  if (wg == 0) STAMP(p, 3);
 
   uint32_t flags = 0;
   for (int d = wg; d < M; d += nwg) {
@@ -1926,6 +1936,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       U[a] = 0;
     }
     lds_barrier();
+    if (wg == 0) STAMP(p, 4);
     // whether the domain can refine at all (a rank with a free slot); if not,
     // only the q[self] column is needed, else the columns omega[s][e] of the
     // domain's instances, then q in place
@@ -1948,6 +1959,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       }
     }
     lds_barrier();
+    if (wg == 0) STAMP(p, 5);
     route_instances(
         p, I, p.fI, p.rchunks_dom, e_of, mask, fdt, qcol, U, [&](int i, int) { return qcol + i * p.QS; }, 1,
         [&](int) { return d; }, [&](int) { return full; }, [](int, int, int, int) {});
@@ -1958,6 +1970,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       Lr[j] = l;
     }
     lds_barrier();
+    if (wg == 0) STAMP(p, 6);
     if (p.general && full) {
       const GenCost gc = general_tables(p, d, sm, lay);
       if (tid < 64) {
@@ -1969,6 +1982,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
       if (tid == 0 && mv) atomicAdd(&p.ctrl[kCtrlMoves], mv);
     }
     lds_barrier();
+    if (wg == 0) STAMP(p, 7);
     // outputs of the domain's ranks
     for (int i = tid; i < G * p.N; i += nt) {
       const int j = (int)fdiv((uint32_t)i, p.fN), t = i - j * p.N;
@@ -1992,13 +2006,18 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   if (tid == 0 && (flags || !synced)) atomicOr(&p.ctrl[kCtrlStatus], flags | (synced ? 0u : TOPOEP_ST_SYNC));
 
   // ---- the last workgroup to finish lists this rank's instances per expert
+  if (wg == 0) STAMP(p, 8);
   drain_then_barrier();
+  if (wg == 0) STAMP(p, 9);
+  if (wg == 0) STAMP_FLUSH(p, 0, 10);
+  if (wg == 0) STAMP_FLUSH(p, 14, 18);
   if (tid == 0) {
     const uint32_t t = __hip_atomic_fetch_add(&p.ctrl[kCtrlTicket], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     misc[4] = t == (uint32_t)nwg - 1;
   }
   __syncthreads();
   if (!misc[4]) return;
+  STAMP(p, 10);
   int *cnt = qcol;                                            // E + 1
   uint32_t *bm = reinterpret_cast<uint32_t *>(qcol + E + 2);  // E * RW
   int *tmp = qcol + E + 2 + E * p.RW;                         // scan scratch (64)
@@ -2040,6 +2059,7 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
   for (int u = 0; u < kListRegs; ++u) count(tid + u * nt, se[u], sq[u]);
   for (int idx = tid + kListRegs * nt; idx < M * I; idx += nt) count(idx, p.seg_e[idx], p.seg_q[idx]);
   __syncthreads();
+  STAMP(p, 11);
   block_excl_scan(cnt, E + 1, tmp);
   for (int e = tid; e <= E; e += nt) p.csr_ptr[e] = cnt[e];
 #pragma unroll
@@ -2055,8 +2075,11 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
     }
   }
   __syncthreads();
+  STAMP(p, 12);
   for (int j = tid; j < cnt[E]; j += nt) p.csr_end[j] = cv[j];
   __syncthreads();
+  STAMP(p, 13);
+  STAMP_FLUSH(p, 10, 14);
   if (tid == 0) {
     uint32_t fin = __hip_atomic_load(&p.ctrl[kCtrlStatus], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     fin |= gst & TOPOEP_ST_RANGE;
@@ -2564,11 +2587,25 @@ __device__ void slot_before(const Plan &p, const int *run, const int *ptr, const
 // Per-wave counts to offsets, one column per key: wc[w * ws + k] (w < nw <=
 // 16 waves, k < n keys, ws > n odd so a column's words sit in distinct
 // banks) becomes base[k] + the counts of waves 0..w-1, and base[k] grows by
-// the column's total (base may be null: offsets from 0).  A group of g
-// lanes (g = nw rounded up to a power of two) per key scans the column in
-// registers instead of walking it with nw dependent LDS round trips.
+// the column's total (base may be null: offsets from 0).  Beyond four waves
+// a group of g lanes (g = nw rounded up to a power of two) per key scans
+// the column in registers instead of walking it with nw dependent LDS
+// round trips.
 __device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *base) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63;
+  if (nw <= 4) {
+    // short columns: one thread walks each
+    for (int k = tid; k < n; k += nt) {
+      int run = base ? base[k] : 0;
+      for (int w = 0; w < nw; ++w) {
+        const int t = wc[w * ws + k];
+        wc[w * ws + k] = run;
+        run += t;
+      }
+      if (base) base[k] = run;
+    }
+    return;
+  }
   const int lg = nw <= 1 ? 0 : 32 - __clz(nw - 1);   // log2 of the group size
   const int g = 1 << lg, w = lane & (g - 1);
   for (int k = tid >> lg; k < n; k += nt >> lg) {
@@ -2687,11 +2724,17 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
     // run[e] counts e's occurrences before this tile: each expert's cursor
     // moves to the entry holding occurrence run[e]
     for (int e = tid; e < E; e += nt) {
+      // first entry of [c.x, c.y) whose cumulative share exceeds run[e]
+      // (shares ascend): a binary search
       int2 c = cur[e];
       const int re = run[e];
-      const int c0 = c.x;
-      while (c.x < c.y && ent[c.x].x <= re) ++c.x;
-      if (c.x != c0) cur[e] = c;
+      int lo2 = c.x, hi2 = c.y;
+      while (lo2 < hi2) {
+        const int mid = (lo2 + hi2) >> 1;
+        if (ent[mid].x <= re) lo2 = mid + 1;
+        else hi2 = mid;
+      }
+      if (lo2 != c.x) cur[e] = make_int2(lo2, c.y);
     }
     if (p.slot_out) slot_before(p, run, ptr, ent, excl);
     for (int e = lane; e < E; e += 64) mywc[e] = 0;
