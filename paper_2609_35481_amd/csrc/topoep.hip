@@ -2309,8 +2309,13 @@ __device__ __forceinline__ void fast_finish(const Plan &p, const SingleState &t,
 // Eq. 10 refinement) and writes replica_slots, send_counts, this rank's
 // instance list and the final status (ctrl word and status_out).  With
 // BAD_ID, NEG_LOAD, RANGE or SYNC in gst only the blank outputs are written.
-template <int Form = kRefineAny>
-__device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status) {
+struct NoHook {
+  __device__ void operator()() const {}
+};
+
+template <int Form = kRefineAny, class Published = NoHook>
+__device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
+                                            Published published = NoHook{}) {
   uint64_t *ck = t.ck, *em = t.em;
   FastDiv *fdt = t.fdt;
   int *hs = t.hs, *ccnt = t.ccnt, *dfree = t.dfree, *repl = t.repl, *slots = t.slots, *used = t.used;
@@ -2355,6 +2360,7 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
         else p.status_out[0] = (int32_t)fin;
         p.status_out[1] = 0;
       }
+      published();
       return;
     }
   }
@@ -2469,6 +2475,7 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
     else p.status_out[0] = (int32_t)fin;
     p.status_out[1] = misc[12];
   }
+  published();
 }
 
 // Receive counts from the single-workgroup solver's final LDS state (after
@@ -2901,7 +2908,10 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   STAMP_CLEAR(32, 39);
   if (tid == 0) p.status_out[0] = 0;   // chunks may OR SYNC into it
   load_omega(p, t.om, t.misc, [&] { single_init(p, t); });
-  if (tid == 0) t.misc[40] = (int)gen;   // (single_init clears words 0..15 only)
+  if (tid == 0) {
+    t.misc[40] = (int)gen;   // (single_init clears words 0..15 only)
+    t.misc[44] = 0;          // the speculative plan went out early
+  }
   lds_barrier();
   STAMP(p, 1);
   const uint64_t total0 = uniform_u64(*reinterpret_cast<const unsigned long long *>(t.misc + 8));
@@ -2912,14 +2922,47 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   // this rank's own count), else it is redone below; nothing reads the
   // outputs before the flags say the plan is ready.
   const bool spec = !(gst0 & kNoPlan);
-  if (spec) single_plan<Form>(p, t, gst0, true);   // (with its status: it usually stands)
+  // the flags: every output the chunks read (the instance list, the final
+  // status, the send offsets) drained first, then released
+  auto release_flags = [&]() {
+    STAMP(p, 10);
+    STAMP_CLK(p, 21);
+    if (tid < 64)
+      for (int b = tid; b < p.nb; b += 64)
+        __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, gen + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto set_flags = [&]() {
+    drain_then_barrier();
+    release_flags();
+  };
+  // as soon as the speculative plan's list and status are written: when the
+  // verdict is already in and says the plan stands (the usual case), the
+  // flags go out at once
+  auto publish_early = [&]() {
+    if (tid == 0) {
+      const uint32_t v = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      t.misc[44] = ((v >> 2) == ((gen + 1u) & 0x3FFFFFFFu) && (v & 3u) == kVerdictSame) ? 1 : 0;
+    }
+    lds_barrier();
+    if (t.misc[44]) {
+      if (p.offs_out) solver_send_offsets(p, t.sendl);
+      set_flags();
+    }
+  };
+  if (spec) single_plan<Form>(p, t, gst0, true, publish_early);   // (with its status: it usually stands)
   STAMP(p, 8);
+  const bool early = t.misc[44] != 0;
   // the last chunk's verdict on this generation: its first read overlaps
   // the drain of the speculative outputs
   uint32_t w = 0;
-  if (tid == 0) w = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  drain_then_barrier();
-  if (tid == 0) {
+  if (!early && tid == 0) w = __hip_atomic_load(&p.ctrl[kCtrlVerdict], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (!early) drain_then_barrier();
+  if (early) {
+    if (tid == 0) {
+      t.misc[2] = 1;
+      t.misc[3] = (int)kVerdictSame;
+    }
+  } else if (tid == 0) {
     const uint32_t want = (gen + 1u) & 0x3FFFFFFFu;
     bool ok = false;
     for (uint32_t it = 0; it < p.spin_limit; ++it) {
@@ -2978,17 +3021,12 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   } else {
     single_plan<Form>(p, t, TOPOEP_ST_SYNC, true);
   }
-  if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
-  // release: every output the chunks read (the instance list, the final
-  // status, the send offsets) before the flags; then the next generation
-  drain_then_barrier();
-  STAMP(p, 10);
-  STAMP_CLK(p, 21);
-  if (tid < 64) {
-    for (int b = tid; b < p.nb; b += 64)
-      __hip_atomic_store(p.flags + (int64_t)b * kFlagStride, gen + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    if (tid == 0) __hip_atomic_store(&p.ctrl[kCtrlGen], gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (!early) {
+    if (planned && p.offs_out) solver_send_offsets(p, t.sendl);
+    set_flags();
   }
+  // the next generation
+  if (tid == 0) __hip_atomic_store(&p.ctrl[kCtrlGen], gen + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   STAMP_FLUSH(p, 0, 12);
   STAMP_FLUSH(p, 20, 39);
   // receive counts of a plan that was made (a refused one wrote zeros):
