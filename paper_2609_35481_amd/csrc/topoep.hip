@@ -2914,9 +2914,16 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   }
   lds_barrier();
   STAMP(p, 1);
+  // Omega's status, worked out by one thread (scalar 64-bit arithmetic that
+  // every wave would otherwise repeat on the CU's one scalar unit)
+  if (tid == 0) {
+    const uint64_t tot = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
+    t.misc[45] = (int)(((uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD) | (out_of_range(p, tot) ? TOPOEP_ST_RANGE : 0u));
+  }
+  lds_barrier();
   const uint64_t total0 = uniform_u64(*reinterpret_cast<const unsigned long long *>(t.misc + 8));
-  const uint32_t neg0 = (uint32_t)uniform_i32(t.misc[0]) & TOPOEP_ST_NEG_LOAD;
-  const uint32_t gst0 = neg0 | (out_of_range(p, total0) ? TOPOEP_ST_RANGE : 0u);
+  const uint32_t gst0 = (uint32_t)uniform_i32(t.misc[45]);
+  const uint32_t neg0 = gst0 & TOPOEP_ST_NEG_LOAD;
   // Speculative plan from Omega as gathered while the chunks count: it is
   // the plan whenever the histogram equals row self (the gathered row is
   // this rank's own count), else it is redone below; nothing reads the
