@@ -88,13 +88,7 @@ __device__ inline void rank_wave(int R, int nbits, const int (&dv)[IPT], int (&l
   wave_sync();
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const bool valid = (unsigned)dv[i] < (unsigned)R;
-    const uint64_t peers = peer_mask(dv[i], valid, nbits);
-    const int c = valid ? mywc[dv[i]] : 0;
-    lr[i] = c + __popcll(peers & lanemask_lt());
-    wave_sync();
-    if (valid && (peers & lanemask_lt()) == 0) mywc[dv[i]] = c + __popcll(peers);
-    wave_sync();
+    lr[i] = wave_rank(dv[i], (unsigned)dv[i] < (unsigned)R, nbits, mywc);
   }
 }
 

@@ -2644,13 +2644,8 @@ __device__ void slot_write(const Plan &p, const int (&dv)[IPT], int64_t wbase, i
   int lr[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const bool valid = wbase + i * 64 < hi && (unsigned)dv[i] < (unsigned)R;
-    const uint64_t peers = peer_mask(dv[i], valid, p.rbits);
-    const int c = valid ? mw[dv[i]] : 0;
-    lr[i] = c + __popcll(peers & lanemask_lt());
-    wave_sync();
-    if (valid && (peers & lanemask_lt()) == 0) mw[dv[i]] = c + __popcll(peers);
-    wave_sync();
+    // (dv is -1 past the end)
+    lr[i] = wave_rank(dv[i], (unsigned)dv[i] < (unsigned)R, p.rbits, mw);
   }
   lds_barrier();
   scan_wave_columns(wcd, ws, R, nw, nullptr);
@@ -2750,14 +2745,8 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
     int lr[IPT];
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
-      const int64_t idx = wbase + i * 64;
-      const bool valid = idx < hi && (unsigned)ev[i] < (unsigned)E;
-      const uint64_t peers = peer_mask(ev[i], valid, p.nbits);
-      const int c = valid ? mywc[ev[i]] : 0;
-      lr[i] = c + __popcll(peers & lanemask_lt());
-      wave_sync();
-      if (valid && (peers & lanemask_lt()) == 0) mywc[ev[i]] = c + __popcll(peers);
-      wave_sync();
+      // (ev is -1 past the end)
+      lr[i] = wave_rank(ev[i], (unsigned)ev[i] < (unsigned)E, p.nbits, mywc);
     }
     lds_barrier();
     scan_wave_columns(wc, ws, E, nw, run);
@@ -3163,13 +3152,8 @@ __device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT],
   int lr[IPT];
 #pragma unroll
   for (int i = 0; i < IPT; ++i) {
-    const bool valid = wbase + i * 64 < hi && (unsigned)dv[i] < (unsigned)R;
-    const uint64_t peers = peer_mask(dv[i], valid, p.rbits);
-    const int c = valid ? mw[dv[i]] : 0;
-    lr[i] = c + __popcll(peers & lanemask_lt());
-    wave_sync();
-    if (valid && (peers & lanemask_lt()) == 0) mw[dv[i]] = c + __popcll(peers);
-    wave_sync();
+    // (dv is -1 past the end)
+    lr[i] = wave_rank(dv[i], (unsigned)dv[i] < (unsigned)R, p.rbits, mw);
   }
   lds_barrier();
   // lane w of the row of rank r: wave w's count, scanned across the row
@@ -3227,14 +3211,9 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   for (int i = 0; i < IPT; ++i) {
     const int64_t idx = wbase + i * 64;
     const bool inr = idx < hi;
-    const bool valid = inr && (unsigned)ev[i] < (unsigned)E;
+    const bool valid = (unsigned)ev[i] < (unsigned)E;   // (ev is -1 past the end)
     bad |= (inr && !valid) ? 1 : 0;
-    const uint64_t peers = peer_mask(ev[i], valid, p.nbits);
-    const int c = valid ? mywc[ev[i]] : 0;
-    lr[i] = c + __popcll(peers & lanemask_lt());
-    wave_sync();
-    if (valid && (peers & lanemask_lt()) == 0) mywc[ev[i]] = c + __popcll(peers);
-    wave_sync();
+    lr[i] = wave_rank(ev[i], valid, p.nbits, mywc);
   }
   bad = __syncthreads_or(bad);
   // publish the chunk's counts; wc becomes each wave's offset in the chunk

@@ -17,29 +17,49 @@ __device__ inline int lane_id() { return threadIdx.x & 63; }
 
 __device__ inline uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
 
-// Lanes of this wave holding the same (valid) value: one ballot per id bit.
-// A lane differs from lane x where some bit of x's value, as read from that
-// bit's ballot, differs from its own; the differences accumulate in one
-// three-input bit operation per mask half (v_bitop3 on gfx950).
-__device__ inline uint64_t peer_mask(int v, bool valid, int nbits) {
-  const uint64_t vm = __ballot(valid);
-  uint32_t dlo = 0, dhi = 0;
-#pragma unroll
-  for (int b = 0; b < 31; ++b) {
-    if (b >= nbits) break;
-    const int sb = (v << (31 - b)) >> 31;   // bit b as 0 or all ones
-    const uint64_t on = __ballot(sb != 0);
-    dlo |= (uint32_t)on ^ (uint32_t)sb;
-    dhi |= (uint32_t)(on >> 32) ^ (uint32_t)sb;
-  }
-  return vm & ~(((uint64_t)dhi << 32) | dlo);
-}
-
 // Order LDS traffic of the lanes of one wave (the refinement runs on one
 // wave and needs no workgroup barrier).
 __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
+}
+
+// Lanes of this wave holding the same value as this lane, among the lanes
+// where valid holds: one ballot per value bit (nbits low bits).  The mask
+// starts as the valid lanes and, per bit, keeps the lanes whose bit (read
+// from that bit's ballot) equals this lane's: a bit-field extract, the
+// ballot's compare and one three-input bit operation per mask half
+// (v_bitop3 on gfx950).
+__device__ inline uint64_t peer_mask(int v, bool valid, int nbits) {
+  const uint64_t vm = __ballot(valid);
+  uint32_t elo = (uint32_t)vm, ehi = (uint32_t)(vm >> 32);
+  for (int b = 0; b < nbits; ++b) {
+    const int sb = __builtin_amdgcn_sbfe(v, b, 1);   // bit b as 0 or all ones
+    const uint64_t on = __ballot(sb != 0);
+    elo &= ~((uint32_t)on ^ (uint32_t)sb);
+    ehi &= ~((uint32_t)(on >> 32) ^ (uint32_t)sb);
+  }
+  return ((uint64_t)ehi << 32) | elo;
+}
+
+// c plus the number of lanes below this one in mask (v_mbcnt).
+__device__ inline int count_below(uint64_t mask, int c) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, (uint32_t)c));
+}
+
+// Stable rank of this lane's value v among the wave's lanes: counts[v] (the
+// wave's earlier occurrences of v, its own LDS row) plus the lanes below
+// holding v; counts[v] then grows by the lanes holding v.  Every lane of a
+// group stores the same new count, so no lane needs to be picked to store
+// it.  Invalid lanes take no part (their result means nothing).
+__device__ inline int wave_rank(int v, bool valid, int nbits, int *counts) {
+  const uint64_t peers = peer_mask(v, valid, nbits);
+  const int c = valid ? counts[v] : 0;
+  const int r = count_below(peers, c);
+  wave_sync();
+  if (valid) counts[v] = c + __popc((uint32_t)peers) + __popc((uint32_t)(peers >> 32));
+  wave_sync();
+  return r;
 }
 
 // Workgroup barrier that orders LDS only: it does not wait for outstanding
