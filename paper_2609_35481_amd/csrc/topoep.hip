@@ -38,6 +38,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <climits>
 #include <mutex>
 #include <vector>
 
@@ -2591,13 +2592,14 @@ __device__ void slot_before(const Plan &p, const int *run, const int *ptr, const
   lds_barrier();
 }
 
-// Per-wave counts to offsets, one column per key: wc[w * ws + k] (w < nw <=
-// 16 waves, k < n keys, ws > n odd so a column's words sit in distinct
-// banks) becomes base[k] + the counts of waves 0..w-1, and base[k] grows by
-// the column's total (base may be null: offsets from 0).  Beyond four waves
-// a group of g lanes (g = nw rounded up to a power of two) per key scans
-// the column in registers instead of walking it with nw dependent LDS
-// round trips.
+// Per-wave counts to offsets, one column per key: wc[(w * ws + k) * S] (w <
+// nw <= 16 waves, k < n keys, ws > n odd so a column's words sit in distinct
+// banks; S: words per element) becomes base[k] + the counts of waves
+// 0..w-1, and base[k] grows by the column's total (base may be null:
+// offsets from 0).  Beyond four waves a group of g lanes (g = nw rounded up
+// to a power of two) per key scans the column in registers instead of
+// walking it with nw dependent LDS round trips.
+template <int S = 1>
 __device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *base) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63;
   if (nw <= 4) {
@@ -2605,8 +2607,8 @@ __device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *ba
     for (int k = tid; k < n; k += nt) {
       int run = base ? base[k] : 0;
       for (int w = 0; w < nw; ++w) {
-        const int t = wc[w * ws + k];
-        wc[w * ws + k] = run;
+        const int t = wc[(w * ws + k) * S];
+        wc[(w * ws + k) * S] = run;
         run += t;
       }
       if (base) base[k] = run;
@@ -2616,7 +2618,7 @@ __device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *ba
   const int lg = nw <= 1 ? 0 : 32 - __clz(nw - 1);   // log2 of the group size
   const int g = 1 << lg, w = lane & (g - 1);
   for (int k = tid >> lg; k < n; k += nt >> lg) {
-    const int v = w < nw ? wc[w * ws + k] : 0;
+    const int v = w < nw ? wc[(w * ws + k) * S] : 0;
     int x = v;
     // inclusive scan inside the group (row shifts; a group never crosses a row)
     int y;
@@ -2626,7 +2628,7 @@ __device__ inline void scan_wave_columns(int *wc, int ws, int n, int nw, int *ba
     y = (int)dpp_mov<0x118>((uint32_t)x); x += w >= 8 ? y : 0;
     const int tot = __shfl(x, lane | (g - 1));
     const int b0 = base ? base[k] : 0;
-    if (w < nw) wc[w * ws + k] = b0 + x - v;
+    if (w < nw) wc[(w * ws + k) * S] = b0 + x - v;
     if (base && w == 0) base[k] = b0 + tot;
   }
 }
@@ -2667,11 +2669,11 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   extern __shared__ int smem_r[];
   const int nt = blockDim.x, nw = nt >> 6;
   const int E = p.E, ws = E | 1;
-  int2 *ent = reinterpret_cast<int2 *>(smem_r);   // nent_cap: (cumulative share, rank) per entry
-  int2 *cur = ent + p.nent_cap;      // E: (entry holding the next occurrence, end of e's entries)
-  int *run = reinterpret_cast<int *>(cur + E);   // E: running offset per expert
-  int *wc = run + E;                 // nw * ws: per-wave counts, then offsets
-  int *ptr = wc + nw * ws;           // E + 1
+  int2 *ent = reinterpret_cast<int2 *>(smem_r);   // nent_cap + 1: (cumulative share, rank) per entry
+  int2 *cur = ent + p.nent_cap + 1;  // E: (entry holding the next occurrence, end of e's entries)
+  int2 *wc = cur + E;                // nw * ws: per wave and expert the count, then (offset, entry)
+  int *run = reinterpret_cast<int *>(wc + nw * ws);   // E: running offset per expert
+  int *ptr = run + E;                // E + 1
   int *wcd = ptr + E + 1;            // nw * (R | 1): send-buffer slots: per-wave counts
   int *excl = wcd + nw * (p.R | 1);  // R: assignments per rank before the tile
   int *so = excl + p.R;              // R + 1 + nw + 1: send offsets, scan scratch
@@ -2713,9 +2715,25 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
   __syncthreads();
   const int nent = ptr[E];
   for (int j = tid; j < nent; j += nt) ent[j] = make_int2(p.csr_end[j], p.csr_r[j]);
-  for (int e = tid; e < E; e += nt) cur[e] = make_int2(ptr[e], ptr[e + 1]);
+  // past the last entry: a sentinel no occurrence lies below
+  if (tid == 0) ent[p.nent_cap] = make_int2(INT_MIN, -1);
   __syncthreads();
-  int *mywc = wc + wave * ws;
+  // run[e] counts e's occurrences before the chunk: each expert's cursor
+  // starts at the entry holding occurrence run[e], the first of [ptr[e],
+  // ptr[e + 1]) whose cumulative share exceeds it (shares ascend: a binary
+  // search); each tile moves it on past its own occurrences.  (The thread
+  // that sets a cursor is the one that walks it below: no barrier.)
+  for (int e = tid; e < E; e += nt) {
+    const int re = run[e], j1 = ptr[e + 1];
+    int lo2 = ptr[e], hi2 = j1;
+    while (lo2 < hi2) {
+      const int mid = (lo2 + hi2) >> 1;
+      if (ent[mid].x <= re) lo2 = mid + 1;
+      else hi2 = mid;
+    }
+    cur[e] = make_int2(lo2, j1);
+  }
+  int2 *mywc = wc + wave * ws;
   for (int64_t base = lo; base < hi; base += tile) {
     int ev[IPT];
 #pragma unroll
@@ -2723,55 +2741,87 @@ __global__ __launch_bounds__(1024) void reroute_kernel(Plan p) {
     // the next tile's ids load while this one is ranked (the barriers below
     // order LDS only, so they do not wait for these loads)
     if (base + tile < hi) load_tile(base + tile);
-    // run[e] counts e's occurrences before this tile: each expert's cursor
-    // moves to the entry holding occurrence run[e]
-    for (int e = tid; e < E; e += nt) {
-      // first entry of [c.x, c.y) whose cumulative share exceeds run[e]
-      // (shares ascend): a binary search
-      int2 c = cur[e];
-      const int re = run[e];
-      int lo2 = c.x, hi2 = c.y;
-      while (lo2 < hi2) {
-        const int mid = (lo2 + hi2) >> 1;
-        if (ent[mid].x <= re) lo2 = mid + 1;
-        else hi2 = mid;
-      }
-      if (lo2 != c.x) cur[e] = make_int2(lo2, c.y);
-    }
     if (p.slot_out) slot_before(p, run, ptr, ent, excl);
-    for (int e = lane; e < E; e += 64) mywc[e] = 0;
+    for (int e = lane; e < E; e += 64) mywc[e].x = 0;
     wave_sync();
     const int64_t wbase = base + (int64_t)wave * 64 * IPT + lane;
+    // ids of this lane left in the chunk (the stores' bound)
+    const int lim = (int)(hi - wbase < 64 * IPT ? hi - wbase : 64 * IPT);
     int lr[IPT];
 #pragma unroll
-    for (int i = 0; i < IPT; ++i) {
-      // (ev is -1 past the end)
-      lr[i] = wave_rank(ev[i], (unsigned)ev[i] < (unsigned)E, p.nbits, mywc);
-    }
+    for (int i = 0; i < IPT; ++i)   // (ev is -1 past the end)
+      lr[i] = wave_rank<2>(ev[i], (unsigned)ev[i] < (unsigned)E, p.nbits, reinterpret_cast<int *>(mywc));
     lds_barrier();
-    scan_wave_columns(wc, ws, E, nw, run);
+    // each wave's offset of e, and the entry holding that first occurrence
+    // (the sentinel when it lies past e's entries), found from e's cursor
+    // (offsets grow with the wave), which then moves past the tile: up to
+    // four waves one thread walks each expert's column once, else the
+    // columns are scanned first
+    // (the current entry's share end stays in a register: LDS is read only
+    // when the walk moves on)
+    auto entry_of = [&](int2 c, int &j, int &ej, int off) {
+      while (j < c.y && ej <= off) {
+        ++j;
+        ej = j < c.y ? ent[j].x : INT_MAX;
+      }
+      return j < c.y ? j : p.nent_cap;
+    };
+    if (nw <= 4) {
+      for (int e = tid; e < E; e += nt) {
+        const int2 c = cur[e];
+        int j = c.x, r = run[e];
+        int ej = j < c.y ? ent[j].x : INT_MAX;
+        for (int w = 0; w < nw; ++w) {
+          int2 *x = wc + w * ws + e;
+          const int t = x->x;
+          *x = make_int2(r, entry_of(c, j, ej, r));
+          r += t;
+        }
+        run[e] = r;
+        entry_of(c, j, ej, r);
+        if (j != c.x) cur[e].x = j;
+      }
+    } else {
+      scan_wave_columns<2>(reinterpret_cast<int *>(wc), ws, E, nw, run);
+      lds_barrier();
+      for (int e = tid; e < E; e += nt) {
+        const int2 c = cur[e];
+        int j = c.x;
+        int ej = j < c.y ? ent[j].x : INT_MAX;
+        for (int w = 0; w < nw; ++w) {
+          int2 *x = wc + w * ws + e;
+          x->y = entry_of(c, j, ej, x->x);
+        }
+        entry_of(c, j, ej, run[e]);
+        if (j != c.x) cur[e].x = j;
+      }
+    }
     lds_barrier();
     int dv[IPT];
 #pragma unroll
     for (int i = 0; i < IPT; ++i) {
-      const int64_t idx = wbase + i * 64;
-      int dest = -1;
-      if (idx < hi) {
-        if ((unsigned)ev[i] < (unsigned)E) {
-          // occurrence rho of e: the entry at e's cursor holds it unless the
-          // occurrences of this tile run past that instance's share
-          const int rho = mywc[ev[i]] + lr[i];
-          const int2 c = cur[ev[i]];
-          for (int j = c.x; j < c.y; ++j) {
-            const int2 en = ent[j];
-            if (rho < en.x) {
-              dest = en.y;
-              break;
-            }
+      // occurrence rho of e: the entry of the wave's first occurrence holds
+      // it unless the wave's occurrences run past that instance's share
+      // (then the entries after it, or none past e's last)
+      const int e = ev[i];
+      const bool valid = (unsigned)e < (unsigned)E;
+      const int2 r = mywc[valid ? e : 0];
+      const int rho = r.x + lr[i];
+      const int2 en = ent[r.y];
+      const bool hit = rho < en.x;
+      int dest = valid && hit ? en.y : -1;
+      const bool slow = valid && !hit;
+      if (slow) {   // (skipped when no lane of the wave needs it)
+        const int j1 = ptr[e + 1];
+        for (int j = r.y + 1; j < j1; ++j) {
+          const int2 en2 = ent[j];
+          if (rho < en2.x) {
+            dest = en2.y;
+            break;
           }
         }
-        p.dest_out[idx] = dest;
       }
+      if (i * 64 < lim) p.dest_out[wbase + i * 64] = dest;
       dv[i] = dest;
     }
     if (p.slot_out) slot_write<IPT>(p, dv, wbase, hi, so, excl, wcd);
@@ -3593,8 +3643,10 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     return TOPOEP_ELIMIT;
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
-  s.lds_reroute = (2 * (size_t)q.nent_cap + 2 * (size_t)E + 2 * (size_t)E + (size_t)(E | 1) * (s.bt / 64) + 1 +
-                   (size_t)(R | 1) * (s.bt / 64) + 2 * (size_t)R + 1 + s.bt / 64 + 1) * 4;
+  // instance entries, cursors, per-wave (count, entry) pairs, run, ptr,
+  // per-wave rank counts, counts before the tile, send offsets and scratch
+  s.lds_reroute = (2 * ((size_t)q.nent_cap + 1) + 2 * (size_t)E + 2 * (size_t)(E | 1) * (s.bt / 64) + (size_t)E +
+                   (size_t)E + 1 + (size_t)(R | 1) * (s.bt / 64) + (size_t)R + (size_t)R + 1 + s.bt / 64 + 1) * 4;
   s.lds_fused = 0;
   if (s.lds_reroute > (size_t)kLdsLimit) return TOPOEP_ELIMIT;
   }

@@ -52,12 +52,14 @@ __device__ inline int count_below(uint64_t mask, int c) {
 // holding v; counts[v] then grows by the lanes holding v.  Every lane of a
 // group stores the same new count, so no lane needs to be picked to store
 // it.  Invalid lanes take no part (their result means nothing).
+// (S: the counts lie S words apart.)
+template <int S = 1>
 __device__ inline int wave_rank(int v, bool valid, int nbits, int *counts) {
   const uint64_t peers = peer_mask(v, valid, nbits);
-  const int c = valid ? counts[v] : 0;
+  const int c = valid ? counts[v * S] : 0;
   const int r = count_below(peers, c);
   wave_sync();
-  if (valid) counts[v] = c + __popc((uint32_t)peers) + __popc((uint32_t)(peers >> 32));
+  if (valid) counts[v * S] = c + __popc((uint32_t)peers) + __popc((uint32_t)(peers >> 32));
   wave_sync();
   return r;
 }
