@@ -9,9 +9,11 @@
 //   - a one-tile workgroup holds its assignments in registers and ranks
 //     them among equal destinations inside each wave (ballots over the
 //     destination bits give each lane its peers), then scans the per-wave
-//     counts across waves in LDS; a longer chunk only counts its
-//     destinations here (LDS atomics) and ranks tile by tile after the
-//     look-back, reading the assignments again;
+//     counts across waves in LDS; a longer chunk is cut into one contiguous
+//     part per wave, each wave only counts its part's destinations here
+//     (LDS atomics), and after the look-back ranks its part step by step
+//     from its own running base, reading the assignments again, with no
+//     workgroup barrier;
 //   - it publishes its per-destination counts (flag 1), then looks back
 //     over up to 64 predecessors at a time: wave 0 waits for their flags in
 //     parallel and stops at the nearest one whose inclusive prefix is
@@ -19,8 +21,9 @@
 //     destination, and (when the grid is longer than one window plus
 //     workgroup 0) the workgroup publishes its own inclusive prefix (flag
 //     2).  Workgroup 0 publishes its counts as its inclusive prefix;
-//   - slot = send_offsets[dest] + (earlier workgroups) + (earlier tiles of
-//     the chunk) + (earlier waves) + (rank in the wave).
+//   - slot = send_offsets[dest] + (earlier workgroups) + (earlier waves, or
+//     their parts) + (earlier steps of the wave's part) + (rank in the
+//     wave).
 // The waits are bounded and only on lower workgroup indices, which are
 // dispatched first.  The last workgroup to finish its look-back (a ticket)
 // clears every flag, so the workspace is zero again for the next call.
@@ -57,13 +60,18 @@ struct Layout {
   uint32_t spin_limit;
 };
 
-// LDS words: per-wave counts (then offsets) [nw][R], the workgroup's counts
-// [R], the exclusive prefix over earlier workgroups [R], send offsets
-// [R + 1], the running slot base of a multi-tile chunk [R] and broadcast
-// words.
+// LDS words: per-wave counts (then offsets, then a long chunk's running
+// slot bases) [nw][R], the workgroup's counts [R], the exclusive prefix over
+// earlier workgroups [R], send offsets [R + 1], broadcast words, and the
+// counting copies of a long chunk's first pass [nw][C][R] (C > 1).
 struct LayoutLds {
-  int wc, agg, excl, offs, run, misc, words;
+  int wc, agg, excl, offs, misc, cnt, words;
 };
+
+// Copies of each wave's counts in the first pass of a long chunk: lane l
+// counts into copy l % C, so equal destinations of one wave instruction
+// meet fewer times on one LDS word (at most 64 KB of copies).
+__host__ __device__ inline int layout_copies(int R) { return R <= 256 ? 4 : (R <= 512 ? 2 : 1); }
 
 __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
   LayoutLds l;
@@ -72,8 +80,8 @@ __host__ __device__ inline LayoutLds layout_lds(int R, int nt) {
   l.agg = o; o += R;
   l.excl = o; o += R;
   l.offs = o; o += R + 1;
-  l.run = o; o += R;
   l.misc = o; o += 8;
+  l.cnt = o; o += layout_copies(R) > 1 ? (nt / 64) * layout_copies(R) * R : 0;
   l.words = o;
   return l;
 }
@@ -112,7 +120,7 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
   const int R = L.R, tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int b = blockIdx.x;
   const LayoutLds l = layout_lds(R, nt);
-  int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs, *run = lsm + l.run;
+  int *wc = lsm + l.wc, *agg = lsm + l.agg, *excl = lsm + l.excl, *offs = lsm + l.offs;
   int *misc = lsm + l.misc;
   const int64_t lo = (int64_t)b * L.chunk;
   const int64_t hi = lo + L.chunk < L.n ? lo + L.chunk : L.n;
@@ -122,6 +130,17 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
   // after the look-back (pass 2), reading the ids twice
   const bool multi = L.chunk > tile;
   const int64_t wofs = (int64_t)wave * 64 * IPT + lane;
+  // a longer chunk: wave w owns the w-th of nw equal contiguous parts, in
+  // steps of 64 IPT ids (the chunk is a whole number of tiles)
+  const int64_t step = 64 * IPT, sub = L.chunk / nw;
+  const int64_t wlo = lo + wave * sub, whi = wlo + sub < hi ? wlo + sub : hi;
+  auto load_step = [&](int (&v)[IPT], int64_t base) {
+#pragma unroll
+    for (int i = 0; i < IPT; ++i) {
+      const int64_t idx = base + lane + i * 64;
+      v[i] = idx < whi ? L.dest[idx] : -1;
+    }
+  };
   // workgroups whose look-back window reaches workgroup 0 never need the
   // inclusive prefix of another one
   const bool publish_incl = L.nb > kLayoutWindow + 1;
@@ -141,19 +160,57 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
     }
     rank_wave<IPT>(R, L.nbits, dv, lr, mywc);
   } else {
-    // pass 1: the chunk's count of every destination, one LDS atomic per
-    // assignment into the wave's own row
-    for (int r = lane; r < R; r += 64) mywc[r] = 0;
+    // pass 1: each wave's count of every destination over its own part of
+    // the chunk, one LDS atomic per assignment into the lane's copy of the
+    // wave's counts (the order of the counting does not matter: a lane
+    // loads four consecutive ids at once; the next step's loads are in
+    // flight meanwhile), then the copies summed into the wave's row
+    const int C = layout_copies(R);
+    int *rows = C > 1 ? lsm + l.cnt + wave * C * R : mywc;
+    for (int r = lane; r < C * R; r += 64) rows[r] = 0;
     wave_sync();
-    for (int64_t base = lo; base < hi; base += tile) {
+    int *myc = rows + (lane & (C - 1)) * R;
+    // V loads of four ids per lane and step (256 V ids; parts start on
+    // multiples of 64 ids, so a 16-byte aligned array keeps them aligned)
+    constexpr int V = IPT >= 4 ? IPT / 4 : 1;
+    const int64_t step1 = 256 * V;
+    const bool vec = (reinterpret_cast<uintptr_t>(L.dest) & 15) == 0;
+    auto load4 = [&](int4 (&v)[V], int64_t base) {
 #pragma unroll
-      for (int i = 0; i < IPT; ++i) {
-        const int64_t idx = base + wofs + i * 64;
-        dv[i] = idx < hi ? L.dest[idx] : -1;
+      for (int j = 0; j < V; ++j) {
+        const int64_t idx = base + (int64_t)(j * 64 + lane) * 4;
+        if (vec && idx + 4 <= whi) {
+          v[j] = *reinterpret_cast<const int4 *>(L.dest + idx);
+        } else {
+          v[j].x = idx < whi ? L.dest[idx] : -1;
+          v[j].y = idx + 1 < whi ? L.dest[idx + 1] : -1;
+          v[j].z = idx + 2 < whi ? L.dest[idx + 2] : -1;
+          v[j].w = idx + 3 < whi ? L.dest[idx + 3] : -1;
+        }
       }
+    };
+    int4 nx[V];
+    load4(nx, wlo);
+    for (int64_t base = wlo; base < whi; base += step1) {
+      int4 cv[V];
 #pragma unroll
-      for (int i = 0; i < IPT; ++i)
-        if ((unsigned)dv[i] < (unsigned)R) atomicAdd(&mywc[dv[i]], 1);
+      for (int j = 0; j < V; ++j) cv[j] = nx[j];
+      if (base + step1 < whi) load4(nx, base + step1);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        if ((unsigned)cv[j].x < (unsigned)R) atomicAdd(&myc[cv[j].x], 1);
+        if ((unsigned)cv[j].y < (unsigned)R) atomicAdd(&myc[cv[j].y], 1);
+        if ((unsigned)cv[j].z < (unsigned)R) atomicAdd(&myc[cv[j].z], 1);
+        if ((unsigned)cv[j].w < (unsigned)R) atomicAdd(&myc[cv[j].w], 1);
+      }
+    }
+    if (C > 1) {
+      wave_sync();
+      for (int r = lane; r < R; r += 64) {
+        int sum = 0;
+        for (int c = 0; c < C; ++c) sum += rows[c * R + r];
+        mywc[r] = sum;
+      }
     }
   }
   lds_barrier();
@@ -249,30 +306,26 @@ __global__ __launch_bounds__(kLayoutThreads) void layout_kernel(Layout L) {
       }
     }
   } else {
-    // pass 2: tile by tile, slot = base of the destination before the tile
-    // + offset of the wave + rank in the wave
-    for (int r = tid; r < R; r += nt) run[r] = offs[r] + excl[r];
-    for (int64_t base = lo; base < hi; base += tile) {
+    // pass 2: the wave's row becomes its first slot per destination (send
+    // offset + earlier workgroups + earlier waves), and each step's slots
+    // are that running base plus the rank in the wave, which the rank
+    // advances: no workgroup barrier
+    for (int r = lane; r < R; r += 64) mywc[r] += offs[r] + excl[r];
+    wave_sync();
+    int nx[IPT];
+    load_step(nx, wlo);
+    for (int64_t base = wlo; base < whi; base += step) {
+#pragma unroll
+      for (int i = 0; i < IPT; ++i) dv[i] = nx[i];
+      if (base + step < whi) load_step(nx, base + step);
 #pragma unroll
       for (int i = 0; i < IPT; ++i) {
-        const int64_t idx = base + wofs + i * 64;
-        dv[i] = idx < hi ? L.dest[idx] : -1;
+        const int d = dv[i];
+        const bool valid = (unsigned)d < (unsigned)R;
+        const int slot = wave_rank(d, valid, L.nbits, mywc);
+        const int64_t idx = base + lane + i * 64;
+        if (idx < whi) L.slot_out[idx] = ok && valid ? slot : -1;
       }
-      rank_wave<IPT>(R, L.nbits, dv, lr, mywc);
-      lds_barrier();
-      scan_waves(R, nw, wc, agg);
-      lds_barrier();
-#pragma unroll
-      for (int i = 0; i < IPT; ++i) {
-        const int64_t idx = base + wofs + i * 64;
-        if (idx < hi) {
-          const int d = dv[i];
-          const bool valid = ok && (unsigned)d < (unsigned)R;
-          L.slot_out[idx] = valid ? run[d] + mywc[d] + lr[i] : -1;
-        }
-      }
-      lds_barrier();
-      for (int r = tid; r < R; r += nt) run[r] += agg[r];
     }
   }
   // this workgroup has read every flag it needs: the last one to get here

@@ -191,6 +191,28 @@ def test_layout_alone(R, n, invalid, skew):
     assert np.array_equal(slot, ref_slot)
 
 
+def test_layout_unaligned_destinations():
+    """Destinations that start 4 bytes past a 16-byte boundary, long chunks:
+    the first pass loads them one by one instead of four at a time."""
+    R, n = 32, 5000000
+    say("layout unaligned R=%d n=%d" % (R, n))
+    rng = np.random.default_rng(4242)
+    dest, send = layout_case(R, n, rng, skew=1.0)
+    T, k = dest.shape
+    big = torch.zeros(T * k + 1, dtype=torch.int32, device=DEV)
+    big[1:] = torch.from_numpy(dest.ravel()).to(DEV)
+    d = big[1:].view(T, k)
+    assert d.data_ptr() % 16 != 0
+    topo = topoep.topology(R, 1, R, 0, 1, 1, 1, 0)
+    p = topoep.LayoutPlanner(topo, T, k, device=DEV)
+    offs, slot = p.layout(d, torch.from_numpy(send).to(DEV))
+    torch.cuda.synchronize()
+    assert int(p.status[0].item()) == 0
+    ref_offs, ref_slot = oracle.layout_ref(R, dest, send)
+    assert np.array_equal(offs.cpu().numpy(), ref_offs)
+    assert np.array_equal(slot.cpu().numpy(), ref_slot)
+
+
 def test_layout_empty_batch():
     offs, slot, _ = layout_gpu(4, np.zeros((0, 2), np.int32), np.zeros(4, np.int32))
     assert offs.tolist() == [0, 0, 0, 0, 0] and slot.shape == (0, 2)
