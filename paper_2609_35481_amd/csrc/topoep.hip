@@ -121,10 +121,12 @@ struct Plan {
   uint32_t *ctrl;
   int32_t *partials, *offsets, *blk_err, *repl1, *seg_e, *seg_q, *csr_ptr, *csr_r, *csr_end;
   int32_t *htot;   // three-kernel plan: each expert's count over the histogram blocks [E]
-  // one-launch plan: each chunk's per-expert counts [nb][E], the histogram
-  // of the ids with a bad-id count [2][E + 1] (one buffer per generation
-  // parity), one flag line per chunk (kFlagStride words apart)
-  uint32_t *pub, *ghist, *flags;
+  // one-launch plan: each chunk's per-expert counts [nb][E] (16 bits: a
+  // chunk holds at most 1024 x 8 ids), the histogram of the ids with a
+  // bad-id count [2][E + 1] (one buffer per generation parity), one flag
+  // line per chunk (kFlagStride words apart)
+  uint16_t *pub;
+  uint32_t *ghist, *flags;
 };
 
 
@@ -3158,7 +3160,7 @@ __device__ __forceinline__ void chunk_offsets(const Plan &p, int b, const uint32
     for (int j0 = 0; j0 < n; j0 += 8) {
       uint32_t w[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) w[u] = p.pub[(int64_t)(b0 + imin(j0 + u, n - 1)) * E + e];
+      for (int u = 0; u < 8; ++u) w[u] = p.pub[(int64_t)(b0 + imin(j0 + u, n - 1)) * E + e];   // (16-bit loads)
 #pragma unroll
       for (int u = 0; u < 8; ++u) sum += j0 + u < n ? (int)w[u] : 0;
     }
@@ -3275,7 +3277,7 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
       wc[w * E + e] = sum;
       sum += c;
     }
-    p.pub[(int64_t)b * E + e] = (uint32_t)sum;
+    p.pub[(int64_t)b * E + e] = (uint16_t)sum;
     if (sum) atomicAdd(gh + e, (uint32_t)sum);
   }
   if (tid == 0 && bad) atomicAdd(gh + E, 1u);
@@ -3686,7 +3688,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   const size_t o_cr = take((size_t)q.nent_cap * 4);
   const size_t o_ce = take((size_t)q.nent_cap * 4);
   const size_t o_ht = take(three ? (size_t)E * 4 : 0);
-  const size_t o_pub = take(one ? (size_t)q.nb * E * 4 : 0);
+  const size_t o_pub = take(one ? (size_t)q.nb * E * 2 : 0);
   *ws_bytes = off;
   if (ws) {
     auto at = [&](size_t o, bool have) { return have ? reinterpret_cast<int32_t *>(ws + o) : nullptr; };
@@ -3703,7 +3705,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     q.csr_end = at(o_ce, true);
     q.htot = at(o_ht, three);
     q.flags = atu(o_flg, one);
-    q.pub = atu(o_pub, one);
+    q.pub = one ? reinterpret_cast<uint16_t *>(ws + o_pub) : nullptr;
     q.ghist = atu(o_gh, one);
   }
   *p = q;
