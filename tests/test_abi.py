@@ -107,8 +107,9 @@ def test_plan_shape_choices(tp):
     workgroups; three kernels otherwise (host-side choice only)."""
     t = tp.topology(32, 8, 256, 0, 1, 8, 14336, 88080384)
     sh = tp.plan_shape(t, 8192, 8, 2)
-    assert sh.kernels == 1 and sh.solver == tp.SOLVER_FUSED and sh.chunk_blocks == 64
-    assert sh.grid[0] == 65 and sh.block[0] == 1024 and sh.items_per_thread == 1
+    # the fewest ids per thread that keep to 32 chunks: two
+    assert sh.kernels == 1 and sh.solver == tp.SOLVER_FUSED and sh.chunk_blocks == 32
+    assert sh.grid[0] == 33 and sh.block[0] == 1024 and sh.items_per_thread == 2
     sh = tp.plan_shape(t, 8192, 8, 2, launch=(4, 0, 0, 0, 3))
     assert sh.chunk_blocks == 16 and sh.items_per_thread == 4
     # 512 threads, 8 ids each: 16 chunks
