@@ -304,7 +304,7 @@ __host__ __device__ inline SingleLds single_lds(const Plan &p) {
 
 // LDS layout of a chunk workgroup of the single-launch plan (nt threads).
 struct ChunkLds {
-  int wc, run, ptr, er, eend, gs, so, flag, words;
+  int wc, run, ptr, ent, gs, so, flag, words;
 };
 
 __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
@@ -313,8 +313,8 @@ __host__ __device__ inline ChunkLds chunk_lds(const Plan &p, int nt) {
   l.wc = o;   o += (nt >> 6) * p.E;          // per-wave counts, then offsets in the block
   l.run = o;  o += p.E;                      // offset of the block per expert
   l.ptr = o;  o += p.E + 1;                  // instance list: first entry per expert
-  l.er = o;   o += p.nent_cap;               //   instance rank
-  l.eend = o; o += p.nent_cap;               //   cumulative share
+  o = (o + 1) & ~1;
+  l.ent = o;  o += 2 * p.nent_cap;           //   (cumulative share, instance rank) per entry
   l.gs = o;   o += imax(nt, p.E);            // partial sums of the chunk's offsets, then counts per rank
   l.so = o;   o += p.R + 1 + (nt >> 6) + 1;  // send offsets and their scan scratch
   l.flag = o; o += 4;
@@ -3187,7 +3187,7 @@ __device__ __forceinline__ void chunk_offsets(const Plan &p, int b, const uint32
 // send offsets.
 template <int IPT>
 __device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT], int64_t wbase, int64_t hi,
-                                            const int *run, const int *ptr, const int *er, const int *eend,
+                                            const int *run, const int *ptr, const int2 *ent,
                                             const int *offs, int *excl, int *wc) {
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int R = p.R, E = p.E;
@@ -3195,9 +3195,9 @@ __device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT],
     const int re = run[e], j1 = ptr[e + 1];
     int start = 0;
     for (int j = ptr[e]; j < j1; ++j) {
-      const int end = eend[j];
+      const int end = ent[j].x, rk = ent[j].y;
       const int c = imin(imax(re - start, 0), end - start);
-      if (c > 0 && (unsigned)er[j] < (unsigned)R) atomicAdd(&excl[er[j]], c);
+      if (c > 0 && (unsigned)rk < (unsigned)R) atomicAdd(&excl[rk], c);
       start = end;
     }
   }
@@ -3244,7 +3244,8 @@ __device__ __forceinline__ void chunk_slots(const Plan &p, const int (&dv)[IPT],
 template <int IPT>
 __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   const ChunkLds l = chunk_lds(p, blockDim.x);
-  int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr, *er = sm + l.er, *eend = sm + l.eend;
+  int *wc = sm + l.wc, *run = sm + l.run, *ptr = sm + l.ptr;
+  int2 *ent = reinterpret_cast<int2 *>(sm + l.ent);
   int *gs = sm + l.gs, *so = sm + l.so, *flag = sm + l.flag;
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, lane = tid & 63, wave = tid >> 6;
   const int E = p.E;
@@ -3319,6 +3320,15 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
   bool ok = wait_flag(p, b, 1, gen + 1u, flag);
   if (ok) chunk_offsets(p, b, p.ghist + (gen & 1u) * (E + 1), run, gs);
   if (b == 0) STAMP(p, 16);
+  // each id's occurrence index rho = chunk offset + wave offset + rank in
+  // the wave, while the plan is still being made
+  __syncthreads();
+  int rho[IPT];
+#pragma unroll
+  for (int i = 0; i < IPT; ++i) {
+    const int e = (unsigned)ev[i] < (unsigned)E ? ev[i] : 0;
+    rho[i] = run[e] + wc[wave * E + e] + lr[i];
+  }
   // the plan is ready
   ok = ok && wait_flag(p, b, 0, gen + 1u, flag);
   if (b == 0) STAMP(p, 14);
@@ -3333,10 +3343,7 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
       const int rv = p.csr_r[imin(i, p.nent_cap - 1)];
       const int xv = p.csr_end[imin(i, p.nent_cap - 1)];
       if (i <= E) ptr[i] = pv < 0 ? 0 : (pv > p.nent_cap ? p.nent_cap : pv);
-      if (i < p.nent_cap) {
-        er[i] = rv;
-        eend[i] = xv;
-      }
+      if (i < p.nent_cap) ent[i] = make_int2(xv, rv);
     }
     if (p.slot_out) {
       // the send offsets (the solver wrote them) in the same round trip;
@@ -3369,11 +3376,11 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
     int dest = -1;
     if (idx < hi) {
       if ((unsigned)ev[i] < (unsigned)E) {
-        const int rho = run[ev[i]] + wc[wave * E + ev[i]] + lr[i];
         const int j1 = ptr[ev[i] + 1];
         for (int j = ptr[ev[i]]; j < j1; ++j) {
-          if (rho < eend[j]) {
-            dest = er[j];
+          const int2 en = ent[j];
+          if (rho[i] < en.x) {
+            dest = en.y;
             break;
           }
         }
@@ -3382,7 +3389,7 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
     }
     dv[i] = dest;
   }
-  if (p.slot_out) chunk_slots<IPT>(p, dv, wbase, hi, run, ptr, er, eend, so, gs, wc);
+  if (p.slot_out) chunk_slots<IPT>(p, dv, wbase, hi, run, ptr, ent, so, gs, wc);
   if (b == 0) {
     STAMP(p, 15);
     STAMP_FLUSH(p, 12, 13);
