@@ -307,7 +307,8 @@ def time_stage(torch, planners, dev_inputs, stage, reps):
 # slots from chunk 0 except "last arrival done" (the last chunk).
 PHASE_SLOTS = [(0, "solver start"), (1, "Omega in LDS"), (23, "plan start"), (22, "stage 1 candidates"),
                (2, "stage 1"), (3, "setup"), (4, "routing"), (5, "refinement"), (6, "outputs"),
-               (7, "instance list"), (8, "speculative plan"), (9, "verdict seen"), (10, "outputs drained"),
+               (7, "instance list"), (10, "flags released"), (8, "speculative plan returned"),
+               (9, "verdict handled"),
                (12, "chunk 0 arrived"), (19, "last arrival start"), (13, "last arrival done"),
                (16, "chunk 0 offsets"), (14, "chunk 0 sees flag"), (15, "chunk 0 done"),
                (24, "s1: candidates"), (26, "s1: ranks"), (27, "ff: lists and hosting"), (28, "ff: counts"), (30, "ff: entries")]
