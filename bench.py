@@ -444,7 +444,10 @@ def measure(torch, topoep, cfg, N, inputs, steps, warmup, stage_reps, launch=Non
     avg_us = stages[dom]
     achieved = nbytes[dom] / (avg_us * 1e-6) / 1e9
     roof = {"bound": "hbm", "kernel": dom + "_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(cfg.name, dom),
+            "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            # (the counters were taken at the workload's own slot count and
+            # the library's launch shape only)
+            "traffic": measured_traffic(cfg.name, dom) if N == cfg.N and launch is None else None,
             "algorithmic_bytes_per_launch": nbytes[dom], "kernel_own_bytes_per_launch": own[dom],
             "frac_kernel_own_bytes": own[dom] / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, "avg_kernel_us": avg_us,
             "floor_ratio": avg_us / (floor_us / kernels) if floor_us > 0 else None}
