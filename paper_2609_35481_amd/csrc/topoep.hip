@@ -527,13 +527,19 @@ __device__ void load_fast(const Plan &p, int *om, int *hs, int *scratch, int *mi
 // Exclusive per-expert offset of every histogram block, for the reroute
 // (offset workgroup h of n_helpers handles kOffsetExperts experts at a time),
 // and each expert's count over all blocks (htot, the histogram of
-// local_topk), announced by one increment of the helpers' counter.
+// local_topk), announced by one increment of the helpers' counter as soon
+// as the totals are written: the offsets follow in a second pass (only the
+// next launch reads them).  scratch: nw x 64 words per expert group of this
+// workgroup (one group when n_helpers covers E, as the host sets it).
 __device__ void block_offsets(const Plan &p, int h, int *scratch, bool announce) {
   const int tid = threadIdx.x, nt = blockDim.x, nw = nt >> 6, E = p.E, nb = p.nb;
   const int el = tid & 63, g = tid >> 6;
   const int per = (nb + nw - 1) / nw;
   const int b0 = g * per, b1 = imin(nb, b0 + per);
-  for (int e0 = h * kOffsetExperts; e0 < E; e0 += p.n_helpers * kOffsetExperts) {
+  const int gstride = p.n_helpers * kOffsetExperts;
+  // pass 1: each wave's sum over its blocks, per expert of every group
+  int grp = 0;
+  for (int e0 = h * kOffsetExperts; e0 < E; e0 += gstride, ++grp) {
     const int e = e0 + el;
     int run = 0;
     if (e < E) {
@@ -545,30 +551,43 @@ __device__ void block_offsets(const Plan &p, int h, int *scratch, bool announce)
         for (int u = 0; u < 8; ++u) run += v[u];
       }
     }
-    scratch[g * 64 + el] = run;
-    __syncthreads();
+    scratch[(grp * nw + g) * 64 + el] = run;
+  }
+  __syncthreads();
+  // the totals (the expert's count over every block), then the announcement
+  grp = 0;
+  for (int e0 = h * kOffsetExperts; e0 < E; e0 += gstride, ++grp) {
+    const int e = e0 + el;
+    if (g == nw - 1 && e < E) {
+      int tot = 0;
+      for (int g2 = 0; g2 < nw; ++g2) tot += scratch[(grp * nw + g2) * 64 + el];
+      p.htot[e] = tot;
+    }
+  }
+  if (announce) {
+    // publish: every total written before the count of finished helpers
+    // (only the per-domain solver reads it)
+    drain_then_barrier();
+    if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlHelpers], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // pass 2: the blocks' exclusive offsets
+  grp = 0;
+  for (int e0 = h * kOffsetExperts; e0 < E; e0 += gstride, ++grp) {
+    const int e = e0 + el;
+    if (e >= E) continue;
     int base = 0;
-    for (int g2 = 0; g2 < g; ++g2) base += scratch[g2 * 64 + el];
-    if (g == nw - 1 && e < E) p.htot[e] = base + run;   // the expert's count over every block
-    if (e < E) {
-      for (int b = b0; b < b1; b += 8) {
-        int v[8];
+    for (int g2 = 0; g2 < g; ++g2) base += scratch[(grp * nw + g2) * 64 + el];
+    for (int b = b0; b < b1; b += 8) {
+      int v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
+      for (int u = 0; u < 8; ++u) v[u] = b + u < b1 ? p.partials[(int64_t)(b + u) * E + e] : 0;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (b + u < b1) p.offsets[(int64_t)(b + u) * E + e] = base;
-          base += v[u];
-        }
+      for (int u = 0; u < 8; ++u) {
+        if (b + u < b1) p.offsets[(int64_t)(b + u) * E + e] = base;
+        base += v[u];
       }
     }
-    __syncthreads();
   }
-  // publish: every total written before the count of finished helpers
-  // (only the per-domain solver reads it)
-  if (!announce) return;
-  drain_then_barrier();
-  if (tid == 0) __hip_atomic_fetch_add(&p.ctrl[kCtrlHelpers], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // The histogram of local_topk (row self of Omega) for the per-domain
