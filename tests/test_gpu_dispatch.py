@@ -180,6 +180,8 @@ def layout_case(R, n, rng, k=8, invalid=0.0, skew=None):
     (7, 8 * 3, 0.0, None),          # smaller than one wave
     (32, 5000000, 0.01, 1.0),       # 2 tiles per workgroup: counts first, ranks after the look-back
     (256, (1 << 24) + 8 * 13, 0.0, 1.4),   # 5 tiles per workgroup, ragged last tile
+    (512, (1 << 22) + 8 * 5, 0.01, 1.1),   # several tiles, two copies of the counts
+    (1024, (1 << 22) + 8 * 3, 0.0, 0.9),   # several tiles, one copy (the most ranks)
 ])
 def test_layout_alone(R, n, invalid, skew):
     say("layout R=%d n=%d" % (R, n))
