@@ -223,6 +223,24 @@ __device__ inline Plan solver_plan(Plan q) {
   return q;
 }
 
+typedef const __attribute__((address_space(4))) Plan KernargPlan;
+
+// The plan's fields for one role of the one-launch kernel, loaded after the
+// role's branch from an opaque pointer to the kernel arguments: otherwise
+// the compiler loads every field either role uses at the kernel's entry and
+// keeps them all live, and the solver's scalar registers spill.  (The host
+// pass only type-checks this function.)
+__device__ inline Plan role_plan(const Plan &p) {
+#if __HIP_DEVICE_COMPILE__
+  (void)p;
+  KernargPlan *k = (KernargPlan *)(__builtin_amdgcn_kernarg_segment_ptr());
+  asm volatile("" : "+s"(k));
+  return *k;
+#else
+  return p;
+#endif
+}
+
 // Scratch words of the histogram reduction (hist_from_partials, load_fast)
 // for up to 1024 threads: max(E, 4 * threads).
 __host__ __device__ inline int hist_scratch_words(const Plan &p) { return imax(p.E, 4 * 1024); }
@@ -1782,8 +1800,10 @@ __device__ GenCost general_tables(const Plan &p, int d, int *sm, const DomainLds
 // domain's instances, routing (Section 4.3), refinement (Eq. 10) and the
 // domain's outputs follow.  The last solver workgroup to finish (a ticket)
 // lists this rank's instances per expert for the reroute and writes the
-// final status.
-__global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
+// final status.  NT: the most threads per workgroup (launch bounds): the
+// usual 512-thread launch gets twice the registers a 1024-thread one may use.
+template <int NT>
+__global__ __launch_bounds__(NT) void solve_kernel(Plan p0) {
   extern __shared__ int64_t smem_s[];
   int *sm = reinterpret_cast<int *>(smem_s);
   if ((int)blockIdx.x >= p0.n_solvers) {
@@ -1913,6 +1933,10 @@ __global__ __launch_bounds__(1024) void solve_kernel(Plan p0) {
 
   uint32_t flags = 0;
   for (int d = wg; d < M; d += nwg) {
+    // the plan's fields load again in every iteration (see role_plan): the
+    // loop usually runs once, and invariants hoisted out of it would only
+    // crowd the scalar registers
+    const Plan p = solver_plan(role_plan(p0));
     if (noplan) {
       for (int i = tid; i < G * p.N; i += nt) p.slots_out[(int64_t)d * G * p.N + i] = -1;
       for (int j = tid; j < G; j += nt) p.send_out[d * G + j] = 0;
@@ -3419,24 +3443,6 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
 // The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold
 // the ids; all are resident at once (nb <= kMaxFusedBlocks) and every wait
 // is bounded.
-typedef const __attribute__((address_space(4))) Plan KernargPlan;
-
-// The plan's fields for one role of the one-launch kernel, loaded after the
-// role's branch from an opaque pointer to the kernel arguments: otherwise
-// the compiler loads every field either role uses at the kernel's entry and
-// keeps them all live, and the solver's scalar registers spill.  (The host
-// pass only type-checks this function.)
-__device__ inline Plan role_plan(const Plan &p) {
-#if __HIP_DEVICE_COMPILE__
-  (void)p;
-  KernargPlan *k = (KernargPlan *)(__builtin_amdgcn_kernarg_segment_ptr());
-  asm volatile("" : "+s"(k));
-  return *k;
-#else
-  return p;
-#endif
-}
-
 // Reg: the refinement runs in registers (refine_in_registers holds for the
 // shape), else in LDS; one instantiation each keeps the other's registers
 // out.
@@ -3671,7 +3677,9 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   s.lds_solve = (size_t)(s.mode == 1 ? single_words : multi_words) * 4;
   q.n_solvers = s.mode == 1 ? 1 : imin(q.M, kMaxSolveGroups);
   // the per-domain solver's workgroups meet at a grid barrier: all resident
-  if (s.mode == 2 && q.n_solvers > resident_capacity(reinterpret_cast<const void *>(solve_kernel), s.st, s.lds_solve))
+  if (s.mode == 2 && q.n_solvers > resident_capacity(s.st <= 512 ? reinterpret_cast<const void *>(solve_kernel<512>)
+                                                                  : reinterpret_cast<const void *>(solve_kernel<1024>),
+                                                     s.st, s.lds_solve))
     return TOPOEP_ELIMIT;
   s.solve_groups = q.n_solvers + q.n_helpers;
   s.lds_hist = (size_t)E * 4;
@@ -3768,7 +3776,8 @@ void set_attrs() {
   allow_lds(reroute_kernel<2>);
   allow_lds(reroute_kernel<4>);
   allow_lds(reroute_kernel<8>);
-  allow_lds(solve_kernel);
+  allow_lds(solve_kernel<512>);
+  allow_lds(solve_kernel<1024>);
   allow_lds(solve_single_kernel);
   allow_lds(plan_fused_kernel<1, false>);
   allow_lds(plan_fused_kernel<1, true>);
@@ -3806,7 +3815,8 @@ void launch_reroute(const Plan &p, const Shape &s, hipStream_t st) {
 
 void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
   if (s.mode == 1) hipLaunchKernelGGL(solve_single_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
-  else hipLaunchKernelGGL(solve_kernel, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
+  else if (s.st <= 512) hipLaunchKernelGGL(solve_kernel<512>, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
+  else hipLaunchKernelGGL(solve_kernel<1024>, dim3(s.solve_groups), dim3(s.st), s.lds_solve, st, p);
 }
 
 template <int IPT>
