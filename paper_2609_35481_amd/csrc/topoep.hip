@@ -1852,6 +1852,7 @@ __global__ __launch_bounds__(NT) void solve_kernel(Plan p0) {
 
   // ---- inter-node placement (Eq. 9), each domain independently
   for (int d = wg; d < M; d += nwg) {
+    const Plan p = solver_plan(role_plan(p0));   // (reloaded: see the domain loop below)
     copy_to_lds(rows, p.gl + (int64_t)d * G * E, G * E);
     if (wg == 0) STAMP(p, 14);
     if (d == dself) row_self(p, hs, qcol, &misc[10]);
