@@ -1280,87 +1280,95 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     RSECT(0);
     uint64_t k1 = ~0ull, k2 = ~0ull, k3 = ~0ull, best_hm = 0;
     int best_a = 0, best_u = 0, best_q = 0;
-    {
-      for (int rd = 0; rd < rounds; ++rd) {
-        const int ai = lane + rd * 64;
-        if (ai >= PN) continue;
-        const int a = rbj * PN + ai;
-        const int *qa = qcol + a * QS;
-        const bool two_level = !General && p.cI > 0;
-        const int e = e_of[a];
-        const int u = U[a];
-        const int qrb = two_level ? qa[rb] : 0;
-        const int qf = two_level ? qa[r0 + jf] : 0;
-        if (e < 0 || u <= 0) continue;
-        const uint64_t hmf = em[e];
-        // the lightest receivers already hosting e (no slot needed)
-        uint32_t lh = ~0u;
-        uint64_t th = 0;
-        for (uint64_t h = hmf & lowm; h; h &= h - 1) {
-          const int j = __ffsll((long long)h) - 1;
-          const uint32_t L = (uint32_t)Lr[j];
-          if (L < lh) {
-            lh = L;
-            th = 0;
-          }
-          if (L == lh) th |= 1ull << j;
+    const bool two_level = !General && p.cI > 0;
+    // instance a of rb (expert e, load u, q[rb] and q[r0 + jf] of its
+    // column, hosting mask hmf of e) scored against its lightest receivers
+    auto score = [&](int a, int e, int u, int qrb, int qf, uint64_t hmf) {
+      const int *qa = qcol + a * QS;
+      // the lightest receivers already hosting e (no slot needed)
+      uint32_t lh = ~0u;
+      uint64_t th = 0;
+      for (uint64_t h = hmf & lowm; h; h &= h - 1) {
+        const int j = __ffsll((long long)h) - 1;
+        const uint32_t L = (uint32_t)Lr[j];
+        if (L < lh) {
+          lh = L;
+          th = 0;
         }
-        const uint32_t lm = lf < lh ? lf : lh;
-        if (lm == ~0u) continue;
-        const uint64_t tset = (lf == lm ? tf : 0) | (lh == lm ? th : 0);
-        const int delta = imin(u, (Lrb - (int)lm) >> 1);
-        // lowest (cost change, rt) among the lightest receivers
-        int64_t bc = INT64_MAX;
-        int bj = 0, bq = 0;
-        for (uint64_t t = tset; t; t &= t - 1) {
-          const int rtj = __ffsll((long long)t) - 1;
-          const bool hosts = (hmf >> rtj) & 1ull;
-          const int rt = r0 + rtj;
-          int64_t dcost = 0;
-          int qrt = 0;
-          if constexpr (General) {
-            // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
-            const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
-            const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
-            int rest = delta;
-            int64_t dt = 0;
-            for (int k = 0; k < R && rest > 0; ++k) {
-              const int s2 = o[k];
-              const int take = imin(rest, qa[s2]);
-              dt += (int64_t)take * (ct[s2] - cb[s2]);
-              rest -= take;
-            }
-            dcost = 2 * p.S * dt;
-            if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
-          } else {
-            if (p.cI > 0) {
-              qrt = rtj == jf ? qf : qa[rt];
-              const int m_rt = imin(delta, qrt);
-              const int rest = delta - m_rt;
-              const int m_rb = rest - imin(rest, u - qrt - qrb);
-              dcost = tokc * (int64_t)(m_rb - m_rt);
-            }
-            if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+        if (L == lh) th |= 1ull << j;
+      }
+      const uint32_t lm = lf < lh ? lf : lh;
+      if (lm == ~0u) return;
+      const uint64_t tset = (lf == lm ? tf : 0) | (lh == lm ? th : 0);
+      const int delta = imin(u, (Lrb - (int)lm) >> 1);
+      // lowest (cost change, rt) among the lightest receivers
+      int64_t bc = INT64_MAX;
+      int bj = 0, bq = 0;
+      for (uint64_t t = tset; t; t &= t - 1) {
+        const int rtj = __ffsll((long long)t) - 1;
+        const bool hosts = (hmf >> rtj) & 1ull;
+        const int rt = r0 + rtj;
+        int64_t dcost = 0;
+        int qrt = 0;
+        if constexpr (General) {
+          // fill delta from the sources in (c(s,rt) - c(s,rb), s) order
+          const uint16_t *o = gc.ord + (rbj * G + rtj) * R;
+          const int *ct = gc.ccol + rtj * R, *cb = gc.ccol + rbj * R;
+          int rest = delta;
+          int64_t dt = 0;
+          for (int k = 0; k < R && rest > 0; ++k) {
+            const int s2 = o[k];
+            const int take = imin(rest, qa[s2]);
+            dt += (int64_t)take * (ct[s2] - cb[s2]);
+            rest -= take;
           }
-          if (dcost < bc) {
-            bc = dcost;
-            bj = rtj;
-            bq = qrt;
+          dcost = 2 * p.S * dt;
+          if (!hosts) dcost += (int64_t)gc.ccol[rtj * R + (int)fdiv((uint32_t)e, p.fP)] * gc.wx[e];
+        } else {
+          if (p.cI > 0) {
+            qrt = rtj == jf ? qf : qa[rt];
+            const int m_rt = imin(delta, qrt);
+            const int rest = delta - m_rt;
+            const int m_rb = rest - imin(rest, u - qrt - qrb);
+            dcost = tokc * (int64_t)(m_rb - m_rt);
           }
+          if (!hosts) dcost += ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
         }
-        const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm;
-        const uint64_t c2 = (uint64_t)bc ^ (1ull << 63);
-        const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj);
-        if (lex_less(c1, c2, c3, k1, k2, k3)) {
-          k1 = c1;
-          k2 = c2;
-          k3 = c3;
-          best_a = a;
-          best_u = u;
-          best_hm = hmf;
-          best_q = bq;
+        if (dcost < bc) {
+          bc = dcost;
+          bj = rtj;
+          bq = qrt;
         }
       }
+      const uint64_t c1 = ((uint64_t)(uint32_t)(0x7FFFFFFF - delta) << 32) | lm;
+      const uint64_t c2 = (uint64_t)bc ^ (1ull << 63);
+      const uint64_t c3 = ((uint64_t)(uint32_t)e << 32) | (uint32_t)(r0 + bj);
+      // (c1, c2, c3) < (k1, k2, k3), with no branches
+      const bool lt = (c1 < k1) | ((c1 == k1) & ((c2 < k2) | ((c2 == k2) & (c3 < k3))));
+      k1 = lt ? c1 : k1;
+      k2 = lt ? c2 : k2;
+      k3 = lt ? c3 : k3;
+      best_a = lt ? a : best_a;
+      best_u = lt ? u : best_u;
+      best_hm = lt ? hmf : best_hm;
+      best_q = lt ? bq : best_q;
+    };
+    // one lane per instance, two instances (rounds of 64) at a time: the
+    // pair's words and hosting masks are read before either is scored, so
+    // their LDS round trips overlap (a lane's instances hold distinct
+    // experts, so the order it scores them in does not matter)
+    for (int rd = 0; rd < rounds; rd += 2) {
+      const int ai0 = lane + rd * 64, ai1 = ai0 + 64;
+      const bool v0 = ai0 < PN, v1 = ai1 < PN;
+      const int a0 = rbj * PN + (v0 ? ai0 : 0), a1 = rbj * PN + (v1 ? ai1 : 0);
+      const int *qa0 = qcol + a0 * QS, *qa1 = qcol + a1 * QS;
+      const int e0 = v0 ? e_of[a0] : -1, e1 = v1 ? e_of[a1] : -1;
+      const int u0 = v0 ? U[a0] : 0, u1 = v1 ? U[a1] : 0;
+      const int qrb0 = two_level ? qa0[rb] : 0, qf0 = two_level ? qa0[r0 + jf] : 0;
+      const int qrb1 = two_level && v1 ? qa1[rb] : 0, qf1 = two_level && v1 ? qa1[r0 + jf] : 0;
+      const uint64_t hm0 = e0 >= 0 ? em[e0] : 0, hm1 = e1 >= 0 ? em[e1] : 0;
+      if (e0 >= 0 && u0 > 0) score(a0, e0, u0, qrb0, qf0, hm0);
+      if (e1 >= 0 && u1 > 0) score(a1, e1, u1, qrb1, qf1, hm1);
     }
     RSECT(1);
     const uint64_t m1 = wave_min_u64(k1);
