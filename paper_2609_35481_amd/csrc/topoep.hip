@@ -108,6 +108,7 @@ struct Plan {
   int R, G, M, E, P, N, Neff, PN, I, self, MW, RW, nbits, rbits, cap1, nent_cap, QS;
   int cI, cX;
   int64_t S, W;
+  uint64_t tot_max;   // two-level model: the least total load out of the exact range (see out_of_range)
   int64_t n, chunk;
   int nb, n_solvers, n_helpers;
   int rchunks_all, rchunks_dom;   // routing: source-domain chunks (divisors of M)
@@ -653,8 +654,12 @@ __device__ inline bool out_of_range_cw(const Plan &p, uint64_t total, uint64_t c
   return tok + rep >= lim;
 }
 
+// The same check for the two-level model, whose c and W the host knows: with
+// k = 4 S c, 4 S total c + c W >= 2^62 holds exactly when c W >= 2^62 or
+// total >= ceil((2^62 - c W) / k), the threshold the host stores in tot_max
+// (0 when c W >= 2^62); two compares instead of overflow-checked products.
 __device__ inline bool out_of_range(const Plan &p, uint64_t total) {
-  return out_of_range_cw(p, total, (uint64_t)imax(p.cI, p.cX), (uint64_t)p.W);
+  return total > 0x7FFFFFFFull || total >= p.tot_max;
 }
 
 // Grid barrier of the per-domain solver workgroups: all of them are
@@ -3011,15 +3016,11 @@ __device__ __forceinline__ void fused_solver(const Plan &p, int *sm) {
   }
   lds_barrier();
   STAMP(p, 1);
-  // Omega's status, worked out by one thread (scalar 64-bit arithmetic that
-  // every wave would otherwise repeat on the CU's one scalar unit)
-  if (tid == 0) {
-    const uint64_t tot = *reinterpret_cast<const unsigned long long *>(t.misc + 8);
-    t.misc[45] = (int)(((uint32_t)t.misc[0] & TOPOEP_ST_NEG_LOAD) | (out_of_range(p, tot) ? TOPOEP_ST_RANGE : 0u));
-  }
-  lds_barrier();
+  // Omega's status (single_plan starts with a barrier before any thread
+  // writes these words again)
   const uint64_t total0 = uniform_u64(*reinterpret_cast<const unsigned long long *>(t.misc + 8));
-  const uint32_t gst0 = (uint32_t)uniform_i32(t.misc[45]);
+  const uint32_t gst0 = ((uint32_t)uniform_i32(t.misc[0]) & TOPOEP_ST_NEG_LOAD) |
+                        (out_of_range(p, total0) ? TOPOEP_ST_RANGE : 0u);
   const uint32_t neg0 = gst0 & TOPOEP_ST_NEG_LOAD;
   // Speculative plan from Omega as gathered while the chunks count: it is
   // the plan whenever the histogram equals row self (the gathered row is
@@ -3574,6 +3575,14 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
   q.cX = t->cost_inter;
   q.S = t->tok_bytes;
   q.W = t->expert_bytes;
+  {
+    // the two-level model's range threshold (out_of_range): exact in 128 bits
+    const unsigned __int128 lim = (unsigned __int128)1 << 62;
+    const uint64_t cm = (uint64_t)imax(imax(q.cI, q.cX), 1);
+    const unsigned __int128 rep = (unsigned __int128)(uint64_t)q.W * cm;
+    const unsigned __int128 kk = (unsigned __int128)4 * (uint64_t)q.S * cm;
+    q.tot_max = rep >= lim ? 0 : (uint64_t)((lim - rep + kk - 1) / kk);
+  }
   q.n = (int64_t)T * k;
   q.spin_limit = kSpinLimit;
   q.iter_limit = kIterLimit;

@@ -427,6 +427,27 @@ def test_range_bit():
     assert got["status"] & topoep.ST_RANGE
 
 
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("W", [0, 3 << 40])
+def test_range_threshold(solver, W):
+    """Both sides of the exact-range limit 4 S total c + c W < 2^62: the
+    largest S that keeps a plan in range, and one more (RANGE), against the
+    oracle's own overflow-checked products."""
+    cfg, gl, tk = _tiny()
+    g = gl.astype(np.int64).copy()
+    g[0] = np.bincount(tk[(tk >= 0) & (tk < cfg.E)], minlength=cfg.E)   # row self of Omega'
+    total = int(g[g > 0].sum())
+    cI, cX = 1, 4
+    x = 4 * cX * total
+    s_in = ((1 << 62) - cX * W - 1) // x
+    got, _ = both(cfg.R, cfg.G, cfg.E, 0, cI, cX, s_in, W, 1, gl, tk, launch=SOLVERS[solver],
+                  what="range threshold, S in range (%s)" % solver)
+    assert not got["status"] & topoep.ST_RANGE
+    got, _ = both(cfg.R, cfg.G, cfg.E, 0, cI, cX, s_in + 1, W, 1, gl, tk, launch=SOLVERS[solver],
+                  what="range threshold, S one past (%s)" % solver)
+    assert got["status"] & topoep.ST_RANGE
+
+
 def test_many_domains_more_than_solver_groups():
     """M = 256 domains (G = 1): solver workgroups loop over several domains."""
     rng = np.random.default_rng(11)
