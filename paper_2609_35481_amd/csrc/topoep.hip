@@ -933,7 +933,9 @@ __device__ inline int row_max_all_i32(int v) {
 // j's load and used slots; only the q columns stay in LDS.  It makes the
 // same moves in the same order as the LDS form (the busiest rank rb, lowest
 // index on ties; one lane per instance of rb scoring its lightest
-// receivers; the minimum of (delta descending, L[rt], cost change, e, rt);
+// receivers, or with at most four instances per rank one row of 16 lanes
+// per instance, a lane per target rank; the minimum of (delta descending,
+// L[rt], cost change, e, rt);
 // the transfer from rt's own assignments, then the other sources
 // ascending, rb's own last), as straight-line vector code with few scalar
 // hand-overs (see vlane and vb).  e_of, U, Lr, used, slots, em and the q
@@ -947,7 +949,10 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
   const bool two_level = p.cI > 0;
   const int64_t tokc = 2 * p.S * (int64_t)p.cI;
   const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
-  const bool one_row = PN <= 16;
+  // rb's instances one per lane, or (at most four of them, pairs) one per
+  // row of 16 lanes, a lane per target rank
+  const bool pairs = PN <= 4;
+  const bool one_row = pairs ? PN <= 1 : PN <= 16;
   const int vl = vgpr(lane);
   const int rank_lane = vb(vl < G), rb_lane = vb(vl < PN), src_lane = vb(vl < R);
   // instance registers: lane l holds instances l and l + 64
@@ -972,63 +977,107 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
     const uint32_t lf = (uint32_t)vlane((int)row_min_all_u32(fr ? (uint32_t)lj : ~0u), 0);
     const uint32_t tfm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr & vb((uint32_t)lj == lf)));
     const uint32_t lightm = (uint32_t)vgpr((int)(uint32_t)__ballot(low & vb((uint32_t)lj <= lf)));
+    const uint32_t lowm = (uint32_t)vgpr((int)(uint32_t)__ballot(low)), frm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr));
     RSECT(0);
-    // ---- lane c < PN: rb's instance a = rbj PN + c, its fields from the lane
-    // holding it
-    const int a = rbj * PN + vl;
-    const int src = (a & 63) << 2;
-    const int e0 = __builtin_amdgcn_ds_bpermute(src, ie0), e1 = __builtin_amdgcn_ds_bpermute(src, ie1);
-    const int u0 = __builtin_amdgcn_ds_bpermute(src, iu0), u1 = __builtin_amdgcn_ds_bpermute(src, iu1);
-    const int h0 = __builtin_amdgcn_ds_bpermute(src, (int)ih0), h1 = __builtin_amdgcn_ds_bpermute(src, (int)ih1);
-    const int *qa = qcol + (rb_lane ? a : 0) * QS;
-    const int qrb = two_level ? qa[rb] : 0;
-    const int hi = vb(a >= 64);
-    const int e = hi ? e1 : e0, u = hi ? u1 : u0;
-    const uint32_t hm = (uint32_t)(hi ? h1 : h0);
-    const int cand = rb_lane & vb(e >= 0) & vb(u > 0);
-    // the lightest receivers hosting e, no heavier than the free level
-    const uint32_t hl = cand ? hm & lightm : 0u;
-    uint32_t lh = ~0u, th = 0u;
-    if (__ballot(hl != 0u)) {
-#pragma unroll
-      for (int j = 0; j < GM; ++j) {
-        const uint32_t Lj = (uint32_t)__builtin_amdgcn_readlane(lj, j);
-        const uint32_t c = (hl >> j) & 1u ? Lj : ~0u;
-        th = c < lh ? 1u << j : (c == lh ? th | (1u << j) : th);
-        lh = c < lh ? c : lh;
-      }
-    }
-    const uint32_t lm = lf < lh ? lf : lh;
-    const int valid = cand & vb(lm != ~0u);
-    const uint32_t tset = valid ? ((lf == lm ? tfm : 0u) | (lh == lm ? th : 0u)) : 0u;
-    const int delta = imin(u, (Lrb - (int)lm) >> 1);
-    // ---- cost change at each target of tset, lowest (cost, rt) kept
-    auto cost_at = [&](int jt, int &qt) {
+    // ---- the candidates: a scored lane's instance of rb (expert e, load u,
+    // hosting mask hm), its lightest receiver level lm, delta, and its best
+    // target bj with that target's cost change bc and q column word bq
+    int e, u, valid, delta, bj, bq;
+    uint32_t hm, lm;
+    int64_t bc;
+    if (pairs) {
+      // lane 16 c + j: rb's instance c (a = rbj PN + c) against local rank
+      // j; the row of 16 lanes of instance c keeps its lightest receivers
+      // (low ranks with a free slot or already hosting e), which are its
+      // targets, each scored by one lane
+      const int c = vl >> 4, jj = vl & 15;
+      const int a = rbj * PN + c;
+      const int src = (a & 63) << 2;
+      const int e0 = __builtin_amdgcn_ds_bpermute(src, ie0), e1 = __builtin_amdgcn_ds_bpermute(src, ie1);
+      const int u0 = __builtin_amdgcn_ds_bpermute(src, iu0), u1 = __builtin_amdgcn_ds_bpermute(src, iu1);
+      const int h0 = __builtin_amdgcn_ds_bpermute(src, (int)ih0), h1 = __builtin_amdgcn_ds_bpermute(src, (int)ih1);
+      const int Lq = __builtin_amdgcn_ds_bpermute(jj << 2, lj);   // rank jj's load (-1 from G on)
+      const int *qa = qcol + (c < PN ? a : 0) * QS;
+      const int qrb = two_level ? qa[rb] : 0;
+      const int qt = two_level ? qa[r0 + (jj < G ? jj : 0)] : 0;
+      const int hi = vb(a >= 64);
+      e = hi ? e1 : e0;
+      u = hi ? u1 : u0;
+      hm = (uint32_t)(hi ? h1 : h0);
+      const int cand = vb(c < PN) & vb(e >= 0) & vb(u > 0);
+      const int hostj = (int)((hm >> jj) & 1u);
+      const int ok = cand & (int)((lowm >> jj) & 1u) & ((int)((frm >> jj) & 1u) | hostj);
+      lm = row_min_all_u32(ok ? (uint32_t)Lq : ~0u);
+      valid = ok & vb((uint32_t)Lq == lm);
+      delta = imin(u, (Lrb - (int)lm) >> 1);
       int64_t dc = 0;
-      qt = 0;
       if (two_level) {
-        qt = qa[r0 + jt];
         const int m_rt = imin(delta, qt);
         const int rest = delta - m_rt;
         const int m_rb = rest - imin(rest, u - qt - qrb);
         dc = tokc * (int64_t)(m_rb - m_rt);
       }
-      const int64_t rep = ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
-      return ((hm >> jt) & 1u) ? dc : dc + rep;
-    };
-    int bj = valid ? __ffs(tset) - 1 : 0;
-    int bq;
-    int64_t bc = cost_at(bj, bq);
-    const uint32_t more = tset & (tset - 1u);
-    if (__ballot(more != 0u)) {
-      for (uint32_t t = more; t; t &= t - 1u) {
-        const int jt = __ffs(t) - 1;
-        int qt;
-        const int64_t dc = cost_at(jt, qt);
-        if (dc < bc) {
-          bc = dc;
-          bj = jt;
-          bq = qt;
+      bc = hostj ? dc : dc + (((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX);
+      bj = jj;
+      bq = qt;
+    } else {
+      // ---- lane c < PN: rb's instance a = rbj PN + c, its fields from the lane
+      // holding it
+      const int a = rbj * PN + vl;
+      const int src = (a & 63) << 2;
+      const int e0 = __builtin_amdgcn_ds_bpermute(src, ie0), e1 = __builtin_amdgcn_ds_bpermute(src, ie1);
+      const int u0 = __builtin_amdgcn_ds_bpermute(src, iu0), u1 = __builtin_amdgcn_ds_bpermute(src, iu1);
+      const int h0 = __builtin_amdgcn_ds_bpermute(src, (int)ih0), h1 = __builtin_amdgcn_ds_bpermute(src, (int)ih1);
+      const int *qa = qcol + (rb_lane ? a : 0) * QS;
+      const int qrb = two_level ? qa[rb] : 0;
+      const int hi = vb(a >= 64);
+      e = hi ? e1 : e0;
+      u = hi ? u1 : u0;
+      hm = (uint32_t)(hi ? h1 : h0);
+      const int cand = rb_lane & vb(e >= 0) & vb(u > 0);
+      // the lightest receivers hosting e, no heavier than the free level
+      const uint32_t hl = cand ? hm & lightm : 0u;
+      uint32_t lh = ~0u, th = 0u;
+      if (__ballot(hl != 0u)) {
+#pragma unroll
+        for (int j = 0; j < GM; ++j) {
+          const uint32_t Lj = (uint32_t)__builtin_amdgcn_readlane(lj, j);
+          const uint32_t c = (hl >> j) & 1u ? Lj : ~0u;
+          th = c < lh ? 1u << j : (c == lh ? th | (1u << j) : th);
+          lh = c < lh ? c : lh;
+        }
+      }
+      lm = lf < lh ? lf : lh;
+      valid = cand & vb(lm != ~0u);
+      const uint32_t tset = valid ? ((lf == lm ? tfm : 0u) | (lh == lm ? th : 0u)) : 0u;
+      delta = imin(u, (Lrb - (int)lm) >> 1);
+      // ---- cost change at each target of tset, lowest (cost, rt) kept
+      auto cost_at = [&](int jt, int &qt) {
+        int64_t dc = 0;
+        qt = 0;
+        if (two_level) {
+          qt = qa[r0 + jt];
+          const int m_rt = imin(delta, qt);
+          const int rest = delta - m_rt;
+          const int m_rb = rest - imin(rest, u - qt - qrb);
+          dc = tokc * (int64_t)(m_rb - m_rt);
+        }
+        const int64_t rep = ((int)fdiv((uint32_t)e, p.fGP) == d) ? repI : repX;
+        return ((hm >> jt) & 1u) ? dc : dc + rep;
+      };
+      bj = valid ? __ffs(tset) - 1 : 0;
+      bc = cost_at(bj, bq);
+      const uint32_t more = tset & (tset - 1u);
+      if (__ballot(more != 0u)) {
+        for (uint32_t t = more; t; t &= t - 1u) {
+          const int jt = __ffs(t) - 1;
+          int qt;
+          const int64_t dc = cost_at(jt, qt);
+          if (dc < bc) {
+            bc = dc;
+            bj = jt;
+            bq = qt;
+          }
         }
       }
     }
@@ -1073,7 +1122,7 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
     const int uw = vlane(u, wl);
     const int qrt = vlane(bq, wl);
     const uint32_t hw = (uint32_t)vlane((int)hm, wl);
-    const int aw_s = rbj_s * PN + wl;
+    const int aw_s = rbj_s * PN + (pairs ? wl >> 4 : wl);
     const int aw = vgpr(aw_s);
     const int fresh = vb(((hw >> rtj) & 1u) == 0u);
     RSECT(2);
