@@ -887,8 +887,14 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 // Forms of the refinement loop: the register form where the domain fits it
 // (refine_in_registers), else the LDS form; a kernel that knows its form
 // carries only that one's code.
-constexpr int kRefineAny = 0, kRefineReg = 1, kRefineLds = 2;
+constexpr int kRefineAny = 0, kRefineReg = 1, kRefineLds = 2, kRefinePairs = 3;
 __host__ __device__ inline bool refine_in_registers(int G, int I, int PN) { return G <= 16 && I <= 128 && PN <= 64; }
+// the register form scoring (instance, target) pairs: at most four instances
+// per rank (a row of 16 lanes each)
+__host__ __device__ inline bool refine_in_pairs(int G, int I, int PN) { return refine_in_registers(G, I, PN) && PN <= 4; }
+__host__ __device__ inline int refine_form(int G, int I, int PN) {
+  return refine_in_pairs(G, I, PN) ? kRefinePairs : (refine_in_registers(G, I, PN) ? kRefineReg : kRefineLds);
+}
 
 // Minimum over each row of 16 lanes, left in every lane of the row.
 __device__ inline uint32_t row_min_all_u32(uint32_t v) {
@@ -940,7 +946,7 @@ __device__ inline int row_max_all_i32(int v) {
 // ascending, rb's own last), as straight-line vector code with few scalar
 // hand-overs (see vlane and vb).  e_of, U, Lr, used, slots, em and the q
 // columns hold the final state on return.
-template <int GM>
+template <int GM, bool Pairs>
 __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                       int *Lr, uint64_t *em, uint32_t *flags) {
   const int lane = lane_id();
@@ -951,7 +957,7 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
   const int64_t repI = (int64_t)p.cI * p.W, repX = (int64_t)p.cX * p.W;
   // rb's instances one per lane, or (at most four of them, pairs) one per
   // row of 16 lanes, a lane per target rank
-  const bool pairs = PN <= 4;
+  constexpr bool pairs = Pairs;
   const bool one_row = pairs ? PN <= 1 : PN <= 16;
   const int vl = vgpr(lane);
   const int rank_lane = vb(vl < G), rb_lane = vb(vl < PN), src_lane = vb(vl < R);
@@ -977,7 +983,6 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
     const uint32_t lf = (uint32_t)vlane((int)row_min_all_u32(fr ? (uint32_t)lj : ~0u), 0);
     const uint32_t tfm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr & vb((uint32_t)lj == lf)));
     const uint32_t lightm = (uint32_t)vgpr((int)(uint32_t)__ballot(low & vb((uint32_t)lj <= lf)));
-    const uint32_t lowm = (uint32_t)vgpr((int)(uint32_t)__ballot(low)), frm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr));
     RSECT(0);
     // ---- the candidates: a scored lane's instance of rb (expert e, load u,
     // hosting mask hm), its lightest receiver level lm, delta, and its best
@@ -985,11 +990,12 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
     int e, u, valid, delta, bj, bq;
     uint32_t hm, lm;
     int64_t bc;
-    if (pairs) {
+    if constexpr (pairs) {
       // lane 16 c + j: rb's instance c (a = rbj PN + c) against local rank
       // j; the row of 16 lanes of instance c keeps its lightest receivers
       // (low ranks with a free slot or already hosting e), which are its
       // targets, each scored by one lane
+      const uint32_t lowm = (uint32_t)vgpr((int)(uint32_t)__ballot(low)), frm = (uint32_t)vgpr((int)(uint32_t)__ballot(fr));
       const int c = vl >> 4, jj = vl & 15;
       const int a = rbj * PN + c;
       const int src = (a & 63) << 2;
@@ -1250,7 +1256,8 @@ __device__ uint32_t refine_domain_reg(const Plan &p, int d, int *e_of, int *U, i
 template <bool General = false, int Form = kRefineAny>
 __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *qcol, int *slots, int *used,
                                   int *Lr, uint64_t *em, uint32_t *flags, bool prepared, GenCost gc = GenCost{}) {
-  static_assert(!(General && Form == kRefineReg), "the register form scores the two-level cost only");
+  static_assert(!(General && (Form == kRefineReg || Form == kRefinePairs)),
+                "the register form scores the two-level cost only");
   const int lane = lane_id();
   const int G = p.G, PN = p.PN, R = p.R, P = p.P, Neff = p.Neff, QS = p.QS, E = p.E, I = p.I;
   if (G < 2) return 0;
@@ -1280,13 +1287,19 @@ __device__ uint32_t refine_domain(const Plan &p, int d, int *e_of, int *U, int *
     }
   }
   wave_sync();
-  if constexpr (!General && Form != kRefineLds) {
+  // (the pairs variant only where the kernel was built for it: the
+  // one-launch plan's; the three-kernel solvers keep one register variant)
+  if constexpr (!General && Form == kRefinePairs) {
+    return G <= 8 ? refine_domain_reg<8, true>(p, d, e_of, U, qcol, slots, used, Lr, em, flags)
+                  : refine_domain_reg<16, true>(p, d, e_of, U, qcol, slots, used, Lr, em, flags);
+  }
+  if constexpr (!General && (Form == kRefineReg || Form == kRefineAny)) {
     if (Form == kRefineReg || refine_in_registers(G, I, PN)) {
-      return G <= 8 ? refine_domain_reg<8>(p, d, e_of, U, qcol, slots, used, Lr, em, flags)
-                    : refine_domain_reg<16>(p, d, e_of, U, qcol, slots, used, Lr, em, flags);
+      return G <= 8 ? refine_domain_reg<8, false>(p, d, e_of, U, qcol, slots, used, Lr, em, flags)
+                    : refine_domain_reg<16, false>(p, d, e_of, U, qcol, slots, used, Lr, em, flags);
     }
   }
-  if constexpr (Form == kRefineReg) {
+  if constexpr (Form == kRefineReg || Form == kRefinePairs) {
     return 0;   // (not reached: the host picks the register form only where it applies)
   } else {
   // One lane per instance of rb.  Among the targets an instance may move to
@@ -3502,17 +3515,17 @@ __device__ __forceinline__ void fused_chunk(const Plan &p, int b, int *sm) {
 // The whole plan in one launch: workgroup 0 solves, workgroups 1..nb hold
 // the ids; all are resident at once (nb <= kMaxFusedBlocks) and every wait
 // is bounded.
-// Reg: the refinement runs in registers (refine_in_registers holds for the
-// shape), else in LDS; one instantiation each keeps the other's registers
-// out.
-template <int IPT, bool Reg>
+// Form: the refinement's form for the shape (refine_form: registers with
+// (instance, target) pairs, registers, or LDS); one instantiation each keeps
+// the others' registers out.
+template <int IPT, int Form>
 __global__ __launch_bounds__(1024) void plan_fused_kernel(Plan p) {
   extern __shared__ int64_t smem_f[];
   int *sm = reinterpret_cast<int *>(smem_f);
   (void)p;
   if (blockIdx.x == 0) {
     const Plan q = solver_plan(role_plan(p));
-    fused_solver<Reg ? kRefineReg : kRefineLds>(q, sm);
+    fused_solver<Form>(q, sm);
   } else {
     const Plan q = role_plan(p);
     fused_chunk<IPT>(q, blockIdx.x - 1, sm);
@@ -3587,7 +3600,7 @@ int resident_capacity(const void *fn, int threads, size_t lds) {
   return cap;
 }
 
-const void *fused_fn(int ipt, bool reg);
+const void *fused_fn(int ipt, int form);
 
 // Validate the arguments and fill the plan's sizes, launch shape and
 // workspace layout (pointers are offsets when ws == nullptr).
@@ -3692,7 +3705,7 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
     bool fused_ok = single_fits && ipt > 0 && fused_words * 4 + 1024 <= kLdsLimit;
     // every workgroup of the launch resident at once (they wait on each other)
     if (fused_ok)
-      fused_ok = nbf + 1 <= resident_capacity(fused_fn(ipt, refine_in_registers(q.G, q.I, q.PN)), st, (size_t)fused_words * 4);
+      fused_ok = nbf + 1 <= resident_capacity(fused_fn(ipt, refine_form(q.G, q.I, q.PN)), st, (size_t)fused_words * 4);
     if (solver == 3 && !fused_ok) return TOPOEP_ELIMIT;
     if (general && solver == 3) return TOPOEP_EINVAL;   // the general model runs the per-domain solver
     if (fused_ok && !general && (solver == 3 || solver == 0)) {
@@ -3820,16 +3833,19 @@ int setup(const topoep_topology *t, int32_t T, int32_t k, int32_t N, const topoe
 
 std::atomic<bool> g_attrs_set{false};
 
-const void *fused_fn(int ipt, bool reg) {
+template <int IPT>
+const void *fused_fn_ipt(int form) {
+  return form == kRefinePairs ? reinterpret_cast<const void *>(plan_fused_kernel<IPT, kRefinePairs>)
+         : form == kRefineReg ? reinterpret_cast<const void *>(plan_fused_kernel<IPT, kRefineReg>)
+                              : reinterpret_cast<const void *>(plan_fused_kernel<IPT, kRefineLds>);
+}
+
+const void *fused_fn(int ipt, int form) {
   switch (ipt) {
-    case 1: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<1, true>)
-                       : reinterpret_cast<const void *>(plan_fused_kernel<1, false>);
-    case 2: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<2, true>)
-                       : reinterpret_cast<const void *>(plan_fused_kernel<2, false>);
-    case 4: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<4, true>)
-                       : reinterpret_cast<const void *>(plan_fused_kernel<4, false>);
-    default: return reg ? reinterpret_cast<const void *>(plan_fused_kernel<8, true>)
-                        : reinterpret_cast<const void *>(plan_fused_kernel<8, false>);
+    case 1: return fused_fn_ipt<1>(form);
+    case 2: return fused_fn_ipt<2>(form);
+    case 4: return fused_fn_ipt<4>(form);
+    default: return fused_fn_ipt<8>(form);
   }
 }
 
@@ -3846,14 +3862,18 @@ void set_attrs() {
   allow_lds(solve_kernel<512>);
   allow_lds(solve_kernel<1024>);
   allow_lds(solve_single_kernel);
-  allow_lds(plan_fused_kernel<1, false>);
-  allow_lds(plan_fused_kernel<1, true>);
-  allow_lds(plan_fused_kernel<2, false>);
-  allow_lds(plan_fused_kernel<2, true>);
-  allow_lds(plan_fused_kernel<4, false>);
-  allow_lds(plan_fused_kernel<4, true>);
-  allow_lds(plan_fused_kernel<8, false>);
-  allow_lds(plan_fused_kernel<8, true>);
+  allow_lds(plan_fused_kernel<1, kRefineLds>);
+  allow_lds(plan_fused_kernel<1, kRefineReg>);
+  allow_lds(plan_fused_kernel<1, kRefinePairs>);
+  allow_lds(plan_fused_kernel<2, kRefineLds>);
+  allow_lds(plan_fused_kernel<2, kRefineReg>);
+  allow_lds(plan_fused_kernel<2, kRefinePairs>);
+  allow_lds(plan_fused_kernel<4, kRefineLds>);
+  allow_lds(plan_fused_kernel<4, kRefineReg>);
+  allow_lds(plan_fused_kernel<4, kRefinePairs>);
+  allow_lds(plan_fused_kernel<8, kRefineLds>);
+  allow_lds(plan_fused_kernel<8, kRefineReg>);
+  allow_lds(plan_fused_kernel<8, kRefinePairs>);
   allow_lds(empty_kernel);
   // (an attribute a kernel refuses must not linger as the caller's error)
   (void)hipGetLastError();
@@ -3887,19 +3907,20 @@ void launch_solve(const Plan &p, const Shape &s, hipStream_t st) {
 }
 
 template <int IPT>
-void launch_fused_ipt(bool reg, dim3 g, dim3 b, size_t lds, hipStream_t st, const Plan &p) {
-  if (reg) hipLaunchKernelGGL((plan_fused_kernel<IPT, true>), g, b, lds, st, p);
-  else hipLaunchKernelGGL((plan_fused_kernel<IPT, false>), g, b, lds, st, p);
+void launch_fused_ipt(int form, dim3 g, dim3 b, size_t lds, hipStream_t st, const Plan &p) {
+  if (form == kRefinePairs) hipLaunchKernelGGL((plan_fused_kernel<IPT, kRefinePairs>), g, b, lds, st, p);
+  else if (form == kRefineReg) hipLaunchKernelGGL((plan_fused_kernel<IPT, kRefineReg>), g, b, lds, st, p);
+  else hipLaunchKernelGGL((plan_fused_kernel<IPT, kRefineLds>), g, b, lds, st, p);
 }
 
 void launch_fused(const Plan &p, const Shape &s, hipStream_t st) {
   const dim3 g(p.nb + 1), b(s.st);
-  const bool reg = refine_in_registers(p.G, p.I, p.PN);
+  const int form = refine_form(p.G, p.I, p.PN);
   switch (s.ipt) {
-    case 1: launch_fused_ipt<1>(reg, g, b, s.lds_fused, st, p); break;
-    case 2: launch_fused_ipt<2>(reg, g, b, s.lds_fused, st, p); break;
-    case 4: launch_fused_ipt<4>(reg, g, b, s.lds_fused, st, p); break;
-    default: launch_fused_ipt<8>(reg, g, b, s.lds_fused, st, p); break;
+    case 1: launch_fused_ipt<1>(form, g, b, s.lds_fused, st, p); break;
+    case 2: launch_fused_ipt<2>(form, g, b, s.lds_fused, st, p); break;
+    case 4: launch_fused_ipt<4>(form, g, b, s.lds_fused, st, p); break;
+    default: launch_fused_ipt<8>(form, g, b, s.lds_fused, st, p); break;
   }
 }
 

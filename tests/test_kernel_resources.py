@@ -81,8 +81,9 @@ def test_every_kernel_is_in_the_library(kernels):
     for part in ("plan_fused_kernel", "solve_kernel", "solve_single_kernel", "hist_kernel", "reroute_kernel",
                  "empty_kernel"):
         assert part in names, part
-    # the one-launch kernel: 4 id widths x 2 refinement forms (registers, LDS)
-    assert sum("plan_fused_kernel" in k[0] for k in kernels) == 8
+    # the one-launch kernel: 4 id widths x 3 refinement forms (registers with
+    # (instance, target) pairs, registers, LDS)
+    assert sum("plan_fused_kernel" in k[0] for k in kernels) == 12
     # the dispatch layout and the replica gather sources add their own
     assert len(kernels) > 20
 
