@@ -885,8 +885,9 @@ __device__ inline int instance_of(const Plan &p, int d, int j, int e, const int 
 }
 
 // Forms of the refinement loop: the register form where the domain fits it
-// (refine_in_registers), else the LDS form; a kernel that knows its form
-// carries only that one's code.
+// (refine_in_registers), scoring (instance, target) pairs when a rank has
+// at most four instances (refine_in_pairs; one-launch kernel only), else
+// the LDS form; a kernel that knows its form carries only that one's code.
 constexpr int kRefineAny = 0, kRefineReg = 1, kRefineLds = 2, kRefinePairs = 3;
 __host__ __device__ inline bool refine_in_registers(int G, int I, int PN) { return G <= 16 && I <= 128 && PN <= 64; }
 // the register form scoring (instance, target) pairs: at most four instances
