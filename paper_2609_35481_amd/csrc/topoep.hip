@@ -2419,16 +2419,22 @@ __device__ __forceinline__ void fast_finish(const Plan &p, const SingleState &t,
     for (int b = 0; b < (E + 63) >> 6; ++b) all += wt[b];
     p.csr_ptr[E] = all;
   }
-  // replica slots: slot t of local rank j of domain d holds stage-1 entry
-  // t G + j (entries are a prefix of the domain's list)
+  lds_barrier();
+  STAMP(p, 30);
+}
+
+// The lean finish's replica slots and send counts, for the caller alone (no
+// chunk reads them, so they go out after the flags): slot t of local rank j
+// of domain d holds stage-1 entry t G + j (entries are a prefix of the
+// domain's list).
+__device__ __forceinline__ void fast_outputs(const Plan &p, const SingleState &t) {
+  const int tid = threadIdx.x, nt = blockDim.x, G = p.G, R = p.R, cap = p.cap1;
   for (int i = tid; i < R * p.N; i += nt) {
     const int r = (int)fdiv((uint32_t)i, p.fN), s2 = i - r * p.N;
     const int d = (int)fdiv((uint32_t)r, p.fG), j = r - d * G;
-    p.slots_out[i] = s2 < p.Neff ? repl[d * cap + s2 * G + j] : -1;
+    p.slots_out[i] = s2 < p.Neff ? t.repl[d * cap + s2 * G + j] : -1;
   }
-  lds_barrier();
-  STAMP(p, 30);
-  for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
+  for (int r = tid; r < R; r += nt) p.send_out[r] = t.sendl[r];
 }
 
 // Every step after the load: with Omega' in om (row self = the histogram hs)
@@ -2439,6 +2445,8 @@ __device__ __forceinline__ void fast_finish(const Plan &p, const SingleState &t,
 struct NoHook {
   __device__ void operator()() const {}
 };
+template <class H> struct IsNoHook { static constexpr bool value = false; };
+template <> struct IsNoHook<NoHook> { static constexpr bool value = true; };
 
 template <int Form = kRefineAny, class Published = NoHook>
 __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t, uint32_t gst, bool or_status,
@@ -2483,11 +2491,17 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
       if (tid == 0) {
         const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
         p.ctrl[kCtrlFinal] = fin;
+        misc[45] = (int)fin;   // (kept in LDS past the hook)
+      }
+      published();
+      // the caller's outputs (no chunk reads them)
+      fast_outputs(p, t);
+      if (tid == 0) {
+        const uint32_t fin = (uint32_t)misc[45];
         if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
         else p.status_out[0] = (int32_t)fin;
         p.status_out[1] = 0;
       }
-      published();
       return;
     }
   }
@@ -2586,23 +2600,46 @@ __device__ __forceinline__ void single_plan(const Plan &p, const SingleState &t,
   }
 
   STAMP(p, 5);
-  // ---- outputs: replica slots, send counts, this rank's instance list
-  for (int i = tid; i < R * p.N; i += nt) {
-    const int r = (int)fdiv((uint32_t)i, p.fN), t2 = i - r * p.N;
-    p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
+  // ---- outputs: replica slots, send counts, this rank's instance list and
+  // the final status.  With a hook (the one-launch plan, whose chunks read
+  // only the list and the final status word) the caller's outputs wait
+  // until the hook has released the chunks.
+  constexpr bool defer = !IsNoHook<Published>::value;
+  auto caller_outputs = [&]() {
+    for (int i = tid; i < R * p.N; i += nt) {
+      const int r = (int)fdiv((uint32_t)i, p.fN), t2 = i - r * p.N;
+      p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
+    }
+    for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
+    if (tid == 0) {
+      const uint32_t fin = (uint32_t)misc[45];
+      if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
+      else p.status_out[0] = (int32_t)fin;
+      p.status_out[1] = misc[12];
+    }
+  };
+  if constexpr (!defer) {
+    for (int i = tid; i < R * p.N; i += nt) {
+      const int r = (int)fdiv((uint32_t)i, p.fN), t2 = i - r * p.N;
+      p.slots_out[i] = t2 < used[r] ? slots[r * Neff + t2] : -1;
+    }
+    for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
   }
-  for (int r = tid; r < R; r += nt) p.send_out[r] = sendl[r];
   STAMP(p, 6);
   emit_instance_list(p, qcol, slots, used, bm, t.wt);
   STAMP(p, 7);
   if (tid == 0) {
     const uint32_t fin = (uint32_t)misc[0] | (gst & TOPOEP_ST_RANGE);
     p.ctrl[kCtrlFinal] = fin;
-    if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
-    else p.status_out[0] = (int32_t)fin;
-    p.status_out[1] = misc[12];
+    misc[45] = (int)fin;   // (kept in LDS past the hook)
+    if constexpr (!defer) {
+      if (or_status) atomicOr(reinterpret_cast<unsigned *>(p.status_out), fin);
+      else p.status_out[0] = (int32_t)fin;
+      p.status_out[1] = misc[12];
+    }
   }
   published();
+  if constexpr (defer) caller_outputs();
 }
 
 // Receive counts from the single-workgroup solver's final LDS state (after
