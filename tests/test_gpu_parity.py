@@ -448,6 +448,18 @@ def test_range_threshold(solver, W):
     assert got["status"] & topoep.ST_RANGE
 
 
+@pytest.mark.parametrize("solver", sorted(SOLVERS))
+@pytest.mark.parametrize("W", [1 << 60, (1 << 60) - 1])
+def test_range_expert_bytes_at_the_bound(solver, W):
+    """c W at 2^62 (every plan out of range, whatever S) and just below it
+    (every plan with a positive load out of range: the bound leaves room
+    for no assignment), against the oracle."""
+    cfg, gl, tk = _tiny()
+    got, _ = both(cfg.R, cfg.G, cfg.E, 0, 1, 4, 1, W, 1, gl, tk, launch=SOLVERS[solver],
+                  what="range at the expert-bytes bound W=%d (%s)" % (W, solver))
+    assert got["status"] & topoep.ST_RANGE
+
+
 def test_many_domains_more_than_solver_groups():
     """M = 256 domains (G = 1): solver workgroups loop over several domains."""
     rng = np.random.default_rng(11)
